@@ -1,0 +1,182 @@
+/*
+ * spconv.h -- C-ABI of the MI355X (gfx950) sparse-convolution layer library.
+ *
+ * A sparse convolution (Section 2.1, Eq. 1 and Eq. 2) runs in two steps
+ * (Section 2.2): the Map step builds the kernel map (Eq. 3) and the
+ * Gather-GEMM-Scatter (GMaS) step applies it to the features.
+ *
+ *   spconv_build_map   Map step: sorted coordinates, output coordinates (Eq. 1),
+ *                      segmented query sorting (Section 5.1.1) and the
+ *                      double-traversed binary search (Section 5.1.2).
+ *   spconv_forward     GMaS step: metadata tables, autotunable-tile Gather
+ *                      (Algorithm 1), reordered and grouped per-offset GEMMs on
+ *                      MFMA (Section 5.2.2) and Scatter (Section 2.2, Step 2).
+ *   spconv_free_map    releases a map's host object.
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers named d_* are DEVICE pointers, h_* HOST pointers.  The caller owns
+ *     and allocates every buffer, including both workspaces; the library never
+ *     allocates device memory.  `stream` is a hipStream_t (NULL = default stream).
+ *   - Coordinates are int32 [n][4] rows (b, x, y, z); b is the batch index and is
+ *     never offset.  Input coordinates must be unique (the paper's point cloud is
+ *     a set, Section 2.1).
+ *   - Weight offsets follow Delta(K, t) of Section 2.1: offset k = ix K^2 + iy K + iz
+ *     (ix, iy, iz in [0, K)) is t * (ix - c, iy - c, iz - c) with c = (K-1)/2 for odd
+ *     K and c = 0 for even K; t is the input coordinate spacing ("tensor stride").
+ *   - Functions return SPCONV_OK (0) or a negative spconv_status; the message of
+ *     the last failure on the calling thread is spconv_last_error().  Nothing
+ *     aborts and no C++ exception crosses the ABI.
+ */
+#ifndef SPCONV_H
+#define SPCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPCONV_OK = 0,
+  SPCONV_EINVAL = -1,      /* bad argument (K <= 0, stride, mode, NULL pointer, ...) */
+  SPCONV_ERANGE = -2,      /* coordinates (plus kernel reach) do not fit a 62-bit key */
+  SPCONV_EDUP = -3,        /* repeated input (or, for SPCONV_UP, output) coordinate */
+  SPCONV_ENOSPC = -4,      /* workspace smaller than the *_workspace_bytes() figure */
+  SPCONV_EHIP = -5,        /* a HIP runtime call failed, or a device-side check did */
+  SPCONV_EUNSUPPORTED = -6 /* dtype / channel count / kernel size not supported */
+} spconv_status;
+
+typedef enum {
+  SPCONV_SUBM = 0, /* stride 1, outputs are the inputs, same rows (Section 2.1: s = 1 gives Q = P) */
+  SPCONV_DOWN = 1, /* outputs Q = unique(floor(p / (t s)) (t s)) (Eq. 1), sorted by (b, x, y, z) */
+  SPCONV_UP = 2    /* transposed (upsampling) conv: the DOWN map of the given fine outputs with
+                      input and output roles swapped */
+} spconv_mode;
+
+typedef enum { SPCONV_F32 = 0, SPCONV_F16 = 1, SPCONV_BF16 = 2 } spconv_dtype;
+
+typedef enum {
+  SPCONV_GROUP_RAGGED = 0, /* one grouped launch over all offsets, no padding rows */
+  SPCONV_GROUP_SORTED = 1, /* Section 5.2.2: offsets sorted by pair count, adjacent
+                              ones grouped, each group padded to its largest member */
+  SPCONV_GROUP_MAPORDER = 2 /* prior-art grouping in Map (offset) order, for comparison */
+} spconv_grouping;
+
+/* Tunables; any field left 0 takes its default.  The Map-step fields are the
+ * hyperparameters of Section 5.1.4 (B = source-block size, C = query-block
+ * limit); the GMaS fields are the Gather / Scatter tile sizes of Algorithm 1
+ * (channels per thread) and the GEMM grouping of Section 5.2.2. */
+typedef struct {
+  int B;             /* source block size, power of two in [64, 4096]; default 256 */
+  int Cq;            /* query block limit (the paper's C), multiple of 256; default 512 */
+  int t_gather;      /* gather tile T in channels; must divide c_in; default: tuned rule */
+  int t_scatter;     /* scatter tile T in channels; must divide c_out; default: tuned rule */
+  int grouping;      /* spconv_grouping + 1 (0 = default SPCONV_GROUP_RAGGED) */
+  int partial_dtype; /* output-buffer (GEMM partial) precision: 0 = float32, 1 = layer dtype */
+  int launch_cost_rows; /* grouping policy: one launch costs this many padded rows; default 32768 */
+  int reserved[9];
+} spconv_options;
+
+typedef struct spconv_map spconv_map; /* opaque host-side object */
+
+/* ---------------------------------------------------------------- Map step --
+ * Device workspace needed by spconv_build_map for n_in input and (SPCONV_UP)
+ * n_out fine output coordinates; for SPCONV_DOWN pass n_out = 0 (|Q| <= n_in).
+ * The workspace holds the map's device arrays and must stay allocated, and not
+ * be reused, until spconv_free_map() of this map (and of maps transposed from it).
+ * Returns 0 for invalid arguments. */
+size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode,
+                                  const spconv_options* opt);
+
+/* Builds the kernel map M = {(j, i, k)} of Eq. 3 (Section 2.2, Step 1) with
+ * segmented query sorting and the double-traversed binary search (Section 5.1).
+ *   d_in_coords  [n_in][4] int32 input coordinates, any row order, unique.
+ *   d_out_coords SPCONV_UP only: [n_out][4] fine output coordinates; else NULL / 0.
+ *   K            kernel size (1..5); K^3 offsets.
+ *   stride       s of Eq. 1 (SPCONV_SUBM requires 1; SPCONV_DOWN / SPCONV_UP: >= 1).
+ *   tensor_stride t: spacing of the input coordinates (SPCONV_UP: of the fine ones).
+ *   opt          NULL or tunables (B, Cq).
+ *   d_workspace  at least spconv_map_workspace_bytes(...) bytes, 256-byte aligned.
+ * Pair indices are rows of the caller's arrays: input rows in the caller's order;
+ * output rows in the caller's order for SUBM / UP and in sorted (b,x,y,z) order for
+ * DOWN.  Synchronises `stream` twice (coordinate bounds, then per-offset counts).
+ * On success *out_map owns a host object to release with spconv_free_map(). */
+int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords,
+                     int64_t n_out, int K, int stride, int tensor_stride, int mode,
+                     const spconv_options* opt, void* d_workspace, size_t ws_bytes,
+                     void* stream, spconv_map** out_map);
+
+/* The transposed map of a SPCONV_DOWN map: pairs (j, i, k) become (i, j, k); no
+ * device work.  The result borrows `down`'s device arrays: free it before `down`. */
+int spconv_map_transpose(const spconv_map* down, spconv_map** out_map);
+
+int64_t spconv_map_n_in(const spconv_map* m);
+int64_t spconv_map_n_out(const spconv_map* m);
+int spconv_map_kvol(const spconv_map* m); /* K^3 */
+/* Device pointer to the [n_out][4] output coordinates: SPCONV_DOWN's sorted Q,
+ * SPCONV_SUBM's inputs, SPCONV_UP's given fine coordinates. */
+const int32_t* spconv_map_out_coords(const spconv_map* m);
+/* h_counts[k] = |M_k| for k in [0, K^3). */
+int spconv_map_counts(const spconv_map* m, int64_t* h_counts);
+/* Device pointers to offset k's pairs: (*d_in_idx)[e] meets (*d_out_idx)[e] through
+ * W_k, e in [0, *count).  Order inside one offset: ascending sorted query position. */
+int spconv_map_pairs(const spconv_map* m, int k, const int32_t** d_in_idx,
+                     const int32_t** d_out_idx, int64_t* count);
+/* Stream-ordered copies into caller buffers: all pairs, offset-major (offset k's
+ * list starts at sum_{k' < k} |M_k'|), into d_in_idx / d_out_idx of M entries;
+ * and the [n_out][4] output coordinates into d_coords. */
+int spconv_map_copy_pairs(const spconv_map* m, int32_t* d_in_idx, int32_t* d_out_idx, void* stream);
+int spconv_map_copy_out_coords(const spconv_map* m, int32_t* d_coords, void* stream);
+/* Releases the host object (the caller frees the device workspace). */
+void spconv_free_map(spconv_map* m);
+
+/* --------------------------------------------------------------- GMaS step --
+ * Device workspace for spconv_forward with this map and these channel counts. */
+size_t spconv_forward_workspace_bytes(const spconv_map* m, int c_in, int c_out, int dtype,
+                                      const spconv_options* opt);
+
+/* Gather-GEMM-Scatter (Section 2.2, Step 2; Section 5.2):
+ *   y_i = sum_k sum_{(j,i) in M_k} x_j W_k       (Eq. 2)
+ *   d_x [n_in][c_in], d_w [K^3][c_in][c_out] (W_k maps a c_in row vector to c_out),
+ *   d_y [n_out][c_out], all row-major in `dtype`; d_y is fully overwritten (rows
+ *   without pairs get zeros).  Products accumulate in float32.
+ * Requirements: c_in, c_out in [1, 1024]; 16-byte rows (c * element size % 16 == 0)
+ * and c_out % 16 == 0.  Asynchronous on `stream`; no host synchronisation. */
+int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in,
+                   int c_out, int dtype, const spconv_options* opt, void* d_workspace,
+                   size_t ws_bytes, void* stream);
+
+/* What spconv_forward will launch for this map (host-only): padded and real
+ * buffer rows (padding overhead = (padded - real) / real, Section 3 figure on
+ * GEMM reordering), number of GEMM launches, and the tiles used. */
+typedef struct {
+  int64_t rows_real;
+  int64_t rows_padded;
+  int n_gemm_launches;
+  int t_gather;
+  int t_scatter;
+  int grouping;
+} spconv_plan_info;
+int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype,
+                        const spconv_options* opt, spconv_plan_info* info);
+
+/* ------------------------------------------------------------ measurement --
+ * Phase timing: while enabled, the library records HIP events on the caller's
+ * stream around each phase of spconv_build_map / spconv_forward (bounds, sort,
+ * outcoords, backward, balance, forward, readback, metadata, gather, gemm,
+ * scatter).  spconv_profile_read() waits for the recorded events and writes the
+ * summed milliseconds and the number of timed intervals per phase into arrays of
+ * at least spconv_profile_phase_count() entries; reset != 0 clears the record. */
+int spconv_profile_enable(int on);
+int spconv_profile_phase_count(void);
+const char* spconv_profile_phase_name(int i);
+int spconv_profile_read(double* h_ms, int64_t* h_intervals, int n, int reset);
+
+/* Thread-local message describing the last non-OK status. */
+const char* spconv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPCONV_H */

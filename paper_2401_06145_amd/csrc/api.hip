@@ -1,0 +1,708 @@
+// Host side of the C-ABI (include/spconv.h): argument checks, workspace plans,
+// the Map-step orchestration (Section 5.1) and the GMaS plan (Section 5.2).
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "spconv.h"
+
+using namespace spc;
+
+struct spconv_map {
+  int mode = 0, K = 0, K3 = 0, stride = 1, tstride = 1;
+  int64_t n_in = 0, n_out = 0;
+  const int32_t* out_coords = nullptr;
+  const int32_t* pin = nullptr;   // concatenated pair lists, offset-major
+  const int32_t* pout = nullptr;
+  std::vector<int64_t> counts;    // |M_k|
+  std::vector<int64_t> ptr;       // prefix of counts, K3 + 1 entries
+  bool transposed = false;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(SPCONV_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define SPC_TRY(expr, where)              \
+  do {                                    \
+    hipError_t _e = (expr);               \
+    if (_e != hipSuccess) return hip_fail(_e, where); \
+  } while (0)
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Bump allocator over a workspace; with base == nullptr it only measures.
+struct Bump {
+  char* base;
+  size_t off = 0;
+  explicit Bump(void* b) : base(static_cast<char*>(b)) {}
+  template <typename T>
+  T* take(int64_t n) {
+    off = align_up(off, 256);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += (size_t)(n > 0 ? n : 0) * sizeof(T);
+    return p;
+  }
+  void* take_bytes(size_t n) {
+    off = align_up(off, 256);
+    void* p = base ? base + off : nullptr;
+    off += n;
+    return p;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Phase timing (measurement API): HIP events around each phase on the stream.
+// ---------------------------------------------------------------------------
+enum Phase {
+  PH_BOUNDS = 0, PH_SORT, PH_OUTCOORDS, PH_BACKWARD, PH_BALANCE, PH_FORWARD, PH_READBACK,
+  PH_METADATA, PH_GATHER, PH_GEMM, PH_SCATTER, PH_COUNT
+};
+const char* kPhaseNames[PH_COUNT] = {"bounds", "sort", "outcoords", "backward", "balance", "forward",
+                                     "readback", "metadata", "gather", "gemm", "scatter"};
+struct PhaseRec {
+  int phase;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof = false;
+std::vector<PhaseRec> g_recs;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t ev_get() {
+  hipEvent_t e = nullptr;
+  if (!g_pool.empty()) {
+    e = g_pool.back();
+    g_pool.pop_back();
+  } else if (hipEventCreate(&e) != hipSuccess) {
+    e = nullptr;
+  }
+  return e;
+}
+
+struct PhaseScope {
+  int phase;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  PhaseScope(int p, hipStream_t st) : phase(p), s(st) {
+    if (!g_prof) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    a = ev_get();
+    if (a) (void)hipEventRecord(a, s);
+  }
+  ~PhaseScope() {
+    if (!a) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    hipEvent_t b = ev_get();
+    if (!b) return;
+    (void)hipEventRecord(b, s);
+    g_recs.push_back({phase, a, b});
+  }
+};
+
+// Pinned host staging for the two read-backs of a map build (one per thread).
+struct Staging {
+  void* p = nullptr;
+  size_t n = 0;
+};
+thread_local Staging g_stage;
+
+void* staging(size_t bytes) {
+  if (g_stage.n < bytes) {
+    if (g_stage.p) (void)hipHostFree(g_stage.p);
+    g_stage.p = nullptr;
+    g_stage.n = 0;
+    if (hipHostMalloc(&g_stage.p, bytes, hipHostMallocDefault) != hipSuccess) return nullptr;
+    g_stage.n = bytes;
+  }
+  return g_stage.p;
+}
+
+// ---------------------------------------------------------------------------
+// Map workspace plan
+// ---------------------------------------------------------------------------
+struct MapBufs {
+  uint64_t* skeys;
+  uint32_t* sidx;
+  uint64_t* qkeys;
+  uint32_t* qrow;
+  int32_t* qcoords;
+  int32_t* pin;
+  int32_t* pout;
+  uint32_t* counts;
+  ControlBlock* cb;
+  uint64_t* kalt;
+  uint32_t* valt;
+  uint64_t* dkeys;
+  uint32_t* dvals;
+  uint32_t* flags;
+  uint32_t* pos;
+  void* sort_tmp;
+  uint32_t* bounds;
+  uint32_t* chunks;
+  uint32_t* istart;
+  void* scan_tmp;
+  int32_t* items;
+  uint64_t* status;
+  int64_t max_items;
+  int64_t nb;
+};
+
+struct Tunables {
+  int B = 256;
+  int Cq = 512;
+};
+
+int read_tunables(const spconv_options* opt, Tunables* t) {
+  if (!opt) return SPCONV_OK;
+  if (opt->B) {
+    if (opt->B < 64 || opt->B > 4096 || (opt->B & (opt->B - 1)))
+      return fail(SPCONV_EINVAL, "B must be a power of two in [64, 4096]");
+    t->B = opt->B;
+  }
+  if (opt->Cq) {
+    const int r = opt->Cq / 256;
+    if (opt->Cq % 256 != 0 || !(r == 1 || r == 2 || r == 4 || r == 8))
+      return fail(SPCONV_EINVAL, "Cq must be 256, 512, 1024 or 2048");
+    t->Cq = opt->Cq;
+  }
+  return SPCONV_OK;
+}
+
+size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunables& tu, int mode, MapBufs* b) {
+  Bump m(base);
+  const int64_t nmax = std::max(n_src, nq_max);
+  b->nb = (n_src + tu.B - 1) / tu.B;
+  b->max_items = (int64_t)K3 * (b->nb + (nq_max + tu.Cq - 1) / tu.Cq) + 1;
+  b->skeys = m.take<uint64_t>(n_src);
+  b->sidx = m.take<uint32_t>(n_src);
+  b->qkeys = (mode == SPCONV_SUBM) ? nullptr : m.take<uint64_t>(nq_max);
+  b->qrow = (mode == SPCONV_SUBM) ? nullptr : m.take<uint32_t>(nq_max);
+  b->qcoords = (mode == SPCONV_DOWN) ? m.take<int32_t>(4 * nq_max) : nullptr;
+  b->pin = m.take<int32_t>((int64_t)K3 * nq_max);
+  b->pout = m.take<int32_t>((int64_t)K3 * nq_max);
+  b->counts = m.take<uint32_t>(K3);
+  b->cb = m.take<ControlBlock>(1);
+  // build-time scratch
+  b->kalt = m.take<uint64_t>(nmax);
+  b->valt = m.take<uint32_t>(nmax);
+  b->dkeys = (mode == SPCONV_DOWN) ? m.take<uint64_t>(n_src) : nullptr;
+  b->dvals = (mode == SPCONV_DOWN) ? m.take<uint32_t>(n_src) : nullptr;
+  b->flags = (mode == SPCONV_DOWN) ? m.take<uint32_t>(n_src) : nullptr;
+  b->pos = (mode == SPCONV_DOWN) ? m.take<uint32_t>(n_src) : nullptr;
+  b->sort_tmp = m.take_bytes(radix_temp_bytes(nmax));
+  const int64_t nkb = (int64_t)K3 * b->nb;
+  b->bounds = m.take<uint32_t>(nkb);
+  b->chunks = m.take<uint32_t>(nkb);
+  b->istart = m.take<uint32_t>(nkb);
+  b->scan_tmp = m.take_bytes(scan_temp_bytes(std::max(nkb, n_src)));
+  b->items = m.take<int32_t>(2 * b->max_items);
+  b->status = m.take<uint64_t>(b->max_items);
+  return align_up(m.off, 256);
+}
+
+int bit_length(uint64_t v) {
+  int b = 0;
+  while (v) {
+    ++b;
+    v >>= 1;
+  }
+  return b;
+}
+
+// Key layout from coordinate bounds; pad = kernel reach plus the Eq. 1 cell.
+int make_layout(const int32_t mn[4], const int32_t mx[4], int K, int stride, int t, KeyLayout* L) {
+  const int64_t pad = (int64_t)t * (K - 1) + (int64_t)t * stride;
+  int width[4];
+  for (int f = 0; f < 4; ++f) {
+    const int64_t p = (f == 0) ? 0 : pad;
+    const int64_t lo = (int64_t)mn[f] - p;
+    const int64_t hi = (int64_t)mx[f] + p;
+    L->lo[f] = lo;
+    width[f] = bit_length((uint64_t)(hi - lo));
+    L->width[f] = width[f];
+  }
+  L->shift[3] = 0;
+  L->shift[2] = width[3];
+  L->shift[1] = width[3] + width[2];
+  L->shift[0] = width[3] + width[2] + width[1];
+  L->total_bits = width[0] + width[1] + width[2] + width[3];
+  if (L->total_bits > 62) return fail(SPCONV_ERANGE, "coordinate extent (plus kernel reach) needs more than 62 key bits");
+  return SPCONV_OK;
+}
+
+// Delta(K, t): offset k = ix K^2 + iy K + iz is t * (ix - c, iy - c, iz - c).
+void offset_deltas(int K, int t, const KeyLayout& L, int64_t* dk) {
+  const int c = (K % 2 == 1) ? (K - 1) / 2 : 0;
+  int k = 0;
+  for (int ix = 0; ix < K; ++ix)
+    for (int iy = 0; iy < K; ++iy)
+      for (int iz = 0; iz < K; ++iz, ++k) {
+        const int64_t dx = (int64_t)t * (ix - c), dy = (int64_t)t * (iy - c), dz = (int64_t)t * (iz - c);
+        dk[k] = dx * ((int64_t)1 << L.shift[1]) + dy * ((int64_t)1 << L.shift[2]) + dz * ((int64_t)1 << L.shift[3]);
+      }
+}
+
+int check_map_args(int64_t n_in, int64_t n_out, int K, int stride, int t, int mode) {
+  if (K < 1 || K > 5) return fail(SPCONV_EUNSUPPORTED, "K must be in [1, 5]");
+  if (t < 1) return fail(SPCONV_EINVAL, "tensor_stride must be >= 1");
+  if (mode != SPCONV_SUBM && mode != SPCONV_DOWN && mode != SPCONV_UP) return fail(SPCONV_EINVAL, "bad mode");
+  if (mode == SPCONV_SUBM && stride != 1) return fail(SPCONV_EINVAL, "SPCONV_SUBM requires stride 1");
+  if (stride < 1) return fail(SPCONV_EINVAL, "stride must be >= 1");
+  if (n_in < 0 || n_out < 0) return fail(SPCONV_EINVAL, "negative size");
+  if (n_in >= (int64_t)1 << 31 || n_out >= (int64_t)1 << 31) return fail(SPCONV_EUNSUPPORTED, "more than 2^31 rows");
+  return SPCONV_OK;
+}
+
+// ---------------------------------------------------------------------------
+// GMaS plan: GEMM grouping (Section 5.2.2) and tiles (Algorithm 1)
+// ---------------------------------------------------------------------------
+struct GmasPlan {
+  int elem = 4, pelem = 4, part_dtype = 0;
+  int t_gather = 0, t_scatter = 0;
+  int grouping = SPCONV_GROUP_RAGGED;
+  int mt_stride = 0;
+  int64_t rows_real = 0, rows_padded = 0;
+  int n_launches = 0;
+  std::vector<std::vector<GemmSeg>> launches;  // one entry per GEMM launch (group)
+};
+
+int elem_bytes(int dtype) { return dtype == SPCONV_F32 ? 4 : 2; }
+
+// Groups consecutive entries of `order` (offset ids) minimising
+// sum_g (launch_cost + members_g * max_count_g); returns group boundaries.
+std::vector<int> dp_groups(const std::vector<int>& order, const std::vector<int64_t>& cnt, int64_t launch_cost) {
+  const int n = (int)order.size();
+  std::vector<int64_t> best(n + 1, INT64_MAX);
+  std::vector<int> from(n + 1, 0);
+  best[0] = 0;
+  for (int j = 1; j <= n; ++j) {
+    int64_t mx = 0;
+    for (int i = j - 1; i >= 0; --i) {
+      mx = std::max(mx, cnt[order[i]]);
+      const int64_t c = best[i] + launch_cost + (int64_t)(j - i) * mx;
+      if (c < best[j]) {
+        best[j] = c;
+        from[j] = i;
+      }
+    }
+  }
+  std::vector<int> cuts;
+  for (int j = n; j > 0; j = from[j]) cuts.push_back(j);
+  cuts.push_back(0);
+  std::reverse(cuts.begin(), cuts.end());
+  return cuts;
+}
+
+int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_options* opt, GmasPlan* p) {
+  if (!m) return fail(SPCONV_EINVAL, "map is NULL");
+  if (dtype != SPCONV_F32 && dtype != SPCONV_F16 && dtype != SPCONV_BF16) return fail(SPCONV_EUNSUPPORTED, "dtype");
+  p->elem = elem_bytes(dtype);
+  if (c_in < 1 || c_out < 1 || c_in > 1024 || c_out > 1024) return fail(SPCONV_EUNSUPPORTED, "channels must be in [1, 1024]");
+  if ((c_in * p->elem) % 16 != 0) return fail(SPCONV_EUNSUPPORTED, "c_in rows must be whole 16-byte vectors");
+  if (c_out % 16 != 0) return fail(SPCONV_EUNSUPPORTED, "c_out must be a multiple of 16");
+  p->part_dtype = (opt && opt->partial_dtype) ? dtype : SPCONV_F32;
+  p->pelem = elem_bytes(p->part_dtype);
+  // tiles: default one 16-byte vector per thread for gather and for the partial reads of scatter
+  p->t_gather = (opt && opt->t_gather) ? opt->t_gather : 16 / p->elem;
+  p->t_scatter = (opt && opt->t_scatter) ? opt->t_scatter : 16 / p->pelem;
+  if (p->t_gather <= 0 || c_in % p->t_gather != 0 || (p->t_gather * p->elem) % 16 != 0 ||
+      (p->t_gather * p->elem / 16) > 16 || ((p->t_gather * p->elem / 16) & (p->t_gather * p->elem / 16 - 1)))
+    return fail(SPCONV_EINVAL, "t_gather must divide c_in and span 1, 2, 4, 8 or 16 16-byte vectors");
+  const int ts = p->t_scatter;
+  if (!(ts == 4 || ts == 8 || ts == 16 || ts == 32 || ts == 64) || c_out % ts != 0 || (ts * p->pelem) % 16 != 0)
+    return fail(SPCONV_EINVAL, "t_scatter must be 4..64 (power of two), divide c_out and span whole 16-byte partial vectors");
+  p->grouping = (opt && opt->grouping) ? opt->grouping - 1 : SPCONV_GROUP_RAGGED;
+  if (p->grouping < 0 || p->grouping > 2) return fail(SPCONV_EINVAL, "grouping");
+  p->mt_stride = (m->K3 + 3) / 4 * 4;
+
+  const int K3 = m->K3;
+  p->rows_real = m->ptr[K3];
+  p->rows_padded = 0;
+  p->launches.clear();
+  // Buffer rows follow the concatenated pair lists (row of pair e of offset k =
+  // ptr[k] + e); grouping decides launches and padded heights only.
+  if (p->grouping == SPCONV_GROUP_RAGGED) {
+    std::vector<int> order;
+    for (int k = 0; k < K3; ++k)
+      if (m->counts[k] > 0) order.push_back(k);
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return m->counts[a] > m->counts[b]; });
+    std::vector<GemmSeg> segs;
+    for (int k : order) segs.push_back(GemmSeg{k, m->ptr[k], m->counts[k], m->counts[k]});
+    p->rows_padded = p->rows_real;
+    if (!segs.empty()) p->launches.push_back(segs);
+  } else {
+    std::vector<int> order(K3);
+    for (int k = 0; k < K3; ++k) order[k] = k;
+    if (p->grouping == SPCONV_GROUP_SORTED)  // non-decreasing pair count
+      std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return m->counts[a] < m->counts[b]; });
+    std::vector<int> nz;
+    for (int k : order)
+      if (m->counts[k] > 0) nz.push_back(k);
+    const int64_t L = (opt && opt->launch_cost_rows > 0) ? opt->launch_cost_rows : 32768;
+    const std::vector<int> cuts = dp_groups(nz, m->counts, L);
+    for (size_t g = 0; g + 1 < cuts.size(); ++g) {
+      int64_t h = 0;
+      for (int i = cuts[g]; i < cuts[g + 1]; ++i) h = std::max(h, m->counts[nz[i]]);
+      std::vector<GemmSeg> segs;
+      for (int i = cuts[g]; i < cuts[g + 1]; ++i) {
+        const int k = nz[i];
+        segs.push_back(GemmSeg{k, m->ptr[k], m->counts[k], h});
+        p->rows_padded += h;
+      }
+      p->launches.push_back(segs);
+    }
+  }
+  p->n_launches = (int)p->launches.size();
+  return SPCONV_OK;
+}
+
+struct FwdBufs {
+  int32_t* imt;
+  int32_t* omt;
+  void* buf_in;
+  void* buf_out;
+};
+
+size_t plan_forward_ws(void* base, const spconv_map* m, int c_in, int c_out, const GmasPlan& p, FwdBufs* b) {
+  Bump a(base);
+  b->imt = a.take<int32_t>(m->n_in * p.mt_stride);
+  b->omt = a.take<int32_t>(m->n_out * p.mt_stride);
+  b->buf_in = a.take_bytes((size_t)p.rows_real * c_in * p.elem);
+  b->buf_out = a.take_bytes((size_t)p.rows_real * c_out * p.pelem);
+  return align_up(a.off, 256);
+}
+
+}  // namespace
+
+// ===========================================================================
+// C-ABI
+// ===========================================================================
+extern "C" {
+
+const char* spconv_last_error(void) { return g_err.c_str(); }
+
+size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode, const spconv_options* opt) {
+  if (check_map_args(n_in, n_out, K, mode == SPCONV_SUBM ? 1 : 2, 1, mode) != SPCONV_OK) return 0;
+  Tunables tu;
+  if (read_tunables(opt, &tu) != SPCONV_OK) return 0;
+  const int64_t n_src = (mode == SPCONV_UP) ? n_out : n_in;
+  const int64_t nq_max = n_in;
+  MapBufs b;
+  return plan_map(nullptr, n_src, nq_max, K * K * K, tu, mode, &b);
+}
+
+int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords, int64_t n_out, int K,
+                     int stride, int tensor_stride, int mode, const spconv_options* opt, void* d_workspace,
+                     size_t ws_bytes, void* stream, spconv_map** out_map) {
+  if (!out_map) return fail(SPCONV_EINVAL, "out_map is NULL");
+  *out_map = nullptr;
+  int st = check_map_args(n_in, mode == SPCONV_UP ? n_out : 0, K, stride, tensor_stride, mode);
+  if (st != SPCONV_OK) return st;
+  if (n_in > 0 && !d_in_coords) return fail(SPCONV_EINVAL, "d_in_coords is NULL");
+  if (mode == SPCONV_UP && n_out > 0 && !d_out_coords) return fail(SPCONV_EINVAL, "d_out_coords is NULL");
+  if (mode != SPCONV_UP) n_out = 0;
+  Tunables tu;
+  if ((st = read_tunables(opt, &tu)) != SPCONV_OK) return st;
+  const int K3 = K * K * K;
+  const int64_t n_src = (mode == SPCONV_UP) ? n_out : n_in;
+  const int64_t nq_max = n_in;
+  MapBufs b;
+  const size_t need = plan_map(nullptr, n_src, nq_max, K3, tu, mode, &b);
+  if (!d_workspace || ws_bytes < need) return fail(SPCONV_ENOSPC, "map workspace too small");
+  if (reinterpret_cast<uintptr_t>(d_workspace) % 256 != 0) return fail(SPCONV_EINVAL, "workspace must be 256-byte aligned");
+  plan_map(d_workspace, n_src, nq_max, K3, tu, mode, &b);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  spconv_map* m = new (std::nothrow) spconv_map();
+  if (!m) return fail(SPCONV_EINVAL, "out of host memory");
+  m->mode = mode;
+  m->K = K;
+  m->K3 = K3;
+  m->stride = stride;
+  m->tstride = tensor_stride;
+  m->n_in = n_in;
+  m->n_out = (mode == SPCONV_SUBM) ? n_in : (mode == SPCONV_UP ? n_out : 0);
+  m->out_coords = (mode == SPCONV_SUBM) ? d_in_coords : (mode == SPCONV_UP ? d_out_coords : b.qcoords);
+  m->pin = b.pin;
+  m->pout = b.pout;
+  m->counts.assign(K3, 0);
+  m->ptr.assign(K3 + 1, 0);
+  auto done_empty = [&]() {
+    *out_map = m;
+    return SPCONV_OK;
+  };
+  if (n_in == 0 || n_src == 0) return done_empty();
+
+  const int32_t* src_coords = (mode == SPCONV_UP) ? d_out_coords : d_in_coords;
+  auto bail = [&](int code) {
+    delete m;
+    return code;
+  };
+  KeyLayout L;
+  {
+    PhaseScope ph(PH_BOUNDS, s);
+    hipError_t e = launch_minmax_init(b.cb, s);
+    if (e == hipSuccess) e = launch_minmax(d_in_coords, n_in, b.cb, s);
+    if (e == hipSuccess && mode == SPCONV_UP) e = launch_minmax(d_out_coords, n_out, b.cb, s);
+    ControlBlock* h = static_cast<ControlBlock*>(staging(65536));
+    if (!h) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
+    if (e == hipSuccess) e = hipMemcpyAsync(h, b.cb, sizeof(ControlBlock), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return bail(hip_fail(e, "coordinate bounds"));
+    if ((st = make_layout(h->minmax, h->minmax + 4, K, stride, tensor_stride, &L)) != SPCONV_OK) return bail(st);
+  }
+  {
+    PhaseScope ph(PH_SORT, s);
+    hipError_t e = launch_pack(src_coords, n_src, L, b.skeys, b.sidx, s);
+    if (e == hipSuccess) e = radix_sort_kv(b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
+    if (e == hipSuccess) e = launch_check_dup(b.skeys, n_src, b.cb, s);
+    if (e == hipSuccess && mode == SPCONV_UP) {
+      e = launch_pack(d_in_coords, n_in, L, b.qkeys, b.qrow, s);
+      if (e == hipSuccess) e = radix_sort_kv(b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits, b.sort_tmp, s);
+      if (e == hipSuccess) e = launch_check_dup(b.qkeys, n_in, b.cb, s);
+    }
+    if (e != hipSuccess) return bail(hip_fail(e, "sort"));
+  }
+  if (mode == SPCONV_DOWN) {
+    PhaseScope ph(PH_OUTCOORDS, s);
+    const int64_t cell = (int64_t)tensor_stride * stride;
+    hipError_t e = launch_down_keys(b.skeys, n_src, L, cell, b.dkeys, b.dvals, s);
+    if (e == hipSuccess) e = radix_sort_kv(b.dkeys, b.dvals, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
+    if (e == hipSuccess)
+      e = unique_keys(b.dkeys, n_src, L, b.flags, b.pos, b.scan_tmp, b.qkeys, b.qrow, b.qcoords, b.cb, s);
+    if (e != hipSuccess) return bail(hip_fail(e, "output coordinates"));
+  }
+
+  SearchArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.skeys = b.skeys;
+  a.sidx = b.sidx;
+  a.n_src = n_src;
+  a.qkeys = (mode == SPCONV_SUBM) ? b.skeys : b.qkeys;
+  a.qrow = (mode == SPCONV_SUBM) ? b.sidx : b.qrow;
+  a.n_q = nq_max;
+  a.n_q_dev = (mode == SPCONV_DOWN) ? &b.cb->n_q : nullptr;
+  a.K3 = K3;
+  offset_deltas(K, tensor_stride, L, a.dk);
+  a.B = tu.B;
+  a.Cq = tu.Cq;
+  a.swap_roles = (mode == SPCONV_UP) ? 1 : 0;
+  {
+    PhaseScope ph(PH_BACKWARD, s);
+    hipError_t e = launch_backward(a, b.nb, b.bounds, s);
+    if (e != hipSuccess) return bail(hip_fail(e, "backward search"));
+  }
+  {
+    PhaseScope ph(PH_BALANCE, s);
+    hipError_t e = balance(a, b.nb, b.bounds, b.chunks, b.istart, b.scan_tmp, b.items, b.status, b.max_items, b.cb, s);
+    if (e == hipSuccess) e = launch_fill_u32(b.counts, 0u, K3, s);
+    if (e != hipSuccess) return bail(hip_fail(e, "balance"));
+  }
+  {
+    PhaseScope ph(PH_FORWARD, s);
+    hipError_t e = launch_forward(a, b.bounds, b.nb, b.items, b.status, b.max_items, b.pin, b.pout, b.counts, b.cb, s);
+    if (e != hipSuccess) return bail(hip_fail(e, "forward search"));
+  }
+  {
+    PhaseScope ph(PH_READBACK, s);
+    char* h = static_cast<char*>(staging(65536));
+    if (!h) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
+    ControlBlock* hc = reinterpret_cast<ControlBlock*>(h);
+    uint32_t* hcnt = reinterpret_cast<uint32_t*>(h + 4096);
+    hipError_t e = hipMemcpyAsync(hc, b.cb, sizeof(ControlBlock), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(hcnt, b.counts, sizeof(uint32_t) * K3, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return bail(hip_fail(e, "count read-back"));
+    if (hc->err & kErrDup) return bail(fail(SPCONV_EDUP, "duplicate coordinates"));
+    if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "forward search look-back exceeded its wait bound"));
+    if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "work-item overflow in the balance step"));
+    if (mode == SPCONV_DOWN) m->n_out = hc->n_q;
+    for (int k = 0; k < K3; ++k) {
+      m->counts[k] = hcnt[k];
+      m->ptr[k + 1] = m->ptr[k] + hcnt[k];
+    }
+  }
+  *out_map = m;
+  return SPCONV_OK;
+}
+
+int spconv_map_transpose(const spconv_map* down, spconv_map** out_map) {
+  if (!down || !out_map) return fail(SPCONV_EINVAL, "NULL argument");
+  *out_map = nullptr;
+  if (down->mode != SPCONV_DOWN) return fail(SPCONV_EINVAL, "only SPCONV_DOWN maps can be transposed");
+  spconv_map* m = new (std::nothrow) spconv_map(*down);
+  if (!m) return fail(SPCONV_EINVAL, "out of host memory");
+  m->mode = SPCONV_UP;
+  m->transposed = true;
+  m->n_in = down->n_out;
+  m->n_out = down->n_in;
+  m->pin = down->pout;
+  m->pout = down->pin;
+  m->out_coords = nullptr;  // the fine coordinates are the DOWN map's inputs (caller-owned)
+  *out_map = m;
+  return SPCONV_OK;
+}
+
+int64_t spconv_map_n_in(const spconv_map* m) { return m ? m->n_in : -1; }
+int64_t spconv_map_n_out(const spconv_map* m) { return m ? m->n_out : -1; }
+int spconv_map_kvol(const spconv_map* m) { return m ? m->K3 : -1; }
+const int32_t* spconv_map_out_coords(const spconv_map* m) { return m ? m->out_coords : nullptr; }
+
+int spconv_map_counts(const spconv_map* m, int64_t* h_counts) {
+  if (!m || !h_counts) return fail(SPCONV_EINVAL, "NULL argument");
+  for (int k = 0; k < m->K3; ++k) h_counts[k] = m->counts[k];
+  return SPCONV_OK;
+}
+
+int spconv_map_pairs(const spconv_map* m, int k, const int32_t** d_in_idx, const int32_t** d_out_idx, int64_t* count) {
+  if (!m || !d_in_idx || !d_out_idx || !count) return fail(SPCONV_EINVAL, "NULL argument");
+  if (k < 0 || k >= m->K3) return fail(SPCONV_EINVAL, "offset index out of range");
+  *d_in_idx = m->pin + m->ptr[k];
+  *d_out_idx = m->pout + m->ptr[k];
+  *count = m->counts[k];
+  return SPCONV_OK;
+}
+
+int spconv_map_copy_pairs(const spconv_map* m, int32_t* d_in_idx, int32_t* d_out_idx, void* stream) {
+  if (!m) return fail(SPCONV_EINVAL, "map is NULL");
+  const int64_t n = m->ptr[m->K3];
+  if (n == 0) return SPCONV_OK;
+  if (!d_in_idx || !d_out_idx) return fail(SPCONV_EINVAL, "NULL destination");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SPC_TRY(hipMemcpyAsync(d_in_idx, m->pin, (size_t)n * 4, hipMemcpyDeviceToDevice, s), "copy pairs");
+  SPC_TRY(hipMemcpyAsync(d_out_idx, m->pout, (size_t)n * 4, hipMemcpyDeviceToDevice, s), "copy pairs");
+  return SPCONV_OK;
+}
+
+int spconv_map_copy_out_coords(const spconv_map* m, int32_t* d_coords, void* stream) {
+  if (!m) return fail(SPCONV_EINVAL, "map is NULL");
+  if (m->n_out == 0) return SPCONV_OK;
+  if (!d_coords) return fail(SPCONV_EINVAL, "NULL destination");
+  if (!m->out_coords) return fail(SPCONV_EINVAL, "this map does not hold its output coordinates");
+  SPC_TRY(hipMemcpyAsync(d_coords, m->out_coords, (size_t)m->n_out * 16, hipMemcpyDeviceToDevice,
+                         static_cast<hipStream_t>(stream)),
+          "copy coordinates");
+  return SPCONV_OK;
+}
+
+void spconv_free_map(spconv_map* m) { delete m; }
+
+size_t spconv_forward_workspace_bytes(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_options* opt) {
+  GmasPlan p;
+  if (make_plan(m, c_in, c_out, dtype, opt, &p) != SPCONV_OK) return 0;
+  FwdBufs b;
+  return plan_forward_ws(nullptr, m, c_in, c_out, p, &b);
+}
+
+int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_options* opt,
+                        spconv_plan_info* info) {
+  if (!info) return fail(SPCONV_EINVAL, "info is NULL");
+  GmasPlan p;
+  const int st = make_plan(m, c_in, c_out, dtype, opt, &p);
+  if (st != SPCONV_OK) return st;
+  info->rows_real = p.rows_real;
+  info->rows_padded = p.rows_padded;
+  info->n_gemm_launches = p.n_launches;
+  info->t_gather = p.t_gather;
+  info->t_scatter = p.t_scatter;
+  info->grouping = p.grouping;
+  return SPCONV_OK;
+}
+
+int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in, int c_out, int dtype,
+                   const spconv_options* opt, void* d_workspace, size_t ws_bytes, void* stream) {
+  GmasPlan p;
+  int st = make_plan(m, c_in, c_out, dtype, opt, &p);
+  if (st != SPCONV_OK) return st;
+  if (m->n_out > 0 && !d_y) return fail(SPCONV_EINVAL, "d_y is NULL");
+  if (p.rows_real > 0 && (!d_x || !d_w)) return fail(SPCONV_EINVAL, "d_x / d_w is NULL");
+  FwdBufs b;
+  const size_t need = plan_forward_ws(nullptr, m, c_in, c_out, p, &b);
+  if (need > 0 && (!d_workspace || ws_bytes < need)) return fail(SPCONV_ENOSPC, "forward workspace too small");
+  if (reinterpret_cast<uintptr_t>(d_workspace) % 256 != 0) return fail(SPCONV_EINVAL, "workspace must be 256-byte aligned");
+  plan_forward_ws(d_workspace, m, c_in, c_out, p, &b);
+  if (m->n_out == 0) return SPCONV_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int K3 = m->K3;
+  {
+    PhaseScope ph(PH_METADATA, s);
+    SPC_TRY(launch_mt_fill(b.imt, m->n_in, b.omt, m->n_out, p.mt_stride, s), "metadata fill");
+    if (p.rows_real > 0) {
+      OffsetTable t;
+      std::memset(&t, 0, sizeof(t));
+      t.K3 = K3;
+      for (int k = 0; k <= K3; ++k) t.pair_start[k] = m->ptr[k];
+      for (int k = 0; k < K3; ++k) t.row_base[k] = m->ptr[k];
+      SPC_TRY(launch_mt_pairs(m->pin, m->pout, p.rows_real, t, b.imt, b.omt, p.mt_stride, s), "metadata tables");
+    }
+  }
+  if (p.rows_real > 0) {
+    {
+      PhaseScope ph(PH_GATHER, s);
+      SPC_TRY(launch_gather(d_x, m->n_in, c_in, p.elem, b.imt, p.mt_stride, K3, b.buf_in, p.t_gather, s), "gather");
+    }
+    {
+      PhaseScope ph(PH_GEMM, s);
+      for (const auto& segs : p.launches)
+        SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), b.buf_in, d_w, b.buf_out, c_in, c_out, dtype, p.part_dtype, s),
+                "grouped GEMM");
+    }
+  }
+  {
+    PhaseScope ph(PH_SCATTER, s);
+    SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, b.omt, p.mt_stride, K3, d_y, dtype, p.t_scatter, s),
+            "scatter");
+  }
+  return SPCONV_OK;
+}
+
+// --------------------------------------------------------------- measurement
+int spconv_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof = on != 0;
+  return SPCONV_OK;
+}
+
+int spconv_profile_phase_count(void) { return PH_COUNT; }
+const char* spconv_profile_phase_name(int i) { return (i >= 0 && i < PH_COUNT) ? kPhaseNames[i] : ""; }
+
+int spconv_profile_read(double* ms, int64_t* launches, int n, int reset) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!ms || !launches || n < PH_COUNT) return fail(SPCONV_EINVAL, "need PH_COUNT entries");
+  for (int i = 0; i < PH_COUNT; ++i) {
+    ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  for (auto& r : g_recs) {
+    float t = 0.f;
+    if (hipEventSynchronize(r.b) != hipSuccess) return fail(SPCONV_EHIP, "event sync");
+    if (hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) return fail(SPCONV_EHIP, "event elapsed");
+    ms[r.phase] += t;
+    launches[r.phase] += 1;
+  }
+  if (reset) {
+    for (auto& r : g_recs) {
+      g_pool.push_back(r.a);
+      g_pool.push_back(r.b);
+    }
+    g_recs.clear();
+  }
+  return SPCONV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,163 @@
+// Internal declarations shared by the library's HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+#include <hip/hip_fp16.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace spc {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Coordinate keys.  (b, x, y, z) is packed into one unsigned 64-bit key whose
+// unsigned order is the lexicographic order of the signed tuple: each field is
+// biased by its low bound and given a fixed bit width, b in the top bits.  The
+// bias leaves room for the kernel's reach, so for any offset delta the key of
+// q + delta is key(q) + dkey(delta) with no carry between fields; a query
+// segment of sorted outputs (Section 5.1.1) is then sorted in key order too.
+// ---------------------------------------------------------------------------
+struct KeyLayout {
+  int64_t lo[4];   // value subtracted from field f before packing
+  int shift[4];    // bit position of field f
+  int width[4];    // bits of field f
+  int total_bits;  // sum of widths (<= 62)
+};
+
+__device__ __forceinline__ uint64_t pack_key(const KeyLayout& L, const int32_t* c) {
+  uint64_t k = 0;
+#pragma unroll
+  for (int f = 0; f < 4; ++f) k |= (uint64_t)((int64_t)c[f] - L.lo[f]) << L.shift[f];
+  return k;
+}
+
+__device__ __forceinline__ int32_t key_field(const KeyLayout& L, uint64_t k, int f) {
+  const uint64_t mask = (L.width[f] >= 64) ? ~0ull : ((1ull << L.width[f]) - 1ull);
+  return (int32_t)((int64_t)((k >> L.shift[f]) & mask) + L.lo[f]);
+}
+
+// Wave helpers (wave64).
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int lane = threadIdx.x & (kWave - 1);
+  return (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+}
+
+__device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
+
+// Device-scope (agent) atomics on 64-bit status words used by the look-back scans.
+__device__ __forceinline__ uint64_t ld_acquire_agent(uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_release_agent(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+// Device error flags, OR-ed into ControlBlock::err by kernels.
+// ---------------------------------------------------------------------------
+enum : uint32_t {
+  kErrDup = 1u,          // two equal keys among the sorted inputs
+  kErrSpin = 2u,         // a look-back wait exceeded its bound
+  kErrOverflow = 4u,     // more work items than the launch was sized for
+};
+
+// Small control block in device memory, read back once at the end of a map build.
+struct ControlBlock {
+  int32_t minmax[8];     // min b,x,y,z then max b,x,y,z (coordinate bounds pass)
+  uint32_t err;          // kErr* flags
+  uint32_t n_q;          // number of distinct output coordinates (DOWN)
+  uint32_t n_items;      // forward-search work items emitted by the balance step
+  uint32_t ticket;       // work-item ticket counter of the forward search
+  uint32_t pad[4];
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (host functions, defined next to their kernels).
+// ---------------------------------------------------------------------------
+
+// scan.hip: exclusive prefix sum of n uint32 values; *d_total (optional) gets the sum.
+size_t scan_temp_bytes(int64_t n);
+hipError_t scan_exclusive_u32(const uint32_t* d_in, uint32_t* d_out, int64_t n, uint32_t* d_total,
+                              void* d_temp, hipStream_t s);
+
+// map_kernels.hip
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+hipError_t launch_minmax_init(ControlBlock* cb, hipStream_t s);
+hipError_t launch_minmax(const int32_t* coords, int64_t n, ControlBlock* cb, hipStream_t s);
+hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals,
+                       hipStream_t s);
+size_t radix_temp_bytes(int64_t n);
+// Sorts (keys, vals) by the low `bits` key bits; the result ends in (keys, vals).
+hipError_t radix_sort_kv(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt,
+                         int64_t n, int bits, void* d_temp, hipStream_t s);
+hipError_t launch_check_dup(const uint64_t* keys, int64_t n, ControlBlock* cb, hipStream_t s);
+hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell,
+                            uint64_t* dkeys, uint32_t* vals, hipStream_t s);
+// Distinct consecutive keys of sorted `keys` -> qkeys, qrow = position, coords; n_q into cb.
+hipError_t unique_keys(const uint64_t* keys, int64_t n, KeyLayout L, uint32_t* flags,
+                       uint32_t* pos, void* d_temp, uint64_t* qkeys, uint32_t* qrow,
+                       int32_t* out_coords, ControlBlock* cb, hipStream_t s);
+hipError_t launch_unpack(const uint64_t* keys, int64_t n, KeyLayout L, int32_t* coords, hipStream_t s);
+
+struct SearchArgs {
+  const uint64_t* skeys;  // sorted source keys [n_src]
+  const uint32_t* sidx;   // their caller rows
+  int64_t n_src;
+  const uint64_t* qkeys;  // sorted query base keys [n_q] (n_q read from n_q_dev if non-null)
+  const uint32_t* qrow;   // their caller rows
+  int64_t n_q;
+  const uint32_t* n_q_dev;
+  int K3;
+  int64_t dk[125];        // key delta of each offset
+  int B;                  // source block size
+  int Cq;                 // query block limit
+  int swap_roles;         // UP: pairs are (query row, source row)
+};
+// Section 5.1.2: backward search, then balance (chunks, scan, emit).
+hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, hipStream_t s);
+hipError_t balance(const SearchArgs& a, int64_t nb, const uint32_t* bounds, uint32_t* chunks,
+                   uint32_t* item_start, void* d_temp, int32_t* items, uint64_t* status,
+                   int64_t max_items, ControlBlock* cb, hipStream_t s);
+// Forward search with in-order compaction of matches into per-offset pair lists.
+hipError_t launch_forward(const SearchArgs& a, const uint32_t* bounds, int64_t nb,
+                          const int32_t* items, uint64_t* status, int64_t max_items,
+                          int32_t* pin, int32_t* pout, uint32_t* counts, ControlBlock* cb,
+                          hipStream_t s);
+
+// gmas_kernels.hip
+constexpr int kMaxOffsets = 125;  // K <= 5
+struct OffsetTable {
+  int K3;
+  int64_t pair_start[kMaxOffsets + 1];  // prefix of |M_k| in the concatenated pair lists
+  int64_t row_base[kMaxOffsets];        // first buffer row of offset k
+};
+hipError_t launch_mt_fill(int32_t* imt, int64_t n_in, int32_t* omt, int64_t n_out, int stride,
+                          hipStream_t s);
+hipError_t launch_mt_pairs(const int32_t* pin, const int32_t* pout, int64_t m_total,
+                           const OffsetTable& t, int32_t* imt, int32_t* omt, int stride,
+                           hipStream_t s);
+// Algorithm 1 gather with tile T channels per thread; elem = element bytes.
+hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const int32_t* imt,
+                         int mt_stride, int K3, void* buf_in, int tile, hipStream_t s);
+// Scatter: y[i] = sum_k buf_out[omt[i][k]] (float32 sum), tile T channels per thread.
+hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out,
+                          const int32_t* omt, int mt_stride, int K3, void* y, int dtype, int tile,
+                          hipStream_t s);
+
+// gemm_mfma.hip: grouped per-offset GEMMs, buf_out[rows of k] = buf_in[rows of k] W_k.
+// A segment is one offset's run of buffer rows; `height` >= `rows` is the padded
+// height the group computes (padding rows are zeros: computed, never loaded or stored).
+struct GemmSeg {
+  int k;
+  int64_t row0;
+  int64_t rows;
+  int64_t height;
+};
+// Launches the segments (any number; split into launches of at most 64 segments).
+hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, void* buf_out,
+                       int c_in, int c_out, int dtype, int part_dtype, hipStream_t s);
+
+}  // namespace spc

@@ -1,0 +1,305 @@
+"""GPU parity: the HIP library (through the C-ABI) against the CPU oracle.
+
+Kernel maps must match bit-exactly as per-offset pair sets; features must be
+within the normwise tolerance max|y - y_ref| / max|y_ref| <= 1e-4 (f32) or
+1e-2 (f16, bf16).  Inputs are seeded; expected values come from the oracle only.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2401_06145_amd import binding as B
+from paper_2401_06145_amd import scenes
+from tests.gpu_helpers import DEV, TOL, assert_map_equal, gpu_pairs, rel_err, say, to_dev, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _cloud(seed, n, lo, hi, nb=2, t=1):
+    rng = np.random.default_rng(seed)
+    side = hi - lo
+    cells = rng.choice(nb * side ** 3, n, replace=False)
+    b = cells // side ** 3
+    r = cells % side ** 3
+    x, y, z = r // side ** 2 + lo, (r // side) % side + lo, r % side + lo
+    c = np.stack([b, x * t, y * t, z * t], axis=1).astype(np.int32)
+    return np.ascontiguousarray(c)
+
+
+def _conv_gpu(coords, x, w, K, stride=1, t=1, mode="subm", out_coords=None, opt=None, dtype="f32"):
+    dc = to_dev(coords)
+    doc = to_dev(out_coords) if out_coords is not None else None
+    km = B.KernelMap.build(dc, K, stride, t, mode, doc, opt)
+    f = B.Forward(km, x.shape[1], w.shape[2], B.TORCH_DTYPES[dtype], opt)
+    y = f(to_dev(x, dtype), to_dev(w, dtype))
+    torch.cuda.synchronize()
+    return km, y
+
+
+# ----------------------------------------------------------------------------
+# Small clouds: many source blocks, pivot edges, split query blocks
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("K", [1, 2, 3, 5])
+@pytest.mark.parametrize("Bsz,Cq", [(64, 256), (256, 512), (1024, 2048)])
+def test_subm_small(K, Bsz, Cq):
+    say(f"subm small K={K} B={Bsz} Cq={Cq}")
+    c = _cloud(10 + K, 3000, -9, 9)
+    x = scenes.features(len(c), 16, "f32", 1)
+    w = scenes.weights(K, 16, 16, "f32", 2)
+    opt = B.Options.make(B=Bsz, Cq=Cq)
+    km, y = _conv_gpu(c, x, w, K, opt=opt)
+    okm = oracle.kernel_map(c, None, K, 1, "subm")
+    assert_map_equal(km, okm)
+    ref = oracle.features(x, w, okm)
+    assert rel_err(to_f64(y), ref) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("K,s,t", [(2, 2, 1), (3, 2, 1), (2, 2, 2), (2, 3, 1), (3, 3, 2)])
+@pytest.mark.parametrize("Bsz", [64, 256])
+def test_down_up_small(K, s, t, Bsz):
+    say(f"down/up small K={K} s={s} t={t} B={Bsz}")
+    c = _cloud(20 + K + s, 2500, -10, 10, t=t)
+    x = scenes.features(len(c), 8, "f32", 3)
+    w = scenes.weights(K, 8, 16, "f32", 4)
+    opt = B.Options.make(B=Bsz, Cq=256)
+    km, y = _conv_gpu(c, x, w, K, s, t, "down", opt=opt)
+    q = oracle.out_coords(c, s, t)
+    qg = km.out_coords().cpu().numpy()
+    assert np.array_equal(qg, q), "DOWN output coordinates differ from Eq. 1"
+    okm = oracle.kernel_map(c, q, K, t, "down")
+    assert_map_equal(km, okm)
+    assert rel_err(to_f64(y), oracle.features(x, w, okm)) <= TOL["f32"]
+    # transposed conv back to the fine sites: built directly, and by transposing
+    xc = scenes.features(len(q), 16, "f32", 5)
+    wu = scenes.weights(K, 16, 16, "f32", 6)
+    oup = oracle.kernel_map(q, c, K, t, "up")
+    yref = oracle.features(xc, wu, oup)
+    kup, yu = _conv_gpu(q, xc, wu, K, s, t, "up", out_coords=c, opt=opt)
+    assert_map_equal(kup, oup)
+    assert rel_err(to_f64(yu), yref) <= TOL["f32"]
+    kt = km.transpose()
+    yt = B.Forward(kt, 16, 16, torch.float32)(to_dev(xc), to_dev(wu))
+    torch.cuda.synchronize()
+    assert_map_equal(kt, oup)
+    assert rel_err(to_f64(yt), yref) <= TOL["f32"]
+
+
+def test_negative_and_wide_coordinates():
+    say("negative / wide coordinates")
+    rng = np.random.default_rng(5)
+    base = _cloud(30, 2000, -6, 6)
+    base[:, 1] = base[:, 1] * 1000 - 7          # wide, negative x
+    base[:, 3] = base[:, 3] - 100000            # far negative z
+    assert len(np.unique(base, axis=0)) == len(base)
+    x = scenes.features(len(base), 4, "f32", 7)
+    w = scenes.weights(3, 4, 16, "f32", 8)
+    km, y = _conv_gpu(base, x, w, 3)
+    okm = oracle.kernel_map(base, None, 3, 1, "subm")
+    assert_map_equal(km, okm)
+    assert rel_err(to_f64(y), oracle.features(x, w, okm)) <= TOL["f32"]
+    _ = rng
+
+
+# ----------------------------------------------------------------------------
+# Hand example and the paper's segment example
+# ----------------------------------------------------------------------------
+
+def test_hand_two_voxel_example():
+    say("hand two-voxel example")
+    p = np.array([[0, 0, 0, 0], [0, 1, 0, 0]], np.int32)
+    x = np.zeros((2, 4), np.float32)
+    x[:, 0] = [1, 2]
+    w = np.zeros((27, 4, 16), np.float32)
+    w[:, 0, 0] = np.arange(27) + 1
+    km, y = _conv_gpu(p, x, w, 3)
+    assert y[:, 0].cpu().tolist() == [60.0, 33.0]
+    assert float(y[:, 1:].abs().max()) == 0.0
+    w2 = np.zeros((8, 4, 16), np.float32)
+    w2[:, 0, 0] = np.arange(8) + 1
+    kd, yd = _conv_gpu(p, x, w2, 2, 2, 1, "down")
+    assert yd[:, 0].cpu().tolist() == [11.0]
+    xc = np.zeros((1, 16), np.float32)
+    xc[0, 0] = 3
+    w3 = np.zeros((8, 16, 16), np.float32)
+    w3[:, 0, 0] = np.arange(8) + 1
+    yu = B.Forward(kd.transpose(), 16, 16, torch.float32)(to_dev(xc), to_dev(w3))
+    assert yu[:, 0].cpu().tolist() == [3.0, 15.0]
+
+
+# ----------------------------------------------------------------------------
+# Workloads at full size
+# ----------------------------------------------------------------------------
+
+def _workload_layer(i, c=None, rows=None):
+    wl = scenes.workload(i, c)
+    L = wl.layers[0]
+    coords = wl.coords
+    say(f"workload {i} ({wl.name}): {len(coords)} voxels")
+    x = scenes.features(len(coords), L.c_in, L.dtype, 2000 + i)
+    w = scenes.weights(L.K, L.c_in, L.c_out, L.dtype, 3000 + i)
+    km, y = _conv_gpu(coords, x, w, L.K, L.stride, 1, L.mode, dtype=L.dtype)
+    okm = oracle.kernel_map(coords, None, L.K, 1, "subm")
+    assert_map_equal(km, okm)
+    xf, wf = scenes.to_f64(x, L.dtype), scenes.to_f64(w, L.dtype)
+    if rows is None:
+        ref = oracle.features(xf, wf, okm)
+        got = to_f64(y)
+    else:
+        sel = np.sort(np.random.default_rng(99).choice(len(coords), rows, replace=False))
+        ref = oracle.features(xf, wf, okm, rows=sel)
+        got = to_f64(y)[sel]
+    err = rel_err(got, ref)
+    print(f"workload {i}: pairs={sum(km.counts())} normwise error {err:.3e}", flush=True)
+    assert err <= TOL[L.dtype]
+    return km, okm
+
+
+def test_workload0_uniform_f32():
+    _workload_layer(0)
+
+
+def test_workload1_lidar_f16():
+    _workload_layer(1)
+
+
+@pytest.mark.parametrize("c", [32, 256])
+def test_workload3_indoor_f16(c):
+    _workload_layer(3, c, rows=None if c <= 64 else 4000)
+
+
+def test_workload2_down_up_f16():
+    wl = scenes.workload(2)
+    coords = wl.coords
+    say(f"workload 2: {len(coords)} voxels")
+    Ld, Lu = wl.layers
+    x = scenes.features(len(coords), Ld.c_in, "f16", 2002)
+    w = scenes.weights(2, Ld.c_in, Ld.c_out, "f16", 3002)
+    km, y = _conv_gpu(coords, x, w, 2, 2, 1, "down", dtype="f16")
+    q = oracle.out_coords(coords, 2, 1)
+    assert np.array_equal(km.out_coords().cpu().numpy(), q)
+    okm = oracle.kernel_map(coords, q, 2, 1, "down")
+    assert_map_equal(km, okm)
+    assert okm.counts.sum() == len(coords)
+    ref = oracle.features(scenes.to_f64(x, "f16"), scenes.to_f64(w, "f16"), okm)
+    assert rel_err(to_f64(y), ref) <= TOL["f16"]
+    # upsample back with the transposed map; the oracle uses its own inputs
+    xc = scenes.features(len(q), Lu.c_in, "f16", 2102)
+    wu = scenes.weights(2, Lu.c_in, Lu.c_out, "f16", 3102)
+    kt = km.transpose()
+    yu = B.Forward(kt, Lu.c_in, Lu.c_out, torch.float16)(to_dev(xc), to_dev(wu))
+    torch.cuda.synchronize()
+    oup = oracle.kernel_map(q, coords, 2, 1, "up")
+    assert_map_equal(kt, oup)
+    refu = oracle.features(scenes.to_f64(xc, "f16"), scenes.to_f64(wu, "f16"), oup)
+    assert rel_err(to_f64(yu), refu) <= TOL["f16"]
+
+
+# ----------------------------------------------------------------------------
+# Parity-neutral parameters, determinism, dtypes
+# ----------------------------------------------------------------------------
+
+def test_grouping_tiles_partials_are_result_neutral():
+    say("grouping / tiles / partial precision")
+    c = scenes.workload(1).coords[:40000].copy()
+    x = scenes.features(len(c), 64, "f16", 11)
+    w = scenes.weights(3, 64, 64, "f16", 12)
+    dc = to_dev(c)
+    km = B.KernelMap.build(dc, 3)
+    xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
+    base = B.Forward(km, 64, 64, torch.float16)(xd, wd)
+    infos = []
+    for g in (B.GROUP_RAGGED, B.GROUP_SORTED, B.GROUP_MAPORDER):
+        for tg, ts in ((8, 4), (16, 8), (64, 16), (32, 64)):
+            opt = B.Options.make(grouping=g, t_gather=tg, t_scatter=ts)
+            y = B.Forward(km, 64, 64, torch.float16, opt)(xd, wd)
+            assert torch.equal(y, base), f"grouping {g} tiles {tg}/{ts} changed the result"
+        infos.append(km.plan(64, 64, torch.float16, B.Options.make(grouping=g)))
+    # sorted grouping never pads more than map-order grouping with the same cost model
+    assert infos[0].rows_padded == infos[0].rows_real
+    assert infos[1].rows_padded <= infos[2].rows_padded
+    yp = B.Forward(km, 64, 64, torch.float16, B.Options.make(partial_dtype=1))(xd, wd)
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    ref = oracle.features(scenes.to_f64(x, "f16"), scenes.to_f64(w, "f16"), okm)
+    assert rel_err(to_f64(yp), ref) <= TOL["f16"]
+
+
+def test_deterministic_pairs():
+    say("deterministic pair order")
+    c = scenes.workload(1).coords
+    dc = to_dev(c)
+    a = gpu_pairs(B.KernelMap.build(dc, 3))
+    b = gpu_pairs(B.KernelMap.build(dc, 3))
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
+
+
+def test_bf16_layer():
+    say("bf16 layer")
+    c = _cloud(40, 5000, -12, 12)
+    x = scenes.features(len(c), 32, "bf16", 13)
+    w = scenes.weights(3, 32, 48, "bf16", 14)
+    km, y = _conv_gpu(c, x, w, 3, dtype="bf16")
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    ref = oracle.features(scenes.to_f64(x, "bf16"), scenes.to_f64(w, "bf16"), okm)
+    assert rel_err(to_f64(y), ref) <= TOL["bf16"]
+
+
+# ----------------------------------------------------------------------------
+# Edge cases and error paths
+# ----------------------------------------------------------------------------
+
+def test_empty_and_single():
+    say("empty and single-voxel inputs")
+    e = torch.zeros((0, 4), dtype=torch.int32, device=DEV)
+    km = B.KernelMap.build(e, 3)
+    assert km.n_out == 0 and sum(km.counts()) == 0
+    kd = B.KernelMap.build(e, 2, 2, 1, "down")
+    assert kd.n_out == 0
+    one = np.array([[3, -5, 7, 11]], np.int32)
+    x = np.ones((1, 4), np.float32)
+    w = scenes.weights(3, 4, 16, "f32", 1)
+    km1, y = _conv_gpu(one, x, w, 3)
+    cnt = km1.counts()
+    assert sum(cnt) == 1 and cnt[13] == 1
+    assert np.allclose(to_f64(y)[0], w[13].sum(0), rtol=1e-6)
+
+
+def test_isolated_rows_get_zeros():
+    say("rows without pairs")
+    c = np.array([[0, 0, 0, 0], [0, 10, 10, 10]], np.int32)
+    x = np.ones((2, 4), np.float32)
+    w = scenes.weights(3, 4, 16, "f32", 1)
+    w[13] = 0  # centre weight zero: both rows have only the centre pair
+    km, y = _conv_gpu(c, x, w, 3)
+    assert float(y.abs().max()) == 0.0
+
+
+def test_error_duplicates_and_range():
+    say("duplicate / out-of-range coordinates")
+    dup = to_dev(np.array([[0, 1, 2, 3], [0, 5, 5, 5], [0, 1, 2, 3]], np.int32))
+    with pytest.raises(B.SpconvError) as ei:
+        B.KernelMap.build(dup, 3)
+    assert ei.value.status == B.SPCONV_EDUP
+    big = to_dev(np.array([[0, -2**31, 0, -2**31], [0, 2**31 - 1, 2**31 - 1, 2**31 - 1]], np.int32))
+    with pytest.raises(B.SpconvError) as ei:
+        B.KernelMap.build(big, 3)
+    assert ei.value.status == B.SPCONV_ERANGE
+
+
+def test_error_forward_args():
+    say("forward argument errors")
+    c = _cloud(50, 100, -3, 3)
+    km = B.KernelMap.build(to_dev(c), 3)
+    with pytest.raises(B.SpconvError) as ei:
+        B.Forward(km, 16, 20, torch.float32)  # c_out not a multiple of 16
+    assert ei.value.status == B.SPCONV_EUNSUPPORTED
+    f = B.Forward(km, 16, 16, torch.float32)
+    tiny = torch.empty(1, dtype=torch.uint8, device=DEV)
+    with pytest.raises(B.SpconvError) as ei:
+        B.spconv_forward(km.handle, torch.zeros(len(c), 16, device=DEV), torch.zeros(27, 16, 16, device=DEV),
+                         torch.zeros(len(c), 16, device=DEV), 16, 16, B.SPCONV_F32, None, tiny)
+    assert ei.value.status == B.SPCONV_ENOSPC
+    _ = f

@@ -155,9 +155,10 @@ struct MapBufs {
   uint32_t* bounds;
   uint32_t* chunks;
   uint32_t* istart;
+  uint32_t* item_cnt;
+  uint32_t* item_off;
+  int32_t* mm_partial;
   void* scan_tmp;
-  int32_t* items;
-  uint64_t* status;
   int64_t max_items;
   int64_t nb;
 };
@@ -209,9 +210,10 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   b->bounds = m.take<uint32_t>(nkb);
   b->chunks = m.take<uint32_t>(nkb);
   b->istart = m.take<uint32_t>(nkb);
-  b->scan_tmp = m.take_bytes(scan_temp_bytes(std::max(nkb, n_src)));
-  b->items = m.take<int32_t>(2 * b->max_items);
-  b->status = m.take<uint64_t>(b->max_items);
+  b->item_cnt = m.take<uint32_t>(b->max_items);
+  b->item_off = m.take<uint32_t>(b->max_items);
+  b->mm_partial = static_cast<int32_t*>(m.take_bytes(minmax_temp_bytes()));
+  b->scan_tmp = m.take_bytes(scan_temp_bytes(std::max(std::max(nkb, n_src), b->max_items)));
   return align_up(m.off, 256);
 }
 
@@ -456,9 +458,8 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   KeyLayout L;
   {
     PhaseScope ph(PH_BOUNDS, s);
-    hipError_t e = launch_minmax_init(b.cb, s);
-    if (e == hipSuccess) e = launch_minmax(d_in_coords, n_in, b.cb, s);
-    if (e == hipSuccess && mode == SPCONV_UP) e = launch_minmax(d_out_coords, n_out, b.cb, s);
+    hipError_t e = launch_minmax(d_in_coords, n_in, d_out_coords, mode == SPCONV_UP ? n_out : 0, b.mm_partial,
+                                 b.cb, s);
     ControlBlock* h = static_cast<ControlBlock*>(staging(65536));
     if (!h) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
     if (e == hipSuccess) e = hipMemcpyAsync(h, b.cb, sizeof(ControlBlock), hipMemcpyDeviceToHost, s);
@@ -468,21 +469,17 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   }
   {
     PhaseScope ph(PH_SORT, s);
-    hipError_t e = launch_pack(src_coords, n_src, L, b.skeys, b.sidx, s);
-    if (e == hipSuccess) e = radix_sort_kv(b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
-    if (e == hipSuccess) e = launch_check_dup(b.skeys, n_src, b.cb, s);
-    if (e == hipSuccess && mode == SPCONV_UP) {
-      e = launch_pack(d_in_coords, n_in, L, b.qkeys, b.qrow, s);
-      if (e == hipSuccess) e = radix_sort_kv(b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits, b.sort_tmp, s);
-      if (e == hipSuccess) e = launch_check_dup(b.qkeys, n_in, b.cb, s);
-    }
+    hipError_t e = radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
+    if (e == hipSuccess && mode == SPCONV_UP)
+      e = radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits, b.sort_tmp, s);
     if (e != hipSuccess) return bail(hip_fail(e, "sort"));
   }
   if (mode == SPCONV_DOWN) {
     PhaseScope ph(PH_OUTCOORDS, s);
     const int64_t cell = (int64_t)tensor_stride * stride;
     hipError_t e = launch_down_keys(b.skeys, n_src, L, cell, b.dkeys, b.dvals, s);
-    if (e == hipSuccess) e = radix_sort_kv(b.dkeys, b.dvals, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
+    if (e == hipSuccess)
+      e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
     if (e == hipSuccess)
       e = unique_keys(b.dkeys, n_src, L, b.flags, b.pos, b.scan_tmp, b.qkeys, b.qrow, b.qcoords, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "output coordinates"));
@@ -502,40 +499,43 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   a.B = tu.B;
   a.Cq = tu.Cq;
   a.swap_roles = (mode == SPCONV_UP) ? 1 : 0;
+  a.check_q = (mode == SPCONV_UP) ? 1 : 0;
   {
     PhaseScope ph(PH_BACKWARD, s);
-    hipError_t e = launch_backward(a, b.nb, b.bounds, s);
+    hipError_t e = launch_backward(a, b.nb, b.bounds, b.chunks, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "backward search"));
   }
   {
     PhaseScope ph(PH_BALANCE, s);
-    hipError_t e = balance(a, b.nb, b.bounds, b.chunks, b.istart, b.scan_tmp, b.items, b.status, b.max_items, b.cb, s);
-    if (e == hipSuccess) e = launch_fill_u32(b.counts, 0u, K3, s);
+    hipError_t e = scan_exclusive_u32(b.chunks, b.istart, (int64_t)K3 * b.nb, &b.cb->n_items, b.scan_tmp, s);
     if (e != hipSuccess) return bail(hip_fail(e, "balance"));
   }
   {
     PhaseScope ph(PH_FORWARD, s);
-    hipError_t e = launch_forward(a, b.bounds, b.nb, b.items, b.status, b.max_items, b.pin, b.pout, b.counts, b.cb, s);
+    hipError_t e = launch_forward(a, false, b.bounds, b.nb, b.istart, b.item_cnt, nullptr, b.max_items, b.pin,
+                                  b.pout, b.cb, s);
+    if (e == hipSuccess) e = scan_exclusive_u32(b.item_cnt, b.item_off, b.max_items, &b.cb->n_pairs, b.scan_tmp, s);
+    if (e == hipSuccess)
+      e = launch_forward(a, true, b.bounds, b.nb, b.istart, b.item_cnt, b.item_off, b.max_items, b.pin, b.pout,
+                         b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "forward search"));
   }
   {
     PhaseScope ph(PH_READBACK, s);
-    char* h = static_cast<char*>(staging(65536));
-    if (!h) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
-    ControlBlock* hc = reinterpret_cast<ControlBlock*>(h);
-    uint32_t* hcnt = reinterpret_cast<uint32_t*>(h + 4096);
+    ControlBlock* hc = static_cast<ControlBlock*>(staging(65536));
+    if (!hc) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
     hipError_t e = hipMemcpyAsync(hc, b.cb, sizeof(ControlBlock), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(hcnt, b.counts, sizeof(uint32_t) * K3, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return bail(hip_fail(e, "count read-back"));
     if (hc->err & kErrDup) return bail(fail(SPCONV_EDUP, "duplicate coordinates"));
-    if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "forward search look-back exceeded its wait bound"));
     if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "work-item overflow in the balance step"));
+    if (hc->n_items > (uint32_t)b.max_items) return bail(fail(SPCONV_EHIP, "work items exceed the launch bound"));
     if (mode == SPCONV_DOWN) m->n_out = hc->n_q;
     for (int k = 0; k < K3; ++k) {
-      m->counts[k] = hcnt[k];
-      m->ptr[k + 1] = m->ptr[k] + hcnt[k];
+      m->counts[k] = (int64_t)hc->seg_pair_start[k + 1] - hc->seg_pair_start[k];
+      m->ptr[k + 1] = hc->seg_pair_start[k + 1];
     }
+    if (m->ptr[K3] != hc->n_pairs) return bail(fail(SPCONV_EHIP, "pair count mismatch"));
   }
   *out_map = m;
   return SPCONV_OK;

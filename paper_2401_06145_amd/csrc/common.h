@@ -47,31 +47,23 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 
 __device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
 
-// Device-scope (agent) atomics on 64-bit status words used by the look-back scans.
-__device__ __forceinline__ uint64_t ld_acquire_agent(uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_release_agent(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // ---------------------------------------------------------------------------
 // Device error flags, OR-ed into ControlBlock::err by kernels.
 // ---------------------------------------------------------------------------
 enum : uint32_t {
   kErrDup = 1u,          // two equal keys among the sorted inputs
-  kErrSpin = 2u,         // a look-back wait exceeded its bound
   kErrOverflow = 4u,     // more work items than the launch was sized for
 };
 
 // Small control block in device memory, read back once at the end of a map build.
+constexpr int kMaxOffsets = 125;  // K <= 5
 struct ControlBlock {
-  int32_t minmax[8];     // min b,x,y,z then max b,x,y,z (coordinate bounds pass)
-  uint32_t err;          // kErr* flags
-  uint32_t n_q;          // number of distinct output coordinates (DOWN)
-  uint32_t n_items;      // forward-search work items emitted by the balance step
-  uint32_t ticket;       // work-item ticket counter of the forward search
-  uint32_t pad[4];
+  int32_t minmax[8];      // min b,x,y,z then max b,x,y,z (coordinate bounds pass)
+  uint32_t err;           // kErr* flags
+  uint32_t n_q;           // number of distinct output coordinates (DOWN)
+  uint32_t n_items;       // forward-search work items of the balance step
+  uint32_t n_pairs;       // total matches
+  uint32_t seg_pair_start[kMaxOffsets + 3];  // first pair of offset k; [K3] = n_pairs
 };
 
 // ---------------------------------------------------------------------------
@@ -85,22 +77,24 @@ hipError_t scan_exclusive_u32(const uint32_t* d_in, uint32_t* d_out, int64_t n, 
 
 // map_kernels.hip
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
-hipError_t launch_minmax_init(ControlBlock* cb, hipStream_t s);
-hipError_t launch_minmax(const int32_t* coords, int64_t n, ControlBlock* cb, hipStream_t s);
+size_t minmax_temp_bytes();
+// Coordinate bounds of a[0..na) and b[0..nb) into cb->minmax; also resets cb.
+hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t nb, int32_t* partial,
+                         ControlBlock* cb, hipStream_t s);
 hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals,
                        hipStream_t s);
 size_t radix_temp_bytes(int64_t n);
-// Sorts (keys, vals) by the low `bits` key bits; the result ends in (keys, vals).
-hipError_t radix_sort_kv(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt,
-                         int64_t n, int bits, void* d_temp, hipStream_t s);
-hipError_t launch_check_dup(const uint64_t* keys, int64_t n, ControlBlock* cb, hipStream_t s);
+// Sorts by the low `bits` key bits; the result ends in (keys, vals).  If `coords` is
+// non-null the input is those coordinates (keys packed with L, values = row index).
+hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals,
+                         uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, int bits, void* d_temp,
+                         hipStream_t s);
 hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell,
                             uint64_t* dkeys, uint32_t* vals, hipStream_t s);
 // Distinct consecutive keys of sorted `keys` -> qkeys, qrow = position, coords; n_q into cb.
 hipError_t unique_keys(const uint64_t* keys, int64_t n, KeyLayout L, uint32_t* flags,
                        uint32_t* pos, void* d_temp, uint64_t* qkeys, uint32_t* qrow,
                        int32_t* out_coords, ControlBlock* cb, hipStream_t s);
-hipError_t launch_unpack(const uint64_t* keys, int64_t n, KeyLayout L, int32_t* coords, hipStream_t s);
 
 struct SearchArgs {
   const uint64_t* skeys;  // sorted source keys [n_src]
@@ -111,24 +105,24 @@ struct SearchArgs {
   int64_t n_q;
   const uint32_t* n_q_dev;
   int K3;
-  int64_t dk[125];        // key delta of each offset
+  int64_t dk[kMaxOffsets];  // key delta of each offset
   int B;                  // source block size
   int Cq;                 // query block limit
   int swap_roles;         // UP: pairs are (query row, source row)
+  int check_q;            // also check the query keys for repeats
 };
-// Section 5.1.2: backward search, then balance (chunks, scan, emit).
-hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, hipStream_t s);
-hipError_t balance(const SearchArgs& a, int64_t nb, const uint32_t* bounds, uint32_t* chunks,
-                   uint32_t* item_start, void* d_temp, int32_t* items, uint64_t* status,
-                   int64_t max_items, ControlBlock* cb, hipStream_t s);
-// Forward search with in-order compaction of matches into per-offset pair lists.
-hipError_t launch_forward(const SearchArgs& a, const uint32_t* bounds, int64_t nb,
-                          const int32_t* items, uint64_t* status, int64_t max_items,
-                          int32_t* pin, int32_t* pout, uint32_t* counts, ControlBlock* cb,
+// Section 5.1.2, backward search fused with the per-(k, b) chunk counts of the
+// balancing step (and the duplicate-key check).
+hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, uint32_t* chunks,
+                           ControlBlock* cb, hipStream_t s);
+// Forward search over the balanced work items: count pass (write = false) fills
+// item_cnt; write pass places pairs at item_off and fills cb->seg_pair_start.
+hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, int64_t nb,
+                          const uint32_t* istart, uint32_t* item_cnt, const uint32_t* item_off,
+                          int64_t max_items, int32_t* pin, int32_t* pout, ControlBlock* cb,
                           hipStream_t s);
 
 // gmas_kernels.hip
-constexpr int kMaxOffsets = 125;  // K <= 5
 struct OffsetTable {
   int K3;
   int64_t pair_start[kMaxOffsets + 1];  // prefix of |M_k| in the concatenated pair lists

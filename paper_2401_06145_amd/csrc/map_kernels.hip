@@ -1,6 +1,11 @@
 // Map step kernels (Section 5.1): coordinate keys, radix sort, output
 // coordinates (Eq. 1), and the segmented-query double-traversed binary search
 // (Section 5.1.2) with in-order compaction of matches into per-offset pair lists.
+//
+// MI355X notes: atomics on one address from many workgroups serialise across the
+// eight XCDs, so no kernel here has such a hot spot: reductions go through
+// per-block partials, and the match compaction is count -> scan -> write
+// (re-running the cheap LDS search) instead of a single pass with a look-back.
 #include <climits>
 
 #include "common.h"
@@ -9,10 +14,10 @@ namespace spc {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kWavesPerBlock = kThreads / kWave;
 
 __global__ void k_fill_u32(uint32_t* p, uint32_t v, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
     p[i] = v;
 }
 
@@ -24,33 +29,22 @@ unsigned grid_for(int64_t n, int per_block = kThreads, int64_t cap = 1 << 20) {
 }
 
 // ----------------------------------------------------------------------------
-// Coordinate bounds (for the key layout)
+// Coordinate bounds: per-block partial min / max, then one block reduces them.
 // ----------------------------------------------------------------------------
-__global__ void k_minmax_init(ControlBlock* cb) {
-  const int t = threadIdx.x;
-  if (t < 4) {
-    cb->minmax[t] = INT_MAX;
-    cb->minmax[4 + t] = INT_MIN;
-  }
-  if (t == 0) {
-    cb->err = 0;
-    cb->n_q = 0;
-    cb->n_items = 0;
-    cb->ticket = 0;
-  }
-}
+constexpr int kMinmaxBlocks = 256;
 
-__global__ __launch_bounds__(kThreads) void k_minmax(const int4* c, int64_t n, ControlBlock* cb) {
+__global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int64_t na, const int4* b, int64_t nb,
+                                                             int32_t* partial) {
   int32_t mn[4] = {INT_MAX, INT_MAX, INT_MAX, INT_MAX};
   int32_t mx[4] = {INT_MIN, INT_MIN, INT_MIN, INT_MIN};
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int4 v = c[i];
-    const int32_t a[4] = {v.x, v.y, v.z, v.w};
+  const int64_t n = na + nb;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int4 v = (i < na) ? a[i] : b[i - na];
+    const int32_t c[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int f = 0; f < 4; ++f) {
-      mn[f] = min(mn[f], a[f]);
-      mx[f] = max(mx[f], a[f]);
+      mn[f] = min(mn[f], c[f]);
+      mx[f] = max(mx[f], c[f]);
     }
   }
 #pragma unroll
@@ -61,17 +55,41 @@ __global__ __launch_bounds__(kThreads) void k_minmax(const int4* c, int64_t n, C
       mx[f] = max(mx[f], __shfl_xor(mx[f], off, kWave));
     }
   }
+  __shared__ int32_t s[kWavesPerBlock][8];
+  const int wave = threadIdx.x / kWave;
   if ((threadIdx.x & (kWave - 1)) == 0) {
 #pragma unroll
     for (int f = 0; f < 4; ++f) {
-      atomicMin(&cb->minmax[f], mn[f]);
-      atomicMax(&cb->minmax[4 + f], mx[f]);
+      s[wave][f] = mn[f];
+      s[wave][4 + f] = mx[f];
     }
+  }
+  __syncthreads();
+  if (threadIdx.x < 8) {
+    const int f = threadIdx.x;
+    int32_t r = s[0][f];
+    for (int w = 1; w < kWavesPerBlock; ++w) r = (f < 4) ? min(r, s[w][f]) : max(r, s[w][f]);
+    partial[blockIdx.x * 8 + f] = r;
+  }
+}
+
+__global__ void k_minmax_final(const int32_t* partial, int nblocks, ControlBlock* cb) {
+  const int f = threadIdx.x;
+  if (f < 8) {
+    int32_t r = (f < 4) ? INT_MAX : INT_MIN;
+    for (int i = 0; i < nblocks; ++i) r = (f < 4) ? min(r, partial[i * 8 + f]) : max(r, partial[i * 8 + f]);
+    cb->minmax[f] = r;
+  }
+  if (f == 0) {
+    cb->err = 0;
+    cb->n_q = 0;
+    cb->n_items = 0;
+    cb->n_pairs = 0;
   }
 }
 
 // ----------------------------------------------------------------------------
-// Key packing
+// Key packing helpers
 // ----------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, KeyLayout L, uint64_t* keys,
                                                    uint32_t* vals) {
@@ -83,22 +101,11 @@ __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, Key
   vals[i] = (uint32_t)i;
 }
 
-__global__ __launch_bounds__(kThreads) void k_unpack(const uint64_t* keys, int64_t n, KeyLayout L, int4* c) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const uint64_t k = keys[i];
-  c[i] = make_int4(key_field(L, k, 0), key_field(L, k, 1), key_field(L, k, 2), key_field(L, k, 3));
-}
-
-__global__ __launch_bounds__(kThreads) void k_check_dup(const uint64_t* keys, int64_t n, ControlBlock* cb) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x + 1;
-  if (i < n && keys[i] == keys[i - 1]) atomicOr(&cb->err, kErrDup);
-}
-
 // ----------------------------------------------------------------------------
 // LSD radix sort of (u64 key, u32 value), 8-bit digits, stable.
 // Per pass: per-tile digit histograms -> exclusive scan (digit-major) -> stable
-// scatter.  Ranks inside a tile come from wave64 ballots that match equal digits.
+// scatter.  Ranks inside a tile come from wave64 ballots that match equal
+// digits.  The first pass may read int32 coordinates and pack the keys itself.
 // ----------------------------------------------------------------------------
 constexpr int kRsItems = 8;
 constexpr int kRsTile = kThreads * kRsItems;
@@ -115,8 +122,20 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d) {
   return m;
 }
 
-__global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t* keys, int64_t n, int shift,
-                                                         uint32_t* hist, int64_t ntiles) {
+template <bool FROM_COORDS>
+__device__ __forceinline__ uint64_t load_key(const uint64_t* keys, const int4* coords, const KeyLayout& L, int64_t i) {
+  if constexpr (FROM_COORDS) {
+    const int4 v = coords[i];
+    const int32_t a[4] = {v.x, v.y, v.z, v.w};
+    return pack_key(L, a);
+  } else {
+    return keys[i];
+  }
+}
+
+template <bool FROM_COORDS>
+__global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t* keys, const int4* coords, KeyLayout L,
+                                                         int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
   __syncthreads();
@@ -125,7 +144,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t* keys, i
   for (int r = 0; r < kRsItems; ++r) {
     const int64_t i = base + r * kThreads + threadIdx.x;
     if (i < n) {
-      const uint32_t d = (uint32_t)(keys[i] >> shift) & 255u;
+      const uint32_t d = (uint32_t)(load_key<FROM_COORDS>(keys, coords, L, i) >> shift) & 255u;
       const uint64_t peers = match_digit(d);
       if ((peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)popc64(peers));
     }
@@ -134,17 +153,18 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t* keys, i
   hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
+template <bool FROM_COORDS>
 __global__ __launch_bounds__(kThreads) void k_radix_scatter(const uint64_t* kin, const uint32_t* vin,
-                                                            uint64_t* kout, uint32_t* vout, int64_t n,
-                                                            int shift, const uint32_t* offs,
-                                                            int64_t ntiles) {
+                                                            const int4* coords, KeyLayout L, uint64_t* kout,
+                                                            uint32_t* vout, int64_t n, int shift,
+                                                            const uint32_t* offs, int64_t ntiles) {
   __shared__ uint32_t run[256];
-  __shared__ uint32_t wcnt[kThreads / kWave][256];
+  __shared__ uint32_t wcnt[kWavesPerBlock][256];
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   run[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
 #pragma unroll
-  for (int w = 0; w < kThreads / kWave; ++w) wcnt[w][tid] = 0;
+  for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][tid] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * kRsTile;
   for (int r = 0; r < kRsItems; ++r) {
@@ -153,8 +173,8 @@ __global__ __launch_bounds__(kThreads) void k_radix_scatter(const uint64_t* kin,
     uint64_t key = 0;
     uint32_t val = 0, d = 0, rank = 0;
     if (valid) {
-      key = kin[i];
-      val = vin[i];
+      key = load_key<FROM_COORDS>(kin, coords, L, i);
+      val = FROM_COORDS ? (uint32_t)i : vin[i];
       d = (uint32_t)(key >> shift) & 255u;
       const uint64_t peers = match_digit(d);
       rank = (uint32_t)popc64(peers & lanemask_lt());
@@ -170,7 +190,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_scatter(const uint64_t* kin,
     __syncthreads();
     uint32_t add = 0;
 #pragma unroll
-    for (int w = 0; w < kThreads / kWave; ++w) {
+    for (int w = 0; w < kWavesPerBlock; ++w) {
       add += wcnt[w][tid];
       wcnt[w][tid] = 0;
     }
@@ -189,8 +209,8 @@ __device__ __forceinline__ int64_t floor_to_cell(int64_t v, int64_t cell) {
   return q * cell;
 }
 
-__global__ __launch_bounds__(kThreads) void k_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L,
-                                                        int64_t cell, uint64_t* dkeys, uint32_t* vals) {
+__global__ __launch_bounds__(kThreads) void k_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell,
+                                                        uint64_t* dkeys, uint32_t* vals) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const uint64_t k = skeys[i];
@@ -221,27 +241,17 @@ __global__ __launch_bounds__(kThreads) void k_unique_write(const uint64_t* keys,
 }
 
 // ----------------------------------------------------------------------------
-// Backward binary search (Section 5.1.2): for source block b and offset k, the
-// query block is the run of sorted queries q with key(q) + dk in
-// (pivot_{b-1}, pivot_b], pivot_b being the block's last key.  bounds[k][b] is
-// the number of queries with key(q) + dk <= pivot_b (an upper bound), found by
-// one wave with a 64-way ballot search: each round every lane tests one probe.
+// 64-way wave search: number of entries of sorted a[0..n) that are <= thr
+// (each round every lane tests one probe; ~log64(n) dependent loads).
 // ----------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb, uint32_t* bounds) {
+template <typename T, typename V>
+__device__ __forceinline__ int64_t wave_upper_bound(const T* a, int64_t n, V thr) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t wid = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
-  if (wid >= (int64_t)a.K3 * nb) return;  // wave-uniform
-  const int k = (int)(wid / nb);
-  const int64_t b = wid - (int64_t)k * nb;
-  const int64_t nq = a.n_q_dev ? (int64_t)*a.n_q_dev : a.n_q;
-  const int64_t last = min((b + 1) * (int64_t)a.B, a.n_src) - 1;
-  // key(q) + dk <= pivot  <=>  key(q) <= pivot - dk, evaluated in signed 64 bits
-  const int64_t thr = (int64_t)a.skeys[last] - a.dk[k];
-  int64_t lo = 0, hi = nq;  // answer in [lo, hi]
+  int64_t lo = 0, hi = n;  // answer in [lo, hi]
   while (hi - lo > kWave) {
     const int64_t step = (hi - lo + kWave - 1) / kWave;
     const int64_t pos = lo + (int64_t)(lane + 1) * step - 1;
-    const bool pred = pos < hi && (int64_t)a.qkeys[pos] <= thr;
+    const bool pred = pos < hi && (V)a[pos] <= thr;
     const int c = popc64(__ballot(pred));
     const int64_t nlo = lo + (int64_t)c * step;
     const int64_t nhi = min(lo + (int64_t)(c + 1) * step - 1, hi);
@@ -249,89 +259,118 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
     hi = nhi;
   }
   const int64_t pos = lo + lane;
-  const bool pred = pos < hi && (int64_t)a.qkeys[pos] <= thr;
-  const int64_t ub = lo + popc64(__ballot(pred));
-  if (lane == 0) bounds[wid] = (uint32_t)ub;
+  const bool pred = pos < hi && (V)a[pos] <= thr;
+  return lo + popc64(__ballot(pred));
 }
 
-// Balance (Section 5.1.2): query blocks larger than Cq are split into chunks.
-__global__ __launch_bounds__(kThreads) void k_chunks(const uint32_t* bounds, int64_t nkb, int64_t nb, int Cq,
-                                                     uint32_t* chunks) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= nkb) return;
-  const int64_t b = i % nb;
-  const uint32_t lo = (b == 0) ? 0u : bounds[i - 1];
-  const uint32_t hi = bounds[i];
-  chunks[i] = (hi - lo + (uint32_t)Cq - 1u) / (uint32_t)Cq;
-}
-
-__global__ __launch_bounds__(kThreads) void k_emit(const uint32_t* chunks, const uint32_t* start, int64_t nkb,
-                                                   int2* items, uint64_t* status, int64_t max_items,
-                                                   ControlBlock* cb) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0) cb->ticket = 0;
-  if (i >= nkb) return;
-  const uint32_t c = chunks[i];
-  const uint32_t s = start[i];
-  for (uint32_t j = 0; j < c; ++j) {
-    const int64_t w = (int64_t)s + j;
-    if (w >= max_items) {
-      atomicOr(&cb->err, kErrOverflow);
-      return;
+// ----------------------------------------------------------------------------
+// Backward binary search (Section 5.1.2) fused with the balancing count.  For
+// source block b and offset k the query block is the run of sorted queries q
+// with key(q) + dk in (pivot_{b-1}, pivot_b], pivot_b being the block's last
+// key.  One wave per (k, b) finds bounds[k][b] = #{q : key(q) + dk <= pivot_b}
+// and the same for pivot_{b-1}, and writes the number of <= Cq chunks the
+// query block splits into.  The k = 0 waves also check the sorted keys for
+// repeats (a point cloud is a set).
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb, uint32_t* bounds, uint32_t* chunks,
+                                                       ControlBlock* cb) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wid = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
+  if (wid >= (int64_t)a.K3 * nb) return;  // wave-uniform
+  const int k = (int)(wid / nb);
+  const int64_t b = wid - (int64_t)k * nb;
+  const int64_t nq = a.n_q_dev ? (int64_t)*a.n_q_dev : a.n_q;
+  const int64_t dk = a.dk[k];
+  // key(q) + dk <= pivot  <=>  key(q) <= pivot - dk, evaluated in signed 64 bits
+  const int64_t last = min((b + 1) * (int64_t)a.B, a.n_src) - 1;
+  const int64_t hi = wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, (int64_t)a.skeys[last] - dk);
+  const int64_t lo = (b == 0) ? 0 : wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, (int64_t)a.skeys[b * a.B - 1] - dk);
+  if (lane == 0) {
+    bounds[wid] = (uint32_t)hi;
+    chunks[wid] = (uint32_t)((hi - lo + a.Cq - 1) / a.Cq);
+  }
+  if (k == 0) {
+    bool dup = false;
+    const int64_t s0 = b * (int64_t)a.B;
+    for (int64_t e = s0 + lane; e <= last; e += kWave) dup |= (e > 0 && a.skeys[e] == a.skeys[e - 1]);
+    if (a.check_q) {
+      const int64_t per = (nq + nb - 1) / nb;
+      for (int64_t e = b * per + lane; e < min((b + 1) * per, nq); e += kWave) dup |= (e > 0 && a.qkeys[e] == a.qkeys[e - 1]);
     }
-    items[w] = make_int2((int)i, (int)j);
-    status[w] = 0ull;
+    if (__ballot(dup) != 0 && lane == 0) atomicOr(&cb->err, kErrDup);
   }
 }
 
 // ----------------------------------------------------------------------------
-// Forward binary search (Section 5.1.2) + compaction.  One workgroup per
-// load-balanced query block: the source block goes to LDS, each lane binary-
-// searches its queries there.  Matches are ranked with wave ballots and the
-// workgroup's base position comes from a decoupled look-back over work items,
-// so the pair lists are written in (offset, sorted query) order in one pass.
+// Forward binary search (Section 5.1.2).  One workgroup per load-balanced
+// query block (work item): the source block is staged in LDS and each lane
+// binary-searches its queries there.  COUNT pass: matches per work item.  WRITE
+// pass: the same search, matches ranked with wave ballots and written at the
+// scanned offset, so every offset's pairs come out in sorted-query order.
 // ----------------------------------------------------------------------------
-constexpr uint64_t kFlagAgg = 1ull << 62;
-constexpr uint64_t kFlagIncl = 2ull << 62;
-constexpr uint64_t kValMask = (1ull << 62) - 1ull;
-constexpr uint32_t kSpinLimit = 1u << 22;
+struct ItemRange {
+  int k;
+  int64_t b, q0, q1;
+};
 
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
+__device__ __forceinline__ ItemRange locate_item(const SearchArgs& a, int64_t w, int64_t nb, const uint32_t* bounds,
+                                                 const uint32_t* istart, int64_t* s_kb) {
+  if (threadIdx.x < kWave) {
+    // last (k, b) whose first item index is <= w
+    const int64_t kb = wave_upper_bound<uint32_t, int64_t>(istart, (int64_t)a.K3 * nb, w) - 1;
+    if (threadIdx.x == 0) *s_kb = kb;
+  }
+  __syncthreads();
+  const int64_t kb = *s_kb;
+  ItemRange r;
+  r.k = (int)(kb / nb);
+  r.b = kb - (int64_t)r.k * nb;
+  const int64_t blo = (r.b == 0) ? 0 : (int64_t)bounds[kb - 1];
+  const int64_t bhi = bounds[kb];
+  r.q0 = blo + (w - (int64_t)istart[kb]) * a.Cq;
+  r.q1 = min(r.q0 + (int64_t)a.Cq, bhi);
+  return r;
 }
 
-template <int ROUNDS>
+__device__ __forceinline__ int lds_lower(const uint64_t* lkey, int nB, int log2B, uint64_t key) {
+  // number of LDS keys < key, by binary lifting over a power-of-two range
+  int pos = 0;
+  for (int step = 1 << (log2B - 1); step > 0; step >>= 1)
+    if (pos + step <= nB && lkey[pos + step - 1] < key) pos += step;
+  if (pos < nB && lkey[pos] < key) ++pos;
+  return pos;
+}
+
+template <int ROUNDS, bool WRITE>
 __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32_t* bounds, int64_t nb,
-                                                      const int2* items, uint64_t* status, int32_t* pin,
-                                                      int32_t* pout, uint32_t* counts, ControlBlock* cb,
-                                                      int log2B) {
+                                                      const uint32_t* istart, uint32_t* item_cnt,
+                                                      const uint32_t* item_off, int32_t* pin, int32_t* pout,
+                                                      ControlBlock* cb, int log2B) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ uint32_t s_ticket;
-  __shared__ uint32_t s_cnt[ROUNDS][kThreads / kWave];
-  __shared__ uint64_t s_base;
+  __shared__ int64_t s_kb;
+  __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
   uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
   uint32_t* lidx = reinterpret_cast<uint32_t*>(smem + sizeof(uint64_t) * a.B);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
+  const int64_t w = blockIdx.x;
+  const int64_t n_items = cb->n_items;
 
-  if (tid == 0) s_ticket = atomicAdd(&cb->ticket, 1u);
-  __syncthreads();
-  const uint32_t w = s_ticket;
-  if (w >= cb->n_items) return;  // workgroup-uniform; later tickets are idle too
+  if (WRITE && w == 0 && tid <= a.K3) {
+    // per-offset pair counts: the items of offset k are [istart[k nb], istart[(k+1) nb])
+    const int k = tid;
+    const int64_t first = (k < a.K3) ? (int64_t)istart[(int64_t)k * nb] : n_items;
+    const uint64_t off = (first < n_items) ? (uint64_t)item_off[first] : (uint64_t)cb->n_pairs;
+    cb->seg_pair_start[k] = (uint32_t)off;
+  }
+  if (w >= n_items) {  // workgroup-uniform; idle items count zero matches
+    if (!WRITE && tid == 0) item_cnt[w] = 0;
+    return;
+  }
 
-  const int2 it = items[w];
-  const int64_t kb = it.x;
-  const int k = (int)(kb / nb);
-  const int64_t b = kb - (int64_t)k * nb;
-  const int64_t blo = (b == 0) ? 0 : (int64_t)bounds[kb - 1];
-  const int64_t bhi = bounds[kb];
-  const int64_t q0 = blo + (int64_t)it.y * a.Cq;
-  const int64_t q1 = min(q0 + (int64_t)a.Cq, bhi);
-
-  const int64_t s0 = b * (int64_t)a.B;
+  const ItemRange it = locate_item(a, w, nb, bounds, istart, &s_kb);
+  const int64_t s0 = it.b * (int64_t)a.B;
   const int nB = (int)min((int64_t)a.B, a.n_src - s0);
   for (int e = tid; e < nB; e += kThreads) {
     lkey[e] = a.skeys[s0 + e];
@@ -339,83 +378,47 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
   }
   __syncthreads();
 
-  const int64_t dk = a.dk[k];
+  const uint64_t dk = (uint64_t)a.dk[it.k];
   int32_t r_in[ROUNDS], r_out[ROUNDS];
   uint64_t bal[ROUNDS];
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
-    const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+    const int64_t qp = it.q0 + (int64_t)r * kThreads + tid;
     bool hit = false;
     r_in[r] = 0;
     r_out[r] = 0;
-    if (qp < q1) {
-      const uint64_t key = a.qkeys[qp] + (uint64_t)dk;
-      // number of LDS keys < key, by binary lifting over a power-of-two range
-      int pos = 0;
-      for (int step = 1 << (log2B - 1); step > 0; step >>= 1)
-        if (pos + step <= nB && lkey[pos + step - 1] < key) pos += step;
-      if (pos < nB && lkey[pos] < key) ++pos;
+    if (qp < it.q1) {
+      const uint64_t key = a.qkeys[qp] + dk;
+      const int pos = lds_lower(lkey, nB, log2B, key);
       if (pos < nB && lkey[pos] == key) {
         hit = true;
-        const int32_t src = (int32_t)lidx[pos];
-        const int32_t qry = (int32_t)a.qrow[qp];
-        r_in[r] = a.swap_roles ? qry : src;
-        r_out[r] = a.swap_roles ? src : qry;
+        if (WRITE) {
+          const int32_t src = (int32_t)lidx[pos];
+          const int32_t qry = (int32_t)a.qrow[qp];
+          r_in[r] = a.swap_roles ? qry : src;
+          r_out[r] = a.swap_roles ? src : qry;
+        }
       }
     }
     bal[r] = __ballot(hit);
     if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal[r]);
   }
   __syncthreads();
-
-  // block-local exclusive offsets in (round, wave) order
   uint32_t total = 0;
   uint32_t before[ROUNDS];
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
 #pragma unroll
-    for (int v = 0; v < kThreads / kWave; ++v) {
+    for (int v = 0; v < kWavesPerBlock; ++v) {
       if (v == wave) before[r] = total;
       total += s_cnt[r][v];
     }
   }
-
-  if (wave == 0) {
-    uint64_t excl = 0;
-    if (w == 0) {
-      if (lane == 0) st_release_agent(&status[0], kFlagIncl | (uint64_t)total);
-    } else {
-      if (lane == 0) st_release_agent(&status[w], kFlagAgg | (uint64_t)total);
-      int64_t p = (int64_t)w - 1;
-      uint32_t spins = 0;
-      while (true) {
-        const int64_t idx = p - lane;
-        const uint64_t sv = (idx >= 0) ? ld_acquire_agent(&status[idx]) : kFlagIncl;
-        const uint32_t flag = (uint32_t)(sv >> 62);
-        if (__ballot(flag == 0) != 0) {
-          if (++spins > kSpinLimit) {
-            if (lane == 0) atomicOr(&cb->err, kErrSpin);
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-          continue;
-        }
-        const uint64_t incl = __ballot(flag == 2);
-        const uint64_t val = sv & kValMask;
-        if (incl != 0) {
-          const int first = __ffsll((unsigned long long)incl) - 1;
-          excl += wave_sum_u64(lane <= first ? val : 0ull);
-          break;
-        }
-        excl += wave_sum_u64(val);
-        p -= kWave;
-      }
-      if (lane == 0) st_release_agent(&status[w], kFlagIncl | (excl + (uint64_t)total));
-    }
-    if (lane == 0) s_base = excl;
+  if (!WRITE) {
+    if (tid == 0) item_cnt[w] = total;
+    return;
   }
-  __syncthreads();
-  const uint64_t base = s_base;
+  const uint64_t base = item_off[w];
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
     if ((bal[r] >> lane) & 1ull) {
@@ -424,7 +427,27 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
       pout[o] = r_out[r];
     }
   }
-  if (tid == 0 && total != 0) atomicAdd(&counts[k], total);
+}
+
+template <bool WRITE>
+hipError_t forward_t(int rounds, unsigned grid, size_t lds, hipStream_t s, const SearchArgs& a,
+                     const uint32_t* bounds, int64_t nb, const uint32_t* istart, uint32_t* item_cnt,
+                     const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb, int log2B) {
+  switch (rounds) {
+#define SPC_F(R)                                                                                                    \
+  case R:                                                                                                           \
+    hipLaunchKernelGGL((k_forward<R, WRITE>), dim3(grid), dim3(kThreads), lds, s, a, bounds, nb, istart, item_cnt, \
+                       item_off, pin, pout, cb, log2B);                                                             \
+    break;
+    SPC_F(1)
+    SPC_F(2)
+    SPC_F(4)
+    SPC_F(8)
+#undef SPC_F
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -438,36 +461,23 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_minmax_init(ControlBlock* cb, hipStream_t s) {
-  hipLaunchKernelGGL(k_minmax_init, dim3(1), dim3(64), 0, s, cb);
+size_t minmax_temp_bytes() { return (size_t)kMinmaxBlocks * 8 * sizeof(int32_t); }
+
+hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t nb, int32_t* partial,
+                         ControlBlock* cb, hipStream_t s) {
+  const unsigned g = grid_for(na + nb, kThreads * 8, kMinmaxBlocks);
+  hipLaunchKernelGGL(k_minmax_partial, dim3(g), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(a), na,
+                     reinterpret_cast<const int4*>(b), nb, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_minmax_final, dim3(1), dim3(64), 0, s, partial, (int)g, cb);
   return hipGetLastError();
 }
 
-hipError_t launch_minmax(const int32_t* coords, int64_t n, ControlBlock* cb, hipStream_t s) {
+hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_minmax, dim3(grid_for(n, kThreads, 1024)), dim3(kThreads), 0, s,
-                     reinterpret_cast<const int4*>(coords), n, cb);
-  return hipGetLastError();
-}
-
-hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals,
-                       hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_pack, dim3(grid_for(n)), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(coords),
-                     n, L, keys, vals);
-  return hipGetLastError();
-}
-
-hipError_t launch_unpack(const uint64_t* keys, int64_t n, KeyLayout L, int32_t* coords, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_unpack, dim3(grid_for(n)), dim3(kThreads), 0, s, keys, n, L,
-                     reinterpret_cast<int4*>(coords));
-  return hipGetLastError();
-}
-
-hipError_t launch_check_dup(const uint64_t* keys, int64_t n, ControlBlock* cb, hipStream_t s) {
-  if (n <= 1) return hipSuccess;
-  hipLaunchKernelGGL(k_check_dup, dim3(grid_for(n - 1)), dim3(kThreads), 0, s, keys, n, cb);
+  hipLaunchKernelGGL(k_pack, dim3(grid_for(n)), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(coords), n, L,
+                     keys, vals);
   return hipGetLastError();
 }
 
@@ -477,40 +487,52 @@ size_t radix_temp_bytes(int64_t n) {
   return (((size_t)nh * sizeof(uint32_t) + 255) & ~(size_t)255) + scan_temp_bytes(nh);
 }
 
-hipError_t radix_sort_kv(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
-                         int bits, void* d_temp, hipStream_t s) {
-  if (n <= 1 || bits <= 0) return hipSuccess;
+hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+                         uint32_t* vals_alt, int64_t n, int bits, void* d_temp, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int passes = (bits + 7) / 8;
+  if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
+  if (n <= 1 || passes == 0) return hipSuccess;
   const int64_t ntiles = (n + kRsTile - 1) / kRsTile;
   uint32_t* hist = static_cast<uint32_t*>(d_temp);
   void* scan_tmp = static_cast<char*>(d_temp) + (((size_t)256 * ntiles * sizeof(uint32_t) + 255) & ~(size_t)255);
-  uint64_t* ka = keys;
-  uint32_t* va = vals;
-  uint64_t* kb = keys_alt;
-  uint32_t* vb = vals_alt;
-  const int passes = (bits + 7) / 8;
+  const int4* c4 = reinterpret_cast<const int4*>(coords);
+  // ping-pong so that the last pass lands in (keys, vals)
+  uint64_t* kb[2] = {keys, keys_alt};
+  uint32_t* vb[2] = {vals, vals_alt};
+  int cur = (passes % 2 == 0) ? 0 : 1;  // buffer holding the input of the next pass
+  if (!coords) {
+    // input is in (keys, vals); an odd pass count needs one copy into the other buffer
+    if (passes % 2 == 1) {
+      hipError_t e = hipMemcpyAsync(keys_alt, keys, (size_t)n * 8, hipMemcpyDeviceToDevice, s);
+      if (e == hipSuccess) e = hipMemcpyAsync(vals_alt, vals, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return e;
+    }
+  }
   for (int p = 0; p < passes; ++p) {
     const int shift = 8 * p;
-    hipLaunchKernelGGL(k_radix_hist, dim3((unsigned)ntiles), dim3(kThreads), 0, s, ka, n, shift, hist, ntiles);
+    const bool first = (p == 0) && coords;
+    // the first pass from coordinates writes into buffer (passes odd ? 0 : 1) directly
+    const int src = cur, dst = (first ? ((passes % 2 == 1) ? 0 : 1) : cur ^ 1);
+    if (first)
+      hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, c4, L, n, shift,
+                         hist, ntiles);
+    else
+      hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], nullptr, L, n,
+                         shift, hist, ntiles);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = scan_exclusive_u32(hist, hist, 256 * ntiles, nullptr, scan_tmp, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_radix_scatter, dim3((unsigned)ntiles), dim3(kThreads), 0, s, ka, va, kb, vb, n, shift,
-                       hist, ntiles);
+    if (first)
+      hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr, c4, L,
+                         kb[dst], vb[dst], n, shift, hist, ntiles);
+    else
+      hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], vb[src],
+                         nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    uint64_t* tk = ka;
-    ka = kb;
-    kb = tk;
-    uint32_t* tv = va;
-    va = vb;
-    vb = tv;
-  }
-  if (ka != keys) {
-    hipError_t e = hipMemcpyAsync(keys, ka, (size_t)n * sizeof(uint64_t), hipMemcpyDeviceToDevice, s);
-    if (e != hipSuccess) return e;
-    e = hipMemcpyAsync(vals, va, (size_t)n * sizeof(uint32_t), hipMemcpyDeviceToDevice, s);
-    if (e != hipSuccess) return e;
+    cur = dst;
   }
   return hipSuccess;
 }
@@ -522,73 +544,39 @@ hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64
   return hipGetLastError();
 }
 
-hipError_t unique_keys(const uint64_t* keys, int64_t n, KeyLayout L, uint32_t* flags, uint32_t* pos,
-                       void* d_temp, uint64_t* qkeys, uint32_t* qrow, int32_t* out_coords, ControlBlock* cb,
-                       hipStream_t s) {
+hipError_t unique_keys(const uint64_t* keys, int64_t n, KeyLayout L, uint32_t* flags, uint32_t* pos, void* d_temp,
+                       uint64_t* qkeys, uint32_t* qrow, int32_t* out_coords, ControlBlock* cb, hipStream_t s) {
   if (n <= 0) return launch_fill_u32(&cb->n_q, 0u, 1, s);
   hipLaunchKernelGGL(k_unique_flags, dim3(grid_for(n)), dim3(kThreads), 0, s, keys, n, flags);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   e = scan_exclusive_u32(flags, pos, n, &cb->n_q, d_temp, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_unique_write, dim3(grid_for(n)), dim3(kThreads), 0, s, keys, n, L, flags, pos, qkeys,
-                     qrow, reinterpret_cast<int4*>(out_coords));
+  hipLaunchKernelGGL(k_unique_write, dim3(grid_for(n)), dim3(kThreads), 0, s, keys, n, L, flags, pos, qkeys, qrow,
+                     reinterpret_cast<int4*>(out_coords));
   return hipGetLastError();
 }
 
-hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, hipStream_t s) {
-  const int64_t waves = (int64_t)a.K3 * nb;
-  if (waves <= 0) return hipSuccess;
-  const int64_t blocks = (waves + (kThreads / kWave) - 1) / (kThreads / kWave);
-  hipLaunchKernelGGL(k_backward, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, nb, bounds);
-  return hipGetLastError();
-}
-
-hipError_t balance(const SearchArgs& a, int64_t nb, const uint32_t* bounds, uint32_t* chunks, uint32_t* item_start,
-                   void* d_temp, int32_t* items, uint64_t* status, int64_t max_items, ControlBlock* cb,
-                   hipStream_t s) {
+hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, uint32_t* chunks, ControlBlock* cb,
+                           hipStream_t s) {
   const int64_t nkb = (int64_t)a.K3 * nb;
-  if (nkb <= 0) return launch_fill_u32(&cb->n_items, 0u, 1, s);
-  hipLaunchKernelGGL(k_chunks, dim3(grid_for(nkb)), dim3(kThreads), 0, s, bounds, nkb, nb, a.Cq, chunks);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  e = scan_exclusive_u32(chunks, item_start, nkb, &cb->n_items, d_temp, s);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_emit, dim3(grid_for(nkb)), dim3(kThreads), 0, s, chunks, item_start, nkb,
-                     reinterpret_cast<int2*>(items), status, max_items, cb);
+  if (nkb <= 0) return hipSuccess;
+  const int64_t blocks = (nkb + kWavesPerBlock - 1) / kWavesPerBlock;
+  hipLaunchKernelGGL(k_backward, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, nb, bounds, chunks, cb);
   return hipGetLastError();
 }
 
-hipError_t launch_forward(const SearchArgs& a, const uint32_t* bounds, int64_t nb, const int32_t* items,
-                          uint64_t* status, int64_t max_items, int32_t* pin, int32_t* pout, uint32_t* counts,
-                          ControlBlock* cb, hipStream_t s) {
-  if (max_items <= 0 || nb <= 0) return hipSuccess;
+hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, int64_t nb, const uint32_t* istart,
+                          uint32_t* item_cnt, const uint32_t* item_off, int64_t max_items, int32_t* pin,
+                          int32_t* pout, ControlBlock* cb, hipStream_t s) {
   int log2B = 0;
   while ((1 << log2B) < a.B) ++log2B;
   const size_t lds = (size_t)a.B * (sizeof(uint64_t) + sizeof(uint32_t));
   const int rounds = a.Cq / kThreads;
-  const int2* it = reinterpret_cast<const int2*>(items);
-  switch (rounds) {
-    case 1:
-      hipLaunchKernelGGL(k_forward<1>, dim3((unsigned)max_items), dim3(kThreads), lds, s, a, bounds, nb, it,
-                         status, pin, pout, counts, cb, log2B);
-      break;
-    case 2:
-      hipLaunchKernelGGL(k_forward<2>, dim3((unsigned)max_items), dim3(kThreads), lds, s, a, bounds, nb, it,
-                         status, pin, pout, counts, cb, log2B);
-      break;
-    case 4:
-      hipLaunchKernelGGL(k_forward<4>, dim3((unsigned)max_items), dim3(kThreads), lds, s, a, bounds, nb, it,
-                         status, pin, pout, counts, cb, log2B);
-      break;
-    case 8:
-      hipLaunchKernelGGL(k_forward<8>, dim3((unsigned)max_items), dim3(kThreads), lds, s, a, bounds, nb, it,
-                         status, pin, pout, counts, cb, log2B);
-      break;
-    default:
-      return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  const unsigned grid = (unsigned)(max_items > 0 ? max_items : 1);
+  if (write)
+    return forward_t<true>(rounds, grid, lds, s, a, bounds, nb, istart, item_cnt, item_off, pin, pout, cb, log2B);
+  return forward_t<false>(rounds, grid, lds, s, a, bounds, nb, istart, item_cnt, item_off, pin, pout, cb, log2B);
 }
 
 }  // namespace spc

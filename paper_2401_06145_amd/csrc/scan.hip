@@ -1,15 +1,17 @@
-// Device-wide exclusive prefix sum of uint32 values (tile reduce -> scan of tile
-// sums -> tile scan with base).  Used for radix-sort digit offsets, for the
-// unique-coordinate compaction of Eq. 1, and for the query-block balancing step
-// of Section 5.1.2.
+// Device-wide exclusive prefix sum of uint32 values.  Up to 16384 values run in
+// one workgroup (1024 threads x 16 values); larger inputs use tile sums -> scan
+// of the sums -> tile scan with a base.  Used for the radix-sort digit offsets,
+// the unique-coordinate compaction of Eq. 1, and the work-item and match
+// offsets of the double-traversed binary search (Section 5.1.2).
 #include "common.h"
 
 namespace spc {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kRounds = 16;
-constexpr int kTile = kThreads * kRounds;  // 4096 values per workgroup
+constexpr int kThreads = 1024;
+constexpr int kItems = 16;
+constexpr int kTile = kThreads * kItems;
+constexpr int kWaves = kThreads / kWave;
 
 // Exclusive scan of one value per thread across the workgroup; *total gets the sum.
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_wave, uint32_t* total) {
@@ -23,47 +25,82 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_wave
   }
   if (lane == kWave - 1) s_wave[wave] = x;
   __syncthreads();
-  uint32_t before = 0, sum = 0;
+  if (wave == 0) {
+    uint32_t s = (lane < kWaves) ? s_wave[lane] : 0u;
+    uint32_t incl = s;
 #pragma unroll
-  for (int w = 0; w < kThreads / kWave; ++w) {
-    const uint32_t s = s_wave[w];
-    before += (w < wave) ? s : 0u;
-    sum += s;
+    for (int d = 1; d < kWaves; d <<= 1) {
+      const uint32_t y = __shfl_up(incl, d, kWave);
+      if (lane >= d) incl += y;
+    }
+    if (lane < kWaves) s_wave[kWaves + lane] = incl - s;  // exclusive wave prefix
+    if (lane == kWaves - 1) s_wave[2 * kWaves] = incl;
   }
-  __syncthreads();  // s_wave is reused by the next call
-  *total = sum;
+  __syncthreads();
+  const uint32_t before = s_wave[kWaves + wave];
+  *total = s_wave[2 * kWaves];
+  __syncthreads();  // s_wave is reused by the caller's next scan
   return before + x - v;
 }
 
-__global__ __launch_bounds__(kThreads) void k_tile_reduce(const uint32_t* in, int64_t n, uint32_t* sums) {
-  __shared__ uint32_t s_wave[kThreads / kWave];
-  const int64_t base = (int64_t)blockIdx.x * kTile;
-  uint32_t acc = 0;
-#pragma unroll 4
-  for (int r = 0; r < kRounds; ++r) {
-    const int64_t i = base + r * kThreads + threadIdx.x;
-    acc += (i < n) ? in[i] : 0u;
+// Loads kItems consecutive values of the tile for this thread (zeros past n).
+__device__ __forceinline__ void load_items(const uint32_t* in, int64_t n, int64_t first, uint32_t v[kItems]) {
+  if (first + kItems <= n && ((reinterpret_cast<uintptr_t>(in + first) & 15) == 0)) {
+    const uint4* p = reinterpret_cast<const uint4*>(in + first);
+#pragma unroll
+    for (int q = 0; q < kItems / 4; ++q) {
+      const uint4 u = p[q];
+      v[4 * q] = u.x;
+      v[4 * q + 1] = u.y;
+      v[4 * q + 2] = u.z;
+      v[4 * q + 3] = u.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) v[i] = (first + i < n) ? in[first + i] : 0u;
   }
+}
+
+__global__ __launch_bounds__(kThreads) void k_tile_reduce(const uint32_t* in, int64_t n, uint32_t* sums) {
+  __shared__ uint32_t s_wave[2 * kWaves + 1];
+  uint32_t v[kItems];
+  load_items(in, n, (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems, v);
+  uint32_t acc = 0;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) acc += v[i];
   uint32_t total;
   block_excl_scan(acc, s_wave, &total);
   if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
-// out may alias in (each element is read and written by the same thread).
+// out may alias in (each value is read, then written, by the same thread).
 __global__ __launch_bounds__(kThreads) void k_tile_scan(const uint32_t* in, uint32_t* out, int64_t n,
                                                         const uint32_t* tile_base, uint32_t* d_total) {
-  __shared__ uint32_t s_wave[kThreads / kWave];
-  const int64_t base = (int64_t)blockIdx.x * kTile;
-  uint32_t carry = tile_base ? tile_base[blockIdx.x] : 0u;
-  for (int r = 0; r < kRounds; ++r) {
-    const int64_t i = base + r * kThreads + threadIdx.x;
-    const uint32_t v = (i < n) ? in[i] : 0u;
-    uint32_t round_total;
-    const uint32_t ex = block_excl_scan(v, s_wave, &round_total);
-    if (i < n) out[i] = carry + ex;
-    carry += round_total;
+  __shared__ uint32_t s_wave[2 * kWaves + 1];
+  const int64_t first = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+  uint32_t v[kItems];
+  load_items(in, n, first, v);
+  uint32_t acc = 0;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) acc += v[i];
+  uint32_t total;
+  uint32_t run = block_excl_scan(acc, s_wave, &total) + (tile_base ? tile_base[blockIdx.x] : 0u);
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const uint32_t t = v[i];
+    v[i] = run;
+    run += t;
   }
-  if (d_total && threadIdx.x == 0 && blockIdx.x == gridDim.x - 1) *d_total = carry;
+  if (first + kItems <= n && ((reinterpret_cast<uintptr_t>(out + first) & 15) == 0)) {
+    uint4* p = reinterpret_cast<uint4*>(out + first);
+#pragma unroll
+    for (int q = 0; q < kItems / 4; ++q) p[q] = make_uint4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i)
+      if (first + i < n) out[first + i] = v[i];
+  }
+  if (d_total && blockIdx.x == gridDim.x - 1 && threadIdx.x == kThreads - 1) *d_total = run;
 }
 
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }

@@ -6,9 +6,13 @@ radix sort, the double-traversed binary search with pair compaction (Map), then
 metadata tables, gather, grouped MFMA GEMMs and scatter (GMaS).  Inputs are
 resident in HBM before timing starts.  Prints one JSON line.
 
-Per-phase times come from HIP events the library records on the launch stream
-during the timed steps; the dominant kernel's algorithmic bytes (or flops) per
-launch divided by its mean duration give the roofline figure.
+Measurement:
+  1. an untimed pass with HIP events around every phase and kernel launch gives
+     the per-phase split (Map ms, GMaS ms) and picks the dominant kernel (most
+     GPU time per step);
+  2. the timed steps record HIP events only around that kernel's launches, on the
+     stream it runs on; its algorithmic bytes (or flops) per launch over the mean
+     launch duration give the roofline figure.
 """
 from __future__ import annotations
 
@@ -23,7 +27,9 @@ sys.path.insert(0, ROOT)
 
 METRIC = "sparse-conv layer ms (Map + GMaS split); Map GB/s, GEMM TFLOP/s vs peak"
 HBM_PEAK_GBS = 8000.0
-MFMA_F16_PEAK_TFLOPS = 2500.0
+MFMA_PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}
+MAP_PHASES = ("bounds", "sort", "outcoords", "backward", "balance", "forward", "readback")
+GMAS_PHASES = ("metadata", "gather", "gemm", "scatter")
 
 
 def parse():
@@ -38,13 +44,47 @@ def parse():
     return p.parse_args()
 
 
+def kernel_models(n, n_out, pairs, L, k3, passes):
+    """Algorithmic (compulsory) bytes or flops per launch of each kernel.
+
+    Returns name -> (bound, amount).  See the measurement section of the design
+    notes for the derivation of each figure.
+    """
+    e = 4 if L.dtype == "f32" else 2
+    ep = e  # GEMM partials are stored in the layer dtype
+    k3p = (k3 + 3) // 4 * 4
+    P = max(passes, 1)
+    # scans per step: one digit-offset scan per radix pass (256 x tiles of 2048 keys),
+    # the chunk-count scan (K^3 x source blocks of 1024) and the match-count scan
+    nb = -(-n // 1024)
+    max_items = k3 * (nb + -(-n_out // 1024)) + 1
+    scan_lens = [256 * -(-n // 2048)] * P + [k3 * nb, max_items]
+    m = {
+        "k_scan": ("hbm", 8.0 * sum(scan_lens) / len(scan_lens)),
+        # radix passes: the first reads int32 coordinates (16 B/row), later ones key + row (12 B)
+        "k_radix_scatter": ("hbm", (16 * n + 12 * n + (P - 1) * 24 * n) / P),
+        "k_radix_hist": ("hbm", (16 * n + (P - 1) * 8 * n) / P),
+        "k_minmax": ("hbm", 16 * n),
+        # forward search: query keys and source keys once, one result word per query
+        "k_forward_count": ("hbm", 8 * n_out + 8 * n + 4 * k3 * n_out),
+        "k_forward_write": ("hbm", 4 * k3 * n_out + 4 * n_out + 4 * n + 8 * pairs),
+        "k_backward": ("hbm", 8 * n_out),
+        "k_fill": ("hbm", 4 * (n + n_out) * k3p / 2),
+        "k_mt_pairs": ("hbm", 16 * pairs),
+        "k_gather": ("hbm", (n + pairs) * L.c_in * e + 4 * n * k3p),
+        "k_scatter": ("hbm", pairs * L.c_out * ep + n_out * L.c_out * e + 4 * n_out * k3p),
+        "k_gemm_bytes": ("hbm", pairs * (L.c_in * e + L.c_out * ep) + k3 * L.c_in * L.c_out * e),
+        "k_gemm_flops": ("mfma", 2.0 * pairs * L.c_in * L.c_out),
+    }
+    return m
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
-    import numpy as np
     import torch
 
     from paper_2401_06145_amd import binding as B
@@ -68,8 +108,8 @@ def main():
     counts = B.spconv_map_counts(h)
     pairs = int(sum(counts))
     n_out = int(B.lib().spconv_map_n_out(h))
-    fwd_ws = torch.empty(B.spconv_forward_workspace_bytes(h, L.c_in, L.c_out, B.DTYPES[tdt], opt), dtype=torch.uint8,
-                         device=dev)
+    fwd_ws = torch.empty(B.spconv_forward_workspace_bytes(h, L.c_in, L.c_out, B.DTYPES[tdt], opt),
+                         dtype=torch.uint8, device=dev)
     plan = B.spconv_forward_plan(h, L.c_in, L.c_out, B.DTYPES[tdt], opt)
     B.spconv_free_map(h)
     y = torch.empty((n_out, L.c_out), dtype=tdt, device=dev)
@@ -82,8 +122,33 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    B.spconv_profile_read(reset=True)
-    B.spconv_profile_enable(True)
+
+    # 1. breakdown (untimed): one pass with events around the phases, then one pass
+    #    per kernel with events around that kernel's launches only
+    R = 10
+    ids = B.profile_ids()
+
+    def timed_pass(mask):
+        B.spconv_profile_read(reset=True)
+        B.spconv_profile_enable(mask)
+        for _ in range(R):
+            step()
+        torch.cuda.synchronize()
+        B.spconv_profile_enable(False)
+        return B.spconv_profile_read(reset=True)
+
+    prof = timed_pass(B.PHASES_ALL)
+    ph_ms = {k: v[0] / R for k, v in prof.items() if not k.startswith("k_")}
+    kern = {}
+    for name, kid in ids.items():
+        if name.startswith("k_"):
+            ms, cnt = timed_pass(1 << kid)[name]
+            if cnt > 0:
+                kern[name] = (ms / R, cnt / R)
+    dominant = max(kern, key=lambda k: kern[k][0])
+
+    # 2. timed steps; events only around the dominant kernel's launches
+    B.spconv_profile_enable(1 << ids[dominant])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -91,42 +156,40 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     B.spconv_profile_enable(False)
-    phases = B.spconv_profile_read(reset=True)
+    live = B.spconv_profile_read(reset=True)[dominant]
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    ph_ms = {k: v[0] / args.steps for k, v in phases.items()}
-    map_phases = ("bounds", "sort", "outcoords", "backward", "balance", "forward", "readback")
-    gmas_phases = ("metadata", "gather", "gemm", "scatter")
-    map_ms = sum(ph_ms[p] for p in map_phases)
-    gmas_ms = sum(ph_ms[p] for p in gmas_phases)
+    mean_launch_ms = live[0] / live[1]
+    launches_per_step = live[1] / args.steps
 
-    e = 4 if L.dtype == "f32" else 2
-    ep = 4  # float32 partial buffer
     k3 = L.K ** 3
-    k3p = (k3 + 3) // 4 * 4
-    # compulsory bytes (sort 28 B/voxel, search 8|Q| + 12|P| + 8M + counts)
-    map_bytes = 28 * n + 8 * n_out + 12 * n + 8 * pairs + 4 * (k3 + 1)
-    gather_bytes = (n + pairs) * L.c_in * e + 4 * n * k3p
-    scatter_bytes = (pairs * ep + n_out * e) * L.c_out + 4 * n_out * k3p
-    gemm_flops = 2.0 * pairs * L.c_in * L.c_out
-    gemm_bytes = pairs * (L.c_in * e + L.c_out * ep) + k3 * L.c_in * L.c_out * e
-    cand = {
-        "gather": ("hbm", gather_bytes, ph_ms["gather"]),
-        "scatter": ("hbm", scatter_bytes, ph_ms["scatter"]),
-        "forward_search": ("hbm", 8 * n_out + 12 * n + 8 * pairs, ph_ms["forward"]),
-        "gemm": ("mfma", gemm_flops, ph_ms["gemm"]),
-    }
-    dom = max(cand, key=lambda k: cand[k][2])
-    bound, work, t_ms = cand[dom]
-    if bound == "hbm":
-        achieved = work / (t_ms * 1e-3) / 1e9
-        roof = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": work,
-                "mean_launch_ms": t_ms}
+    passes = int(round(kern.get("k_radix_scatter", (0, 0))[1]))
+    models = kernel_models(n, n_out, pairs, L, k3, passes)
+    if dominant == "k_gemm":
+        # with materialised buffers the GEMM's intensity is below the MFMA ridge: price it on HBM
+        flops = models["k_gemm_flops"][1]
+        byts = models["k_gemm_bytes"][1]
+        ridge = MFMA_PEAK_TFLOPS[L.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+        bound, work = ("hbm", byts) if flops / byts < ridge else ("mfma", flops)
     else:
-        achieved = work / (t_ms * 1e-3) / 1e12
-        roof = {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": MFMA_F16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / MFMA_F16_PEAK_TFLOPS, "traffic": None,
-                "algorithmic_flops": work, "mean_launch_ms": t_ms}
+        bound, work = models[dominant]
+    if bound == "hbm":
+        achieved = work / (mean_launch_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None, "kernel": dominant,
+                "algorithmic_bytes_per_launch": int(work)}
+    else:
+        peak = MFMA_PEAK_TFLOPS[L.dtype]
+        achieved = work / (mean_launch_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 5), "traffic": None, "kernel": dominant,
+                "algorithmic_flops_per_launch": work}
+    roof.update({"mean_launch_ms": round(mean_launch_ms, 6), "launches_per_step": launches_per_step})
+
+    map_ms = sum(ph_ms.get(p, 0.0) for p in MAP_PHASES)
+    gmas_ms = sum(ph_ms.get(p, 0.0) for p in GMAS_PHASES)
+    map_bytes = 28 * n + 8 * n_out + 12 * n + 8 * pairs + 4 * (k3 + 1)
+    gemm_ms = kern.get("k_gemm", (float("nan"), 1))[0]
+    gemm_tflops = models["k_gemm_flops"][1] / (gemm_ms * 1e-3) / 1e12
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -150,17 +213,16 @@ def main():
         "map_ms": round(map_ms, 5),
         "gmas_ms": round(gmas_ms, 5),
         "phases_ms": {k: round(v, 5) for k, v in ph_ms.items()},
+        "kernels_ms_per_step": {k: round(v[0], 5) for k, v in sorted(kern.items(), key=lambda t: -t[1][0])},
         "map_gbps_compulsory": round(map_bytes / (map_ms * 1e-3) / 1e9, 2),
-        "gemm_tflops": round(gemm_flops / (ph_ms["gemm"] * 1e-3) / 1e12, 3),
-        "gemm_frac_mfma_f16": round(gemm_flops / (ph_ms["gemm"] * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
-        "gemm_operand_bytes": gemm_bytes,
+        "gemm_tflops": round(gemm_tflops, 3),
+        "gemm_frac_mfma": round(gemm_tflops / MFMA_PEAK_TFLOPS[L.dtype], 5),
         "padding_overhead": (plan.rows_padded - plan.rows_real) / max(plan.rows_real, 1),
         "gemm_launches": plan.n_gemm_launches,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))
-    _ = np
 
 
 def cpu_baseline(coords, x, w, L):

@@ -68,12 +68,13 @@ typedef enum {
  * limit); the GMaS fields are the Gather / Scatter tile sizes of Algorithm 1
  * (channels per thread) and the GEMM grouping of Section 5.2.2. */
 typedef struct {
-  int B;             /* source block size, power of two in [64, 4096]; default 256 */
-  int Cq;            /* query block limit (the paper's C), multiple of 256; default 512 */
+  int B;             /* source block size, power of two in [64, 4096]; default 1024 */
+  int Cq;            /* query block limit (the paper's C): 256, 512, 1024 or 2048; default 1024 */
   int t_gather;      /* gather tile T in channels; must divide c_in; default: tuned rule */
   int t_scatter;     /* scatter tile T in channels; must divide c_out; default: tuned rule */
   int grouping;      /* spconv_grouping + 1 (0 = default SPCONV_GROUP_RAGGED) */
-  int partial_dtype; /* output-buffer (GEMM partial) precision: 0 = float32, 1 = layer dtype */
+  int partial_dtype; /* GEMM partial (output buffer) precision: 1 = float32, 2 = layer dtype;
+                        0 = default (layer dtype; sums are float32 either way) */
   int launch_cost_rows; /* grouping policy: one launch costs this many padded rows; default 32768 */
   int reserved[9];
 } spconv_options;
@@ -162,13 +163,16 @@ int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype,
                         const spconv_options* opt, spconv_plan_info* info);
 
 /* ------------------------------------------------------------ measurement --
- * Phase timing: while enabled, the library records HIP events on the caller's
- * stream around each phase of spconv_build_map / spconv_forward (bounds, sort,
- * outcoords, backward, balance, forward, readback, metadata, gather, gemm,
- * scatter).  spconv_profile_read() waits for the recorded events and writes the
- * summed milliseconds and the number of timed intervals per phase into arrays of
- * at least spconv_profile_phase_count() entries; reset != 0 clears the record. */
-int spconv_profile_enable(int on);
+ * Event timing: for every id whose bit is set in `mask`, the library records HIP
+ * events on the caller's stream around that phase of spconv_build_map /
+ * spconv_forward (ids 0..10: bounds, sort, outcoords, backward, balance, forward,
+ * readback, metadata, gather, gemm, scatter) or around each launch of that kernel
+ * (ids 16..31; spconv_profile_phase_name() gives the names, "" for unused ids).
+ * mask = 0 turns timing off.  spconv_profile_read() waits for the recorded events
+ * and writes the summed milliseconds and the number of timed intervals per id
+ * into host arrays of at least spconv_profile_phase_count() entries; reset != 0
+ * clears the record. */
+int spconv_profile_enable(uint64_t mask);
 int spconv_profile_phase_count(void);
 const char* spconv_profile_phase_name(int i);
 int spconv_profile_read(double* h_ms, int64_t* h_intervals, int n, int reset);

@@ -101,7 +101,7 @@ def lib() -> ctypes.CDLL:
     L.spconv_forward.restype = c_int
     L.spconv_forward_plan.argtypes = [vp, c_int, c_int, c_int, optp, ctypes.POINTER(PlanInfo)]
     L.spconv_forward_plan.restype = c_int
-    L.spconv_profile_enable.argtypes = [c_int]
+    L.spconv_profile_enable.argtypes = [ctypes.c_uint64]
     L.spconv_profile_enable.restype = c_int
     L.spconv_profile_phase_count.argtypes = []
     L.spconv_profile_phase_count.restype = c_int
@@ -194,16 +194,41 @@ def spconv_forward_plan(m, c_in: int, c_out: int, dtype: int, opt: Options | Non
     return info
 
 
-def spconv_profile_enable(on: bool) -> None:
-    lib().spconv_profile_enable(1 if on else 0)
+def profile_ids() -> dict:
+    """name -> id of every timed phase (ids < 16) and kernel (names start with 'k_')."""
+    n = lib().spconv_profile_phase_count()
+    out = {}
+    for i in range(n):
+        name = lib().spconv_profile_phase_name(i).decode()
+        if name:
+            out[name] = i
+    return out
+
+
+PHASES_ALL = (1 << 16) - 1
+
+
+def spconv_profile_enable(mask) -> None:
+    """mask: an int bit mask of ids, True (all phases and kernels) or False (off)."""
+    if mask is True:
+        mask = (1 << 64) - 1
+    elif mask is False or mask is None:
+        mask = 0
+    lib().spconv_profile_enable(ctypes.c_uint64(int(mask)))
 
 
 def spconv_profile_read(reset: bool = True) -> dict:
+    """name -> (summed ms, number of timed intervals) for every id that has a name."""
     n = lib().spconv_profile_phase_count()
     ms = (ctypes.c_double * n)()
     cnt = (ctypes.c_int64 * n)()
     _check(lib().spconv_profile_read(ms, cnt, n, 1 if reset else 0), "spconv_profile_read")
-    return {lib().spconv_profile_phase_name(i).decode(): (ms[i], cnt[i]) for i in range(n)}
+    out = {}
+    for i in range(n):
+        name = lib().spconv_profile_phase_name(i).decode()
+        if name:
+            out[name] = (ms[i], cnt[i])
+    return out
 
 
 # ----------------------------------------------------------------------------

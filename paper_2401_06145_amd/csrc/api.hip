@@ -68,18 +68,21 @@ struct Bump {
 // ---------------------------------------------------------------------------
 // Phase timing (measurement API): HIP events around each phase on the stream.
 // ---------------------------------------------------------------------------
-enum Phase {
-  PH_BOUNDS = 0, PH_SORT, PH_OUTCOORDS, PH_BACKWARD, PH_BALANCE, PH_FORWARD, PH_READBACK,
-  PH_METADATA, PH_GATHER, PH_GEMM, PH_SCATTER, PH_COUNT
-};
-const char* kPhaseNames[PH_COUNT] = {"bounds", "sort", "outcoords", "backward", "balance", "forward",
-                                     "readback", "metadata", "gather", "gemm", "scatter"};
+const char* prof_name(int id) {
+  static const char* kNames[PROF_IDS] = {
+      "bounds", "sort", "outcoords", "backward", "balance", "forward", "readback", "metadata", "gather", "gemm",
+      "scatter", "", "", "", "", "",
+      "k_minmax", "k_radix_hist", "k_radix_scatter", "k_scan", "k_copy", "k_down_keys", "k_unique", "k_backward",
+      "k_forward_count", "k_forward_write", "k_fill", "k_mt_pairs", "k_gather", "k_gemm", "k_scatter", "k_pack",
+      "", "", "", "", "", "", "", ""};
+  return (id >= 0 && id < PROF_IDS) ? kNames[id] : "";
+}
 struct PhaseRec {
   int phase;
   hipEvent_t a, b;
 };
 std::mutex g_prof_mu;
-bool g_prof = false;
+uint64_t g_prof_mask = 0;
 std::vector<PhaseRec> g_recs;
 std::vector<hipEvent_t> g_pool;
 
@@ -88,31 +91,45 @@ hipEvent_t ev_get() {
   if (!g_pool.empty()) {
     e = g_pool.back();
     g_pool.pop_back();
-  } else if (hipEventCreate(&e) != hipSuccess) {
+  } else if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) {
+    // timing events only: no system-scope release needed around the timed kernels
     e = nullptr;
   }
   return e;
 }
 
-struct PhaseScope {
-  int phase;
+struct OpenRec {
+  int id;
   hipStream_t s;
-  hipEvent_t a = nullptr;
-  PhaseScope(int p, hipStream_t st) : phase(p), s(st) {
-    if (!g_prof) return;
-    std::lock_guard<std::mutex> lk(g_prof_mu);
-    a = ev_get();
-    if (a) (void)hipEventRecord(a, s);
-  }
-  ~PhaseScope() {
-    if (!a) return;
-    std::lock_guard<std::mutex> lk(g_prof_mu);
-    hipEvent_t b = ev_get();
-    if (!b) return;
-    (void)hipEventRecord(b, s);
-    g_recs.push_back({phase, a, b});
-  }
+  hipEvent_t a;
 };
+
+}  // namespace
+
+namespace spc {
+ProfScope::ProfScope(int id, hipStream_t s) {
+  if (!((g_prof_mask >> id) & 1ull)) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t a = ev_get();
+  if (!a) return;
+  (void)hipEventRecord(a, s);
+  rec = new (std::nothrow) OpenRec{id, s, a};
+}
+ProfScope::~ProfScope() {
+  if (!rec) return;
+  OpenRec* r = static_cast<OpenRec*>(rec);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t b = ev_get();
+  if (b) {
+    (void)hipEventRecord(b, r->s);
+    g_recs.push_back({r->id, r->a, b});
+  }
+  delete r;
+}
+}  // namespace spc
+
+namespace {
+using PhaseScope = spc::ProfScope;
 
 // Pinned host staging for the two read-backs of a map build (one per thread).
 struct Staging {
@@ -155,6 +172,7 @@ struct MapBufs {
   uint32_t* bounds;
   uint32_t* chunks;
   uint32_t* istart;
+  int32_t* res;
   uint32_t* item_cnt;
   uint32_t* item_off;
   int32_t* mm_partial;
@@ -164,8 +182,8 @@ struct MapBufs {
 };
 
 struct Tunables {
-  int B = 256;
-  int Cq = 512;
+  int B = 1024;
+  int Cq = 1024;
 };
 
 int read_tunables(const spconv_options* opt, Tunables* t) {
@@ -210,6 +228,7 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   b->bounds = m.take<uint32_t>(nkb);
   b->chunks = m.take<uint32_t>(nkb);
   b->istart = m.take<uint32_t>(nkb);
+  b->res = m.take<int32_t>((int64_t)K3 * nq_max);
   b->item_cnt = m.take<uint32_t>(b->max_items);
   b->item_off = m.take<uint32_t>(b->max_items);
   b->mm_partial = static_cast<int32_t*>(m.take_bytes(minmax_temp_bytes()));
@@ -317,7 +336,11 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
   if (c_in < 1 || c_out < 1 || c_in > 1024 || c_out > 1024) return fail(SPCONV_EUNSUPPORTED, "channels must be in [1, 1024]");
   if ((c_in * p->elem) % 16 != 0) return fail(SPCONV_EUNSUPPORTED, "c_in rows must be whole 16-byte vectors");
   if (c_out % 16 != 0) return fail(SPCONV_EUNSUPPORTED, "c_out must be a multiple of 16");
-  p->part_dtype = (opt && opt->partial_dtype) ? dtype : SPCONV_F32;
+  // GEMM partials: 1 = float32, 2 = the layer dtype; default float32 for f32 layers and
+  // the layer dtype otherwise (the scatter still sums them in float32)
+  const int pd = opt ? opt->partial_dtype : 0;
+  if (pd < 0 || pd > 2) return fail(SPCONV_EINVAL, "partial_dtype must be 0, 1 or 2");
+  p->part_dtype = (pd == 1) ? SPCONV_F32 : (pd == 2 ? dtype : dtype);
   p->pelem = elem_bytes(p->part_dtype);
   // tiles: default one 16-byte vector per thread for gather and for the partial reads of scatter
   p->t_gather = (opt && opt->t_gather) ? opt->t_gather : 16 / p->elem;
@@ -500,6 +523,8 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   a.Cq = tu.Cq;
   a.swap_roles = (mode == SPCONV_UP) ? 1 : 0;
   a.check_q = (mode == SPCONV_UP) ? 1 : 0;
+  a.res = b.res;
+  a.res_stride = nq_max;
   {
     PhaseScope ph(PH_BACKWARD, s);
     hipError_t e = launch_backward(a, b.nb, b.bounds, b.chunks, b.cb, s);
@@ -672,19 +697,19 @@ int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* 
 }
 
 // --------------------------------------------------------------- measurement
-int spconv_profile_enable(int on) {
+int spconv_profile_enable(uint64_t mask) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  g_prof = on != 0;
+  g_prof_mask = mask;
   return SPCONV_OK;
 }
 
-int spconv_profile_phase_count(void) { return PH_COUNT; }
-const char* spconv_profile_phase_name(int i) { return (i >= 0 && i < PH_COUNT) ? kPhaseNames[i] : ""; }
+int spconv_profile_phase_count(void) { return PROF_IDS; }
+const char* spconv_profile_phase_name(int i) { return prof_name(i); }
 
 int spconv_profile_read(double* ms, int64_t* launches, int n, int reset) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  if (!ms || !launches || n < PH_COUNT) return fail(SPCONV_EINVAL, "need PH_COUNT entries");
-  for (int i = 0; i < PH_COUNT; ++i) {
+  if (!ms || !launches || n < PROF_IDS) return fail(SPCONV_EINVAL, "need spconv_profile_phase_count() entries");
+  for (int i = 0; i < PROF_IDS; ++i) {
     ms[i] = 0.0;
     launches[i] = 0;
   }

@@ -67,6 +67,26 @@ struct ControlBlock {
 };
 
 // ---------------------------------------------------------------------------
+// Measurement: HIP events around phases and around individual kernel launches,
+// recorded only for the ids enabled in the profiling mask (api.hip).
+// ---------------------------------------------------------------------------
+enum ProfId : int {
+  // phases (host-visible steps, including the read-back synchronisations)
+  PH_BOUNDS = 0, PH_SORT, PH_OUTCOORDS, PH_BACKWARD, PH_BALANCE, PH_FORWARD, PH_READBACK,
+  PH_METADATA, PH_GATHER, PH_GEMM, PH_SCATTER,
+  // kernels
+  KN_MINMAX = 16, KN_RADIX_HIST, KN_RADIX_SCATTER, KN_SCAN, KN_COPY, KN_DOWN_KEYS, KN_UNIQUE,
+  KN_BACKWARD, KN_FORWARD_COUNT, KN_FORWARD_WRITE, KN_FILL, KN_MT_PAIRS, KN_GATHER, KN_GEMM, KN_SCATTER,
+  KN_PACK,
+  PROF_IDS = 40
+};
+struct ProfScope {
+  void* rec = nullptr;
+  ProfScope(int id, hipStream_t s);
+  ~ProfScope();
+};
+
+// ---------------------------------------------------------------------------
 // Launchers (host functions, defined next to their kernels).
 // ---------------------------------------------------------------------------
 
@@ -110,6 +130,8 @@ struct SearchArgs {
   int Cq;                 // query block limit
   int swap_roles;         // UP: pairs are (query row, source row)
   int check_q;            // also check the query keys for repeats
+  int32_t* res;           // [K3][res_stride] per-query match (sorted source position or -1)
+  int64_t res_stride;
 };
 // Section 5.1.2, backward search fused with the per-(k, b) chunk counts of the
 // balancing step (and the duplicate-key check).

@@ -161,6 +161,7 @@ hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const
       break;
     }
   if (nt == 0) return hipErrorInvalidValue;
+  ProfScope ps(KN_GEMM, s);
   const size_t lds = (size_t)16 * nt * ldk * sizeof(T);
   const dim3 grid((unsigned)total_tiles, (unsigned)(nt_all / nt));
   const T* a = static_cast<const T*>(A);

@@ -138,6 +138,7 @@ unsigned blocks_for(int64_t threads) { return (unsigned)((threads + kThreads - 1
 template <typename TP, typename TO>
 hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* omt, int stride, int K3, void* y,
                      int tile, hipStream_t s) {
+  ProfScope ps(KN_SCATTER, s);
   const int64_t threads = n_out * (c_out / tile);
   const dim3 g(blocks_for(threads)), b(kThreads);
   const TP* p = static_cast<const TP*>(buf);
@@ -172,6 +173,7 @@ hipError_t launch_mt_fill(int32_t* imt, int64_t n_in, int32_t* omt, int64_t n_ou
 hipError_t launch_mt_pairs(const int32_t* pin, const int32_t* pout, int64_t m_total, const OffsetTable& t,
                            int32_t* imt, int32_t* omt, int stride, hipStream_t s) {
   if (m_total <= 0) return hipSuccess;
+  ProfScope ps(KN_MT_PAIRS, s);
   hipLaunchKernelGGL(k_mt_pairs, dim3(blocks_for(m_total)), dim3(kThreads), 0, s, pin, pout, m_total, t, imt, omt,
                      stride);
   return hipGetLastError();
@@ -183,6 +185,7 @@ hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const 
   const int row_vec = c_in * elem / 16;
   const int v = tile * elem / 16;
   if (v <= 0 || row_vec % v != 0) return hipErrorInvalidValue;
+  ProfScope ps(KN_GATHER, s);
   const int64_t threads = n_in * (row_vec / v);
   const dim3 g(blocks_for(threads)), b(kThreads);
   const uint4* xp = static_cast<const uint4*>(x);

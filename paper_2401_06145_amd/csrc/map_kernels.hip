@@ -73,12 +73,35 @@ __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int6
   }
 }
 
-__global__ void k_minmax_final(const int32_t* partial, int nblocks, ControlBlock* cb) {
+__global__ __launch_bounds__(kThreads) void k_minmax_final(const int32_t* partial, int nblocks, ControlBlock* cb) {
+  // one partial per thread (nblocks <= kMinmaxBlocks == kThreads), then wave and block reduce
+  int32_t r[8];
+#pragma unroll
+  for (int f = 0; f < 8; ++f) r[f] = (f < 4) ? INT_MAX : INT_MIN;
+  if ((int)threadIdx.x < nblocks) {
+#pragma unroll
+    for (int f = 0; f < 8; ++f) r[f] = partial[threadIdx.x * 8 + f];
+  }
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) {
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int32_t o = __shfl_xor(r[f], off, kWave);
+      r[f] = (f < 4) ? min(r[f], o) : max(r[f], o);
+    }
+  }
+  __shared__ int32_t s[kWavesPerBlock][8];
+  const int wave = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+#pragma unroll
+    for (int f = 0; f < 8; ++f) s[wave][f] = r[f];
+  }
+  __syncthreads();
   const int f = threadIdx.x;
   if (f < 8) {
-    int32_t r = (f < 4) ? INT_MAX : INT_MIN;
-    for (int i = 0; i < nblocks; ++i) r = (f < 4) ? min(r, partial[i * 8 + f]) : max(r, partial[i * 8 + f]);
-    cb->minmax[f] = r;
+    int32_t v = s[0][f];
+    for (int w = 1; w < kWavesPerBlock; ++w) v = (f < 4) ? min(v, s[w][f]) : max(v, s[w][f]);
+    cb->minmax[f] = v;
   }
   if (f == 0) {
     cb->err = 0;
@@ -350,7 +373,6 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
   __shared__ int64_t s_kb;
   __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
   uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
-  uint32_t* lidx = reinterpret_cast<uint32_t*>(smem + sizeof(uint64_t) * a.B);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
@@ -372,11 +394,12 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
   const ItemRange it = locate_item(a, w, nb, bounds, istart, &s_kb);
   const int64_t s0 = it.b * (int64_t)a.B;
   const int nB = (int)min((int64_t)a.B, a.n_src - s0);
-  for (int e = tid; e < nB; e += kThreads) {
-    lkey[e] = a.skeys[s0 + e];
-    lidx[e] = a.sidx[s0 + e];
+  if (!WRITE) {
+    for (int e = tid; e < nB; e += kThreads) lkey[e] = a.skeys[s0 + e];
+    __syncthreads();
   }
-  __syncthreads();
+  // dense per-query result of this offset: sorted source position, or -1
+  int32_t* res = a.res + (int64_t)it.k * a.res_stride;
 
   const uint64_t dk = (uint64_t)a.dk[it.k];
   int32_t r_in[ROUNDS], r_out[ROUNDS];
@@ -388,12 +411,16 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
     r_in[r] = 0;
     r_out[r] = 0;
     if (qp < it.q1) {
-      const uint64_t key = a.qkeys[qp] + dk;
-      const int pos = lds_lower(lkey, nB, log2B, key);
-      if (pos < nB && lkey[pos] == key) {
-        hit = true;
-        if (WRITE) {
-          const int32_t src = (int32_t)lidx[pos];
+      if (!WRITE) {
+        const uint64_t key = a.qkeys[qp] + dk;
+        const int pos = lds_lower(lkey, nB, log2B, key);
+        hit = pos < nB && lkey[pos] == key;
+        res[qp] = hit ? (int32_t)(s0 + pos) : -1;
+      } else {
+        const int32_t sp = res[qp];
+        if (sp >= 0) {
+          hit = true;
+          const int32_t src = (int32_t)a.sidx[sp];
           const int32_t qry = (int32_t)a.qrow[qp];
           r_in[r] = a.swap_roles ? qry : src;
           r_out[r] = a.swap_roles ? src : qry;
@@ -433,6 +460,7 @@ template <bool WRITE>
 hipError_t forward_t(int rounds, unsigned grid, size_t lds, hipStream_t s, const SearchArgs& a,
                      const uint32_t* bounds, int64_t nb, const uint32_t* istart, uint32_t* item_cnt,
                      const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb, int log2B) {
+  ProfScope ps(WRITE ? KN_FORWARD_WRITE : KN_FORWARD_COUNT, s);
   switch (rounds) {
 #define SPC_F(R)                                                                                                    \
   case R:                                                                                                           \
@@ -457,6 +485,7 @@ hipError_t forward_t(int rounds, unsigned grid, size_t lds, hipStream_t s, const
 // ----------------------------------------------------------------------------
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  ProfScope ps(KN_FILL, s);
   hipLaunchKernelGGL(k_fill_u32, dim3(grid_for(n, kThreads, 4096)), dim3(kThreads), 0, s, p, v, n);
   return hipGetLastError();
 }
@@ -465,17 +494,19 @@ size_t minmax_temp_bytes() { return (size_t)kMinmaxBlocks * 8 * sizeof(int32_t);
 
 hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t nb, int32_t* partial,
                          ControlBlock* cb, hipStream_t s) {
+  ProfScope ps(KN_MINMAX, s);
   const unsigned g = grid_for(na + nb, kThreads * 8, kMinmaxBlocks);
   hipLaunchKernelGGL(k_minmax_partial, dim3(g), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(a), na,
                      reinterpret_cast<const int4*>(b), nb, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_minmax_final, dim3(1), dim3(64), 0, s, partial, (int)g, cb);
+  hipLaunchKernelGGL(k_minmax_final, dim3(1), dim3(kThreads), 0, s, partial, (int)g, cb);
   return hipGetLastError();
 }
 
 hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  ProfScope ps(KN_PACK, s);
   hipLaunchKernelGGL(k_pack, dim3(grid_for(n)), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(coords), n, L,
                      keys, vals);
   return hipGetLastError();
@@ -504,6 +535,7 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
   if (!coords) {
     // input is in (keys, vals); an odd pass count needs one copy into the other buffer
     if (passes % 2 == 1) {
+      ProfScope ps(KN_COPY, s);
       hipError_t e = hipMemcpyAsync(keys_alt, keys, (size_t)n * 8, hipMemcpyDeviceToDevice, s);
       if (e == hipSuccess) e = hipMemcpyAsync(vals_alt, vals, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
       if (e != hipSuccess) return e;
@@ -514,23 +546,30 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
     const bool first = (p == 0) && coords;
     // the first pass from coordinates writes into buffer (passes odd ? 0 : 1) directly
     const int src = cur, dst = (first ? ((passes % 2 == 1) ? 0 : 1) : cur ^ 1);
-    if (first)
-      hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, c4, L, n, shift,
-                         hist, ntiles);
-    else
-      hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], nullptr, L, n,
-                         shift, hist, ntiles);
-    hipError_t e = hipGetLastError();
+    hipError_t e;
+    {
+      ProfScope ps(KN_RADIX_HIST, s);
+      if (first)
+        hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, c4, L, n, shift,
+                           hist, ntiles);
+      else
+        hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], nullptr, L, n,
+                           shift, hist, ntiles);
+      e = hipGetLastError();
+    }
     if (e != hipSuccess) return e;
     e = scan_exclusive_u32(hist, hist, 256 * ntiles, nullptr, scan_tmp, s);
     if (e != hipSuccess) return e;
-    if (first)
-      hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr, c4, L,
-                         kb[dst], vb[dst], n, shift, hist, ntiles);
-    else
-      hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], vb[src],
-                         nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles);
-    e = hipGetLastError();
+    {
+      ProfScope ps(KN_RADIX_SCATTER, s);
+      if (first)
+        hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr, c4,
+                           L, kb[dst], vb[dst], n, shift, hist, ntiles);
+      else
+        hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], vb[src],
+                           nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles);
+      e = hipGetLastError();
+    }
     if (e != hipSuccess) return e;
     cur = dst;
   }
@@ -540,6 +579,7 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
 hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell, uint64_t* dkeys,
                             uint32_t* vals, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  ProfScope ps(KN_DOWN_KEYS, s);
   hipLaunchKernelGGL(k_down_keys, dim3(grid_for(n)), dim3(kThreads), 0, s, skeys, n, L, cell, dkeys, vals);
   return hipGetLastError();
 }
@@ -547,6 +587,7 @@ hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64
 hipError_t unique_keys(const uint64_t* keys, int64_t n, KeyLayout L, uint32_t* flags, uint32_t* pos, void* d_temp,
                        uint64_t* qkeys, uint32_t* qrow, int32_t* out_coords, ControlBlock* cb, hipStream_t s) {
   if (n <= 0) return launch_fill_u32(&cb->n_q, 0u, 1, s);
+  ProfScope ps(KN_UNIQUE, s);
   hipLaunchKernelGGL(k_unique_flags, dim3(grid_for(n)), dim3(kThreads), 0, s, keys, n, flags);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -562,6 +603,7 @@ hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, ui
   const int64_t nkb = (int64_t)a.K3 * nb;
   if (nkb <= 0) return hipSuccess;
   const int64_t blocks = (nkb + kWavesPerBlock - 1) / kWavesPerBlock;
+  ProfScope ps(KN_BACKWARD, s);
   hipLaunchKernelGGL(k_backward, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, nb, bounds, chunks, cb);
   return hipGetLastError();
 }
@@ -571,7 +613,7 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
                           int32_t* pout, ControlBlock* cb, hipStream_t s) {
   int log2B = 0;
   while ((1 << log2B) < a.B) ++log2B;
-  const size_t lds = (size_t)a.B * (sizeof(uint64_t) + sizeof(uint32_t));
+  const size_t lds = write ? 0 : (size_t)a.B * sizeof(uint64_t);
   const int rounds = a.Cq / kThreads;
   const unsigned grid = (unsigned)(max_items > 0 ? max_items : 1);
   if (write)

@@ -113,12 +113,9 @@ size_t scan_temp_bytes(int64_t n) {
   return align256((size_t)nt * sizeof(uint32_t)) + scan_temp_bytes(nt);
 }
 
-hipError_t scan_exclusive_u32(const uint32_t* d_in, uint32_t* d_out, int64_t n, uint32_t* d_total,
-                              void* d_temp, hipStream_t s) {
-  if (n <= 0) {
-    if (d_total) return launch_fill_u32(d_total, 0u, 1, s);
-    return hipSuccess;
-  }
+namespace {
+hipError_t scan_impl(const uint32_t* d_in, uint32_t* d_out, int64_t n, uint32_t* d_total, void* d_temp,
+                     hipStream_t s) {
   if (n <= kTile) {
     hipLaunchKernelGGL(k_tile_scan, dim3(1), dim3(kThreads), 0, s, d_in, d_out, n, nullptr, d_total);
     return hipGetLastError();
@@ -129,10 +126,21 @@ hipError_t scan_exclusive_u32(const uint32_t* d_in, uint32_t* d_out, int64_t n, 
   hipLaunchKernelGGL(k_tile_reduce, dim3((unsigned)nt), dim3(kThreads), 0, s, d_in, n, sums);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = scan_exclusive_u32(sums, sums, nt, nullptr, rest, s);
+  e = scan_impl(sums, sums, nt, nullptr, rest, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tile_scan, dim3((unsigned)nt), dim3(kThreads), 0, s, d_in, d_out, n, sums, d_total);
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t scan_exclusive_u32(const uint32_t* d_in, uint32_t* d_out, int64_t n, uint32_t* d_total,
+                              void* d_temp, hipStream_t s) {
+  if (n <= 0) {
+    if (d_total) return launch_fill_u32(d_total, 0u, 1, s);
+    return hipSuccess;
+  }
+  ProfScope ps(KN_SCAN, s);
+  return scan_impl(d_in, d_out, n, d_total, d_temp, s);
 }
 
 }  // namespace spc

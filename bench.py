@@ -41,7 +41,23 @@ def parse():
     p.add_argument("--channels", type=int, default=None, help="channel width for recipe 3")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--grouping", type=int, default=None)
+    p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                   help="only run a plain device copy of this many MiB (HBM counter calibration)")
     return p.parse_args()
+
+
+def copy_calibration(mib: int) -> None:
+    """A plain device-to-device copy of known size: reads and writes `mib` MiB once."""
+    import torch
+
+    n = mib * 1024 * 1024 // 4
+    src = torch.arange(n, dtype=torch.int32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_mib": mib, "bytes_read": n * 4, "bytes_written": n * 4,
+                      "dispatches": 3}))
 
 
 def kernel_models(n, n_out, pairs, L, k3, passes):
@@ -81,6 +97,9 @@ def kernel_models(n, n_out, pairs, L, k3, passes):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        copy_calibration(args.calibrate_copy)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path.",
               file=sys.stderr)

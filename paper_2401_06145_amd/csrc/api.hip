@@ -344,7 +344,11 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
   p->pelem = elem_bytes(p->part_dtype);
   // tiles: default one 16-byte vector per thread for gather and for the partial reads of scatter
   p->t_gather = (opt && opt->t_gather) ? opt->t_gather : 16 / p->elem;
-  p->t_scatter = (opt && opt->t_scatter) ? opt->t_scatter : 16 / p->pelem;
+  // Algorithm 2 on gfx950 picked 16 channels (two 16-byte vectors) for 2-byte partials and
+  // 4 channels for float32 ones on every tuned layer; fall back to one vector if 16 does not divide
+  int ts_default = (p->pelem == 2) ? 16 : 4;
+  if (c_out % ts_default != 0) ts_default = 16 / p->pelem;
+  p->t_scatter = (opt && opt->t_scatter) ? opt->t_scatter : ts_default;
   if (p->t_gather <= 0 || c_in % p->t_gather != 0 || (p->t_gather * p->elem) % 16 != 0 ||
       (p->t_gather * p->elem / 16) > 16 || ((p->t_gather * p->elem / 16) & (p->t_gather * p->elem / 16 - 1)))
     return fail(SPCONV_EINVAL, "t_gather must divide c_in and span 1, 2, 4, 8 or 16 16-byte vectors");
@@ -492,9 +496,11 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   }
   {
     PhaseScope ph(PH_SORT, s);
-    hipError_t e = radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
+    hipError_t e = radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp,
+                                 &b.cb->err, s);
     if (e == hipSuccess && mode == SPCONV_UP)
-      e = radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits, b.sort_tmp, s);
+      e = radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits, b.sort_tmp,
+                        &b.cb->err, s);
     if (e != hipSuccess) return bail(hip_fail(e, "sort"));
   }
   if (mode == SPCONV_DOWN) {
@@ -502,7 +508,8 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     const int64_t cell = (int64_t)tensor_stride * stride;
     hipError_t e = launch_down_keys(b.skeys, n_src, L, cell, b.dkeys, b.dvals, s);
     if (e == hipSuccess)
-      e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp, s);
+      e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp,
+                        &b.cb->err, s);
     if (e == hipSuccess)
       e = unique_keys(b.dkeys, n_src, L, b.flags, b.pos, b.scan_tmp, b.qkeys, b.qrow, b.qcoords, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "output coordinates"));
@@ -554,6 +561,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     if (e != hipSuccess) return bail(hip_fail(e, "count read-back"));
     if (hc->err & kErrDup) return bail(fail(SPCONV_EDUP, "duplicate coordinates"));
     if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "work-item overflow in the balance step"));
+    if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "radix-sort look-back exceeded its wait bound"));
     if (hc->n_items > (uint32_t)b.max_items) return bail(fail(SPCONV_EHIP, "work items exceed the launch bound"));
     if (mode == SPCONV_DOWN) m->n_out = hc->n_q;
     for (int k = 0; k < K3; ++k) {

@@ -52,6 +52,7 @@ __device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
 // ---------------------------------------------------------------------------
 enum : uint32_t {
   kErrDup = 1u,          // two equal keys among the sorted inputs
+  kErrSpin = 2u,         // a look-back wait exceeded its bound
   kErrOverflow = 4u,     // more work items than the launch was sized for
 };
 
@@ -106,9 +107,10 @@ hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* 
 size_t radix_temp_bytes(int64_t n);
 // Sorts by the low `bits` key bits; the result ends in (keys, vals).  If `coords` is
 // non-null the input is those coordinates (keys packed with L, values = row index).
+// Look-back waits that exceed their bound set kErrSpin in *err (nothing hangs).
 hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals,
                          uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, int bits, void* d_temp,
-                         hipStream_t s);
+                         uint32_t* err, hipStream_t s);
 hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell,
                             uint64_t* dkeys, uint32_t* vals, hipStream_t s);
 // Distinct consecutive keys of sorted `keys` -> qkeys, qrow = position, coords; n_q into cb.

@@ -6,6 +6,7 @@
 // eight XCDs, so no kernel here has such a hot spot: reductions go through
 // per-block partials, and the match compaction is count -> scan -> write
 // (re-running the cheap LDS search) instead of a single pass with a look-back.
+#include <algorithm>
 #include <climits>
 
 #include "common.h"
@@ -125,13 +126,35 @@ __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, Key
 }
 
 // ----------------------------------------------------------------------------
-// LSD radix sort of (u64 key, u32 value), 8-bit digits, stable.
-// Per pass: per-tile digit histograms -> exclusive scan (digit-major) -> stable
-// scatter.  Ranks inside a tile come from wave64 ballots that match equal
-// digits.  The first pass may read int32 coordinates and pack the keys itself.
+// LSD radix sort of (u64 key, u32 value), 8-bit digits, stable, one kernel per
+// pass.  An up-front kernel counts the digits of every pass in one read
+// (per-block partials, no global atomics).  Each pass kernel then takes a tile
+// ticket, ranks its keys with wave64 ballots that match equal digits, publishes
+// its per-digit counts, and adds up the counts of all earlier tiles by looking
+// back over their published words.  Tiles are numbered in start order, so every
+// tile a workgroup waits for is already running; waits are bounded and report
+// an error flag instead of hanging.  The first pass may read int32 coordinates
+// and pack the keys itself.
 // ----------------------------------------------------------------------------
 constexpr int kRsItems = 8;
 constexpr int kRsTile = kThreads * kRsItems;
+constexpr int kRsUpBlocks = 64;
+constexpr int kRsMaxPasses = 8;
+constexpr uint32_t kStAgg = 1u << 30;   // word holds this tile's count of the digit
+constexpr uint32_t kStIncl = 2u << 30;  // word holds the count over tiles 0..this one
+constexpr uint32_t kStVal = (1u << 30) - 1u;
+constexpr uint32_t kSpinLimit = 1u << 20;
+constexpr int kLookWindow = 16;
+
+// Device-coherent (agent-scope) loads and stores of look-back words.  A word carries
+// its own payload (flag + count) and no other data is published with it, so relaxed
+// ordering suffices, which keeps a window of loads in flight together.
+__device__ __forceinline__ uint32_t ld_coherent(uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coherent(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // Lanes of the wave whose digit equals this lane's digit (among active lanes).
 __device__ __forceinline__ uint64_t match_digit(uint32_t d) {
@@ -157,7 +180,160 @@ __device__ __forceinline__ uint64_t load_key(const uint64_t* keys, const int4* c
 }
 
 template <bool FROM_COORDS>
-__global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t* keys, const int4* coords, KeyLayout L,
+__global__ __launch_bounds__(kThreads) void k_radix_upsweep(const uint64_t* keys, const int4* coords, KeyLayout L,
+                                                            int64_t n, int passes, uint32_t* gpart, uint32_t* status,
+                                                            int64_t status_words, uint32_t* tickets) {
+  __shared__ uint32_t h[kRsMaxPasses][256];
+  for (int p = 0; p < passes; ++p) h[p][threadIdx.x] = 0;
+  __syncthreads();
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
+    const uint64_t key = load_key<FROM_COORDS>(keys, coords, L, i);
+    for (int p = 0; p < passes; ++p) {
+      const uint32_t d = (uint32_t)(key >> (8 * p)) & 255u;
+      const uint64_t peers = match_digit(d);
+      if ((peers & lanemask_lt()) == 0) atomicAdd(&h[p][d], (uint32_t)popc64(peers));
+    }
+  }
+  __syncthreads();
+  for (int p = 0; p < passes; ++p) gpart[((int64_t)blockIdx.x * passes + p) * 256 + threadIdx.x] = h[p][threadIdx.x];
+  // clear the pass kernels' look-back words and tickets
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < status_words; i += (int64_t)gridDim.x * kThreads)
+    status[i] = 0u;
+  if (blockIdx.x == 0 && (int)threadIdx.x < passes) tickets[threadIdx.x] = 0u;
+}
+
+template <bool FROM_COORDS>
+__global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, const uint32_t* vin, const int4* coords,
+                                                         KeyLayout L, uint64_t* kout, uint32_t* vout, int64_t n,
+                                                         int pass, int passes, const uint32_t* gpart, int gblocks,
+                                                         uint32_t* status, uint32_t* tickets, uint32_t* err) {
+  __shared__ uint32_t s_tile;
+  __shared__ uint32_t cnt[256];
+  __shared__ uint32_t run[256];
+  __shared__ uint32_t wcnt[kWavesPerBlock][256];
+  __shared__ uint32_t s_wave[kWavesPerBlock];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int shift = 8 * pass;
+  if (tid == 0) s_tile = atomicAdd(&tickets[pass], 1u);
+  cnt[tid] = 0;
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][tid] = 0;
+  // count of digit `tid` over all keys, from the up-front partials
+  uint32_t tot = 0;
+  for (int g = 0; g < gblocks; ++g) tot += gpart[((int64_t)g * passes + pass) * 256 + tid];
+  __syncthreads();
+  const int64_t tile = s_tile;
+  const int64_t base = tile * kRsTile;
+
+  uint64_t key[kRsItems];
+  uint32_t val[kRsItems];
+#pragma unroll
+  for (int r = 0; r < kRsItems; ++r) {
+    const int64_t i = base + r * kThreads + tid;
+    key[r] = 0;
+    val[r] = 0;
+    if (i < n) {
+      key[r] = load_key<FROM_COORDS>(kin, coords, L, i);
+      val[r] = FROM_COORDS ? (uint32_t)i : vin[i];
+      const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
+      const uint64_t peers = match_digit(d);
+      if ((peers & lanemask_lt()) == 0) atomicAdd(&cnt[d], (uint32_t)popc64(peers));
+    }
+  }
+  // exclusive scan of the global digit counts: first position of digit `tid`
+  uint32_t x = tot;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, kWave);
+    if (lane >= d) x += y;
+  }
+  if (lane == kWave - 1) s_wave[wave] = x;
+  __syncthreads();
+  uint32_t gofs = x - tot;
+  for (int w = 0; w < wave; ++w) gofs += s_wave[w];
+
+  // publish this tile's count of digit `tid` and look back over earlier tiles
+  const uint32_t c = cnt[tid];
+  uint32_t* st = status + (int64_t)pass * gridDim.x * 256;
+  uint32_t excl = 0;
+  if (tile == 0) {
+    st_coherent(&st[tid], kStIncl | c);
+  } else {
+    st_coherent(&st[tile * 256 + tid], kStAgg | c);
+    // Windows of kLookWindow predecessor words are fetched together (independent
+    // loads in flight, each a device-coherent round trip), then consumed in order
+    // until an inclusive word ends the walk.
+    int64_t j = tile - 1;
+    uint32_t spins = 0;
+    bool done = false;
+    while (!done && j >= 0) {
+      uint32_t v[kLookWindow];
+#pragma unroll
+      for (int q = 0; q < kLookWindow; ++q) v[q] = (j - q >= 0) ? ld_coherent(&st[(j - q) * 256 + tid]) : kStIncl;
+      int q = 0;
+      for (; q < kLookWindow; ++q) {
+        const uint32_t f = v[q] & ~kStVal;
+        if (f == 0) break;  // not published yet: fetch again from here
+        excl += v[q] & kStVal;
+        if (f == kStIncl) {
+          done = true;
+          break;
+        }
+      }
+      if (done) break;
+      j -= q;
+      if (q < kLookWindow) {
+        if (++spins > kSpinLimit) {
+          atomicOr(err, kErrSpin);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    st_coherent(&st[tile * 256 + tid], kStIncl | (excl + c));
+  }
+  run[tid] = gofs + excl;
+  __syncthreads();
+
+  // stable scatter: rounds in index order, ranks within a round from wave ballots
+#pragma unroll
+  for (int r = 0; r < kRsItems; ++r) {
+    const int64_t i = base + r * kThreads + tid;
+    const bool valid = i < n;
+    uint32_t d = 0, rank = 0;
+    if (valid) {
+      d = (uint32_t)(key[r] >> shift) & 255u;
+      const uint64_t peers = match_digit(d);
+      rank = (uint32_t)popc64(peers & lanemask_lt());
+      if (rank == 0) wcnt[wave][d] = (uint32_t)popc64(peers);
+    }
+    __syncthreads();
+    if (valid) {
+      uint32_t pos = run[d] + rank;
+      for (int w = 0; w < wave; ++w) pos += wcnt[w][d];
+      kout[pos] = key[r];
+      vout[pos] = val[r];
+    }
+    __syncthreads();
+    uint32_t add = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      add += wcnt[w][tid];
+      wcnt[w][tid] = 0;
+    }
+    run[tid] += add;
+    __syncthreads();
+  }
+}
+
+// Small inputs (few tiles): per-tile digit histograms -> exclusive scan
+// (digit-major) -> stable scatter, three launches per pass.  With few tiles
+// every workgroup of a one-kernel pass would start at once and find no
+// inclusive prefix to stop its look-back, so this variant is faster there.
+template <bool FROM_COORDS>
+__global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, KeyLayout L,
                                                          int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
@@ -177,7 +353,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t* keys, c
 }
 
 template <bool FROM_COORDS>
-__global__ __launch_bounds__(kThreads) void k_radix_scatter(const uint64_t* kin, const uint32_t* vin,
+__global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t* kin, const uint32_t* vin,
                                                             const int4* coords, KeyLayout L, uint64_t* kout,
                                                             uint32_t* vout, int64_t n, int shift,
                                                             const uint32_t* offs, int64_t ntiles) {
@@ -512,49 +688,51 @@ hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* 
   return hipGetLastError();
 }
 
+// One-kernel passes need many more tiles than workgroups that run at once, so
+// that most look-backs stop at a finished predecessor.
+constexpr int64_t kOnesweepMinTiles = 1024;
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
 size_t radix_temp_bytes(int64_t n) {
-  const int64_t ntiles = (n + kRsTile - 1) / kRsTile;
-  const int64_t nh = 256 * (ntiles < 1 ? 1 : ntiles);
-  return (((size_t)nh * sizeof(uint32_t) + 255) & ~(size_t)255) + scan_temp_bytes(nh);
+  const int64_t ntiles = std::max<int64_t>(1, (n + kRsTile - 1) / kRsTile);
+  const size_t gpart = (size_t)kRsUpBlocks * kRsMaxPasses * 256 * sizeof(uint32_t);
+  const size_t status = (size_t)kRsMaxPasses * ntiles * 256 * sizeof(uint32_t);
+  const size_t onesweep = align256(gpart) + align256(status) + 256;
+  const size_t tiled = align256((size_t)256 * ntiles * sizeof(uint32_t)) + scan_temp_bytes(256 * ntiles);
+  return std::max(onesweep, tiled);
 }
 
-hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
-                         uint32_t* vals_alt, int64_t n, int bits, void* d_temp, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  const int passes = (bits + 7) / 8;
-  if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
-  if (n <= 1 || passes == 0) return hipSuccess;
+namespace {
+// Small inputs: three launches per pass (tile histograms, scan, scatter).
+hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+                            uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
   const int64_t ntiles = (n + kRsTile - 1) / kRsTile;
   uint32_t* hist = static_cast<uint32_t*>(d_temp);
-  void* scan_tmp = static_cast<char*>(d_temp) + (((size_t)256 * ntiles * sizeof(uint32_t) + 255) & ~(size_t)255);
+  void* scan_tmp = static_cast<char*>(d_temp) + align256((size_t)256 * ntiles * sizeof(uint32_t));
   const int4* c4 = reinterpret_cast<const int4*>(coords);
-  // ping-pong so that the last pass lands in (keys, vals)
   uint64_t* kb[2] = {keys, keys_alt};
   uint32_t* vb[2] = {vals, vals_alt};
-  int cur = (passes % 2 == 0) ? 0 : 1;  // buffer holding the input of the next pass
-  if (!coords) {
-    // input is in (keys, vals); an odd pass count needs one copy into the other buffer
-    if (passes % 2 == 1) {
-      ProfScope ps(KN_COPY, s);
-      hipError_t e = hipMemcpyAsync(keys_alt, keys, (size_t)n * 8, hipMemcpyDeviceToDevice, s);
-      if (e == hipSuccess) e = hipMemcpyAsync(vals_alt, vals, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
-      if (e != hipSuccess) return e;
-    }
+  int cur = (passes % 2 == 0) ? 0 : 1;
+  if (!coords && passes % 2 == 1) {
+    ProfScope ps(KN_COPY, s);
+    hipError_t e = hipMemcpyAsync(keys_alt, keys, (size_t)n * 8, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(vals_alt, vals, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return e;
   }
   for (int p = 0; p < passes; ++p) {
     const int shift = 8 * p;
     const bool first = (p == 0) && coords;
-    // the first pass from coordinates writes into buffer (passes odd ? 0 : 1) directly
     const int src = cur, dst = (first ? ((passes % 2 == 1) ? 0 : 1) : cur ^ 1);
     hipError_t e;
     {
       ProfScope ps(KN_RADIX_HIST, s);
       if (first)
-        hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, c4, L, n, shift,
-                           hist, ntiles);
-      else
-        hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], nullptr, L, n,
+        hipLaunchKernelGGL(k_radix_tile_hist<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, c4, L, n,
                            shift, hist, ntiles);
+      else
+        hipLaunchKernelGGL(k_radix_tile_hist<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], nullptr,
+                           L, n, shift, hist, ntiles);
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
@@ -563,11 +741,74 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
     {
       ProfScope ps(KN_RADIX_SCATTER, s);
       if (first)
-        hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr, c4,
-                           L, kb[dst], vb[dst], n, shift, hist, ntiles);
+        hipLaunchKernelGGL(k_radix_tile_scatter<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr,
+                           c4, L, kb[dst], vb[dst], n, shift, hist, ntiles);
       else
-        hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], vb[src],
-                           nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles);
+        hipLaunchKernelGGL(k_radix_tile_scatter<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src],
+                           vb[src], nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles);
+      e = hipGetLastError();
+    }
+    if (e != hipSuccess) return e;
+    cur = dst;
+  }
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+                         uint32_t* vals_alt, int64_t n, int bits, void* d_temp, uint32_t* err, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int passes = (bits + 7) / 8;
+  if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
+  if (n <= 1 || passes == 0) return hipSuccess;
+  if (passes > kRsMaxPasses || n >= ((int64_t)1 << 30)) return hipErrorInvalidValue;
+  const int64_t ntiles = (n + kRsTile - 1) / kRsTile;
+  if (ntiles < kOnesweepMinTiles)
+    return radix_sort_tiled(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
+  const size_t gpart_bytes = (size_t)kRsUpBlocks * kRsMaxPasses * 256 * sizeof(uint32_t);
+  uint32_t* gpart = static_cast<uint32_t*>(d_temp);
+  uint32_t* status = reinterpret_cast<uint32_t*>(static_cast<char*>(d_temp) + ((gpart_bytes + 255) & ~(size_t)255));
+  const int64_t status_words = (int64_t)passes * ntiles * 256;
+  uint32_t* tickets = reinterpret_cast<uint32_t*>(
+      reinterpret_cast<char*>(status) +
+      (((size_t)kRsMaxPasses * ntiles * 256 * sizeof(uint32_t) + 255) & ~(size_t)255));
+  const int gblocks = (int)std::min<int64_t>(kRsUpBlocks, ntiles);
+  const int4* c4 = reinterpret_cast<const int4*>(coords);
+  hipError_t e;
+  {
+    ProfScope ps(KN_RADIX_HIST, s);
+    if (coords)
+      hipLaunchKernelGGL(k_radix_upsweep<true>, dim3(gblocks), dim3(kThreads), 0, s, nullptr, c4, L, n, passes, gpart,
+                         status, status_words, tickets);
+    else
+      hipLaunchKernelGGL(k_radix_upsweep<false>, dim3(gblocks), dim3(kThreads), 0, s, keys, nullptr, L, n, passes,
+                         gpart, status, status_words, tickets);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  // ping-pong so that the last pass lands in (keys, vals)
+  uint64_t* kb[2] = {keys, keys_alt};
+  uint32_t* vb[2] = {vals, vals_alt};
+  int cur = (passes % 2 == 0) ? 0 : 1;  // buffer holding the input of the next pass
+  if (!coords && passes % 2 == 1) {
+    // input is in (keys, vals); an odd pass count needs one copy into the other buffer
+    ProfScope ps(KN_COPY, s);
+    e = hipMemcpyAsync(keys_alt, keys, (size_t)n * 8, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(vals_alt, vals, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return e;
+  }
+  for (int p = 0; p < passes; ++p) {
+    const bool first = (p == 0) && coords;
+    // the first pass from coordinates writes into buffer (passes odd ? 0 : 1) directly
+    const int src = cur, dst = (first ? ((passes % 2 == 1) ? 0 : 1) : cur ^ 1);
+    {
+      ProfScope ps(KN_RADIX_SCATTER, s);
+      if (first)
+        hipLaunchKernelGGL(k_radix_pass<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr, c4, L,
+                           kb[dst], vb[dst], n, p, passes, gpart, gblocks, status, tickets, err);
+      else
+        hipLaunchKernelGGL(k_radix_pass<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], vb[src],
+                           nullptr, L, kb[dst], vb[dst], n, p, passes, gpart, gblocks, status, tickets, err);
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

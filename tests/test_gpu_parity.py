@@ -230,6 +230,19 @@ def test_grouping_tiles_partials_are_result_neutral():
     assert e32 <= TOL["f16"] and e16 <= TOL["f16"] / 3
 
 
+def test_large_cloud_one_kernel_sort_passes():
+    """2.4M voxels: more than 1024 radix tiles, so the sort runs one kernel per pass
+    (tile ranks + look-back); K = 2 keeps the oracle's map fast."""
+    say("large uniform cloud, 2.4M voxels")
+    c = scenes.uniform_cells(2_400_000, 400, 4242)
+    km = B.KernelMap.build(to_dev(c), 2)
+    okm = oracle.kernel_map(c, None, 2, 1, "subm")
+    assert_map_equal(km, okm)
+    qd = B.KernelMap.build(to_dev(c), 2, 2, 1, "down")
+    q = oracle.out_coords(c, 2, 1)
+    assert np.array_equal(qd.out_coords().cpu().numpy(), q)
+
+
 def test_deterministic_pairs():
     say("deterministic pair order")
     c = scenes.workload(1).coords

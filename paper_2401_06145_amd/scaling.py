@@ -1,0 +1,103 @@
+"""Point-count scaling of the Map step on one MI355X.
+
+Extends the paper's density study (Section 6.2: random clouds in a 400^3 volume
+with 10^4 .. 10^6 points) to 16M voxels, to show where the Map kernels leave the
+latency-bound regime.  For each size it builds the submanifold K = 3 map
+(bounds, sort, backward search, balance, forward search, compaction) and reports
+phase times from HIP events, the compulsory Map bytes per second, and each main
+kernel's algorithmic bytes over its own event time.
+
+    python -m paper_2401_06145_amd.scaling --sizes 10000 100000 1000000 4000000 16000000
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+
+import torch
+
+if __package__ in (None, ""):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+from paper_2401_06145_amd import binding as B  # noqa: E402
+from paper_2401_06145_amd import scenes  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+
+
+def measure(n: int, side: int, rounds: int, K: int = 3):
+    dev = torch.device("cuda:0")
+    c = scenes.uniform_cells_large(n, side, 5000 + n % 997) if n > 1_000_000 else scenes.uniform_cells(n, side, 5000)
+    coords = torch.from_numpy(c).to(dev)
+    ws = torch.empty(B.spconv_map_workspace_bytes(n, 0, K, B.SPCONV_SUBM), dtype=torch.uint8, device=dev)
+
+    def build():
+        h = B.spconv_build_map(coords, None, K, 1, 1, B.SPCONV_SUBM, None, ws)
+        B.spconv_free_map(h)
+        return h
+
+    h = B.spconv_build_map(coords, None, K, 1, 1, B.SPCONV_SUBM, None, ws)
+    pairs = sum(B.spconv_map_counts(h))
+    B.spconv_free_map(h)
+    for _ in range(2):
+        build()
+    torch.cuda.synchronize()
+    ids = B.profile_ids()
+
+    def timed(mask):
+        B.spconv_profile_read(reset=True)
+        B.spconv_profile_enable(mask)
+        for _ in range(rounds):
+            build()
+        torch.cuda.synchronize()
+        B.spconv_profile_enable(False)
+        return B.spconv_profile_read(reset=True)
+
+    ph = timed(B.PHASES_ALL)
+    phases = {k: v[0] / rounds for k, v in ph.items() if not k.startswith("k_") and v[1] > 0}
+    kern = {}
+    for name in ("k_radix_scatter", "k_radix_hist", "k_backward", "k_forward_count", "k_forward_write"):
+        ms, cnt = timed(1 << ids[name])[name]
+        if cnt:
+            kern[name] = (ms / cnt, cnt / rounds)
+    k3 = K ** 3
+    map_ms = sum(phases.values())
+    sort_ms = phases.get("sort", 0.0)
+    # compulsory bytes: sort 28 B/voxel; search 8|Q| + 12|P| + 8M + counts
+    map_bytes = 28 * n + 8 * n + 12 * n + 8 * pairs + 4 * (k3 + 1)
+    passes = kern.get("k_radix_scatter", (0, 0))[1]
+    per_launch = {
+        "k_radix_scatter": (16 * n + 12 * n + (passes - 1) * 24 * n) / max(passes, 1),
+        "k_forward_count": 8 * n + 8 * n + 4 * k3 * n,
+        "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 8 * pairs,
+    }
+    row = {"voxels": n, "grid": side, "pairs": pairs, "map_ms": round(map_ms, 4),
+           "phases_ms": {k: round(v, 4) for k, v in phases.items()},
+           "map_gbps_compulsory": round(map_bytes / (map_ms * 1e-3) / 1e9, 1),
+           "sort_gbps": round(28 * n / (sort_ms * 1e-3) / 1e9, 1) if sort_ms else None,
+           "kernels": {}}
+    for name, (ms, per_step) in kern.items():
+        ent = {"mean_launch_ms": round(ms, 4), "launches_per_build": per_step}
+        if name in per_launch:
+            gbs = per_launch[name] / (ms * 1e-3) / 1e9
+            ent.update({"gbps": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)})
+        row["kernels"][name] = ent
+    return row
+
+
+def main(argv=None):
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--sizes", type=int, nargs="+",
+                   default=[10_000, 100_000, 1_000_000, 2_000_000, 4_000_000, 8_000_000, 16_000_000])
+    p.add_argument("--rounds", type=int, default=10)
+    a = p.parse_args(argv)
+    if not torch.cuda.is_available():
+        raise SystemExit("the sweep needs a GPU")
+    for n in a.sizes:
+        side = 400 if n <= 1_000_000 else 800
+        print(json.dumps(measure(n, side, a.rounds)), flush=True)
+
+
+if __name__ == "__main__":
+    main()

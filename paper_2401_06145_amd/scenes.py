@@ -99,6 +99,24 @@ def uniform_cells(n: int, side: int, seed: int, batch: int = 0) -> np.ndarray:
     return np.ascontiguousarray(c)
 
 
+def uniform_cells_large(n: int, side: int, seed: int, batch: int = 0) -> np.ndarray:
+    """``n`` distinct cells of a side^3 grid for large n (draws with replacement,
+    keeps distinct cells, trims to n in a seeded random order)."""
+    rng = np.random.default_rng(seed)
+    total = side ** 3
+    if n > total // 2:
+        raise ValueError("density too high for rejection drawing")
+    cells = np.unique(rng.integers(0, total, int(n * 1.1) + 1024, dtype=np.int64))
+    while cells.size < n:
+        cells = np.unique(np.concatenate([cells, rng.integers(0, total, n, dtype=np.int64)]))
+    cells = cells[rng.permutation(cells.size)[:n]]
+    x = cells // (side * side)
+    y = (cells // side) % side
+    z = cells % side
+    b = np.full(n, batch, dtype=np.int64)
+    return np.ascontiguousarray(np.stack([b, x, y, z], axis=1).astype(np.int32))
+
+
 # ----------------------------------------------------------------------------
 # LiDAR-like outdoor scene
 # ----------------------------------------------------------------------------

@@ -76,7 +76,10 @@ typedef struct {
   int partial_dtype; /* GEMM partial (output buffer) precision: 1 = float32, 2 = layer dtype;
                         0 = default (layer dtype; sums are float32 either way) */
   int launch_cost_rows; /* grouping policy: one launch costs this many padded rows; default 32768 */
-  int reserved[9];
+  int presorted;     /* spconv_build_map: 1 = the input rows are already unique and in ascending
+                        (b, x, y, z) order (e.g. a DOWN map's outputs), so the sort is skipped
+                        (Section 5.1.1); checked on the device (SPCONV_EINVAL if not sorted) */
+  int reserved[8];
 } spconv_options;
 
 typedef struct spconv_map spconv_map; /* opaque host-side object */
@@ -147,6 +150,20 @@ size_t spconv_forward_workspace_bytes(const spconv_map* m, int c_in, int c_out, 
 int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in,
                    int c_out, int dtype, const spconv_options* opt, void* d_workspace,
                    size_t ws_bytes, void* stream);
+
+/* spconv_forward with an elementwise epilogue fused into the scatter's single
+ * write: y = act(sum + residual).  d_residual: NULL or [n_out][c_out] in `dtype`
+ * (may equal d_y); relu != 0 applies max(0, .) after the add.  For networks of
+ * sparse-conv layers (residual blocks, ReLU after each conv). */
+int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in,
+                      int c_out, int dtype, const void* d_residual, int relu,
+                      const spconv_options* opt, void* d_workspace, size_t ws_bytes, void* stream);
+
+/* Row-wise channel concatenation d_out[i] = [d_a[i] | d_b[i]] of [n][c_a] and
+ * [n][c_b] in `dtype` (c * element size a multiple of 16 bytes); for the skip
+ * connections of encoder-decoder networks.  Asynchronous on `stream`. */
+int spconv_concat_rows(const void* d_a, int c_a, const void* d_b, int c_b, void* d_out, int64_t n,
+                       int dtype, void* stream);
 
 /* What spconv_forward will launch for this map (host-only): padded and real
  * buffer rows (padding overhead = (padded - real) / real, Section 3 figure on

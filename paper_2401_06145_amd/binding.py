@@ -26,7 +26,8 @@ TORCH_DTYPES = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat
 EXPORTED = [
     "spconv_map_workspace_bytes", "spconv_build_map", "spconv_map_transpose", "spconv_map_n_in",
     "spconv_map_n_out", "spconv_map_kvol", "spconv_map_out_coords", "spconv_map_counts",
-    "spconv_map_pairs", "spconv_map_copy_pairs", "spconv_map_copy_out_coords", "spconv_free_map", "spconv_forward_workspace_bytes", "spconv_forward",
+    "spconv_map_pairs", "spconv_map_copy_pairs", "spconv_map_copy_out_coords", "spconv_free_map",
+    "spconv_forward_workspace_bytes", "spconv_forward", "spconv_forward_ex", "spconv_concat_rows",
     "spconv_forward_plan", "spconv_profile_enable", "spconv_profile_phase_count",
     "spconv_profile_phase_name", "spconv_profile_read", "spconv_last_error",
 ]
@@ -41,7 +42,7 @@ class SpconvError(RuntimeError):
 class Options(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int), ("Cq", ctypes.c_int), ("t_gather", ctypes.c_int),
                 ("t_scatter", ctypes.c_int), ("grouping", ctypes.c_int), ("partial_dtype", ctypes.c_int),
-                ("launch_cost_rows", ctypes.c_int), ("reserved", ctypes.c_int * 9)]
+                ("launch_cost_rows", ctypes.c_int), ("presorted", ctypes.c_int), ("reserved", ctypes.c_int * 8)]
 
     @classmethod
     def make(cls, **kw) -> "Options":
@@ -99,6 +100,10 @@ def lib() -> ctypes.CDLL:
     L.spconv_forward_workspace_bytes.restype = sz
     L.spconv_forward.argtypes = [vp, vp, vp, vp, c_int, c_int, c_int, optp, vp, sz, vp]
     L.spconv_forward.restype = c_int
+    L.spconv_forward_ex.argtypes = [vp, vp, vp, vp, c_int, c_int, c_int, vp, c_int, optp, vp, sz, vp]
+    L.spconv_forward_ex.restype = c_int
+    L.spconv_concat_rows.argtypes = [vp, c_int, vp, c_int, vp, i64, c_int, vp]
+    L.spconv_concat_rows.restype = c_int
     L.spconv_forward_plan.argtypes = [vp, c_int, c_int, c_int, optp, ctypes.POINTER(PlanInfo)]
     L.spconv_forward_plan.restype = c_int
     L.spconv_profile_enable.argtypes = [ctypes.c_uint64]
@@ -186,6 +191,25 @@ def spconv_forward(m, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, c_in: i
     st = lib().spconv_forward(m, _ptr(x), _ptr(w), _ptr(y), c_in, c_out, dtype, _opt(opt), _ptr(workspace),
                               workspace.numel(), _stream(stream))
     _check(st, "spconv_forward")
+
+
+def spconv_forward_ex(m, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, c_in: int, c_out: int, dtype: int,
+                      residual: torch.Tensor | None, relu: bool, opt: Options | None, workspace: torch.Tensor,
+                      stream=None) -> None:
+    st = lib().spconv_forward_ex(m, _ptr(x), _ptr(w), _ptr(y), c_in, c_out, dtype, _ptr(residual), 1 if relu else 0,
+                                 _opt(opt), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "spconv_forward_ex")
+
+
+def spconv_concat_rows(a: torch.Tensor, b: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    if a.shape[0] != b.shape[0] or a.dtype != b.dtype:
+        raise ValueError("row counts / dtypes differ")
+    if out is None:
+        out = torch.empty((a.shape[0], a.shape[1] + b.shape[1]), dtype=a.dtype, device=a.device)
+    st = lib().spconv_concat_rows(_ptr(a), a.shape[1], _ptr(b), b.shape[1], _ptr(out), a.shape[0], DTYPES[a.dtype],
+                                  _stream(stream))
+    _check(st, "spconv_concat_rows")
+    return out
 
 
 def spconv_forward_plan(m, c_in: int, c_out: int, dtype: int, opt: Options | None = None) -> PlanInfo:
@@ -319,15 +343,23 @@ class Forward:
         self.workspace = _device_bytes(n, dev)
         self.device = dev
 
-    def __call__(self, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    def __call__(self, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor | None = None, stream=None,
+                 residual: torch.Tensor | None = None, relu: bool = False) -> torch.Tensor:
         if y is None:
             y = torch.empty((self.kmap.n_out, self.c_out), dtype=self.dtype, device=self.device)
-        for t, shape in ((x, (self.kmap.n_in, self.c_in)), (w, (self.kmap.kvol, self.c_in, self.c_out)),
-                         (y, (self.kmap.n_out, self.c_out))):
+        checks = [(x, (self.kmap.n_in, self.c_in)), (w, (self.kmap.kvol, self.c_in, self.c_out)),
+                  (y, (self.kmap.n_out, self.c_out))]
+        if residual is not None:
+            checks.append((residual, (self.kmap.n_out, self.c_out)))
+        for t, shape in checks:
             if tuple(t.shape) != shape or t.dtype != self.dtype or not t.is_contiguous():
                 raise ValueError(f"expected contiguous {self.dtype} {shape}, got {t.dtype} {tuple(t.shape)}")
-        spconv_forward(self.kmap.handle, x, w, y, self.c_in, self.c_out, DTYPES[self.dtype], self.opt,
-                       self.workspace, stream)
+        if residual is None and not relu:
+            spconv_forward(self.kmap.handle, x, w, y, self.c_in, self.c_out, DTYPES[self.dtype], self.opt,
+                           self.workspace, stream)
+        else:
+            spconv_forward_ex(self.kmap.handle, x, w, y, self.c_in, self.c_out, DTYPES[self.dtype], residual, relu,
+                              self.opt, self.workspace, stream)
         return y
 
 

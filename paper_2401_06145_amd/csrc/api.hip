@@ -184,6 +184,7 @@ struct MapBufs {
 struct Tunables {
   int B = 1024;
   int Cq = 1024;
+  bool presorted = false;
 };
 
 int read_tunables(const spconv_options* opt, Tunables* t) {
@@ -199,6 +200,7 @@ int read_tunables(const spconv_options* opt, Tunables* t) {
       return fail(SPCONV_EINVAL, "Cq must be 256, 512, 1024 or 2048");
     t->Cq = opt->Cq;
   }
+  t->presorted = opt->presorted != 0;
   return SPCONV_OK;
 }
 
@@ -496,11 +498,14 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   }
   {
     PhaseScope ph(PH_SORT, s);
-    hipError_t e = radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp,
-                                 &b.cb->err, s);
+    // sorted inputs (a previous layer's outputs) only need their keys packed (Section 5.1.1)
+    hipError_t e = tu.presorted ? launch_pack(src_coords, n_src, L, b.skeys, b.sidx, s)
+                                : radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits,
+                                                b.sort_tmp, &b.cb->err, s);
     if (e == hipSuccess && mode == SPCONV_UP)
-      e = radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits, b.sort_tmp,
-                        &b.cb->err, s);
+      e = tu.presorted ? launch_pack(d_in_coords, n_in, L, b.qkeys, b.qrow, s)
+                       : radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits,
+                                       b.sort_tmp, &b.cb->err, s);
     if (e != hipSuccess) return bail(hip_fail(e, "sort"));
   }
   if (mode == SPCONV_DOWN) {
@@ -562,6 +567,8 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     if (hc->err & kErrDup) return bail(fail(SPCONV_EDUP, "duplicate coordinates"));
     if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "work-item overflow in the balance step"));
     if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "radix-sort look-back exceeded its wait bound"));
+    if (hc->err & kErrUnsorted)
+      return bail(fail(SPCONV_EINVAL, "rows declared presorted are not in ascending (b, x, y, z) order"));
     if (hc->n_items > (uint32_t)b.max_items) return bail(fail(SPCONV_EHIP, "work items exceed the launch bound"));
     if (mode == SPCONV_DOWN) m->n_out = hc->n_q;
     for (int k = 0; k < K3; ++k) {
@@ -659,6 +666,24 @@ int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype, con
 
 int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in, int c_out, int dtype,
                    const spconv_options* opt, void* d_workspace, size_t ws_bytes, void* stream) {
+  return spconv_forward_ex(m, d_x, d_w, d_y, c_in, c_out, dtype, nullptr, 0, opt, d_workspace, ws_bytes, stream);
+}
+
+int spconv_concat_rows(const void* d_a, int c_a, const void* d_b, int c_b, void* d_out, int64_t n, int dtype,
+                       void* stream) {
+  if (dtype != SPCONV_F32 && dtype != SPCONV_F16 && dtype != SPCONV_BF16) return fail(SPCONV_EUNSUPPORTED, "dtype");
+  const int e = elem_bytes(dtype);
+  if (n < 0 || c_a < 0 || c_b < 0 || (c_a * e) % 16 != 0 || (c_b * e) % 16 != 0)
+    return fail(SPCONV_EUNSUPPORTED, "concat needs 16-byte channel blocks");
+  if (n == 0 || c_a + c_b == 0) return SPCONV_OK;
+  if (!d_out || (c_a && !d_a) || (c_b && !d_b)) return fail(SPCONV_EINVAL, "NULL pointer");
+  SPC_TRY(launch_concat(d_a, c_a, d_b, c_b, d_out, n, e, static_cast<hipStream_t>(stream)), "concat");
+  return SPCONV_OK;
+}
+
+int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in, int c_out,
+                      int dtype, const void* d_residual, int relu, const spconv_options* opt, void* d_workspace,
+                      size_t ws_bytes, void* stream) {
   GmasPlan p;
   int st = make_plan(m, c_in, c_out, dtype, opt, &p);
   if (st != SPCONV_OK) return st;
@@ -698,7 +723,8 @@ int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* 
   }
   {
     PhaseScope ph(PH_SCATTER, s);
-    SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, b.omt, p.mt_stride, K3, d_y, dtype, p.t_scatter, s),
+    SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, b.omt, p.mt_stride, K3, d_y, dtype, p.t_scatter,
+                           d_residual, relu, s),
             "scatter");
   }
   return SPCONV_OK;

@@ -54,6 +54,7 @@ enum : uint32_t {
   kErrDup = 1u,          // two equal keys among the sorted inputs
   kErrSpin = 2u,         // a look-back wait exceeded its bound
   kErrOverflow = 4u,     // more work items than the launch was sized for
+  kErrUnsorted = 8u,     // rows declared sorted are not in (b, x, y, z) order
 };
 
 // Small control block in device memory, read back once at the end of a map build.
@@ -161,9 +162,13 @@ hipError_t launch_mt_pairs(const int32_t* pin, const int32_t* pout, int64_t m_to
 hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const int32_t* imt,
                          int mt_stride, int K3, void* buf_in, int tile, hipStream_t s);
 // Scatter: y[i] = sum_k buf_out[omt[i][k]] (float32 sum), tile T channels per thread.
+// Optional epilogue: y = relu?(sum + residual) (residual NULL: none).
 hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out,
                           const int32_t* omt, int mt_stride, int K3, void* y, int dtype, int tile,
-                          hipStream_t s);
+                          const void* residual, int relu, hipStream_t s);
+// out[i] = [a[i] | b[i]] for row-major a [n][ca], b [n][cb] (16-byte multiples).
+hipError_t launch_concat(const void* a, int ca, const void* b, int cb, void* out, int64_t n, int elem,
+                         hipStream_t s);
 
 // gemm_mfma.hip: grouped per-offset GEMMs, buf_out[rows of k] = buf_in[rows of k] W_k.
 // A segment is one offset's run of buffer rows; `height` >= `rows` is the padded

@@ -83,11 +83,13 @@ __device__ __forceinline__ __half from_f32<__half>(float v) { return __float2hal
 template <>
 __device__ __forceinline__ __hip_bfloat16 from_f32<__hip_bfloat16>(float v) { return __float2bfloat16(v); }
 
-// TILE channels per thread; partials of type TP, output of type TO.
+// TILE channels per thread; partials of type TP, output of type TO.  Optional
+// epilogue fused into the single write: y = relu?(sum + residual).  `residual`
+// may alias y (each thread reads its tile before writing it).
 template <int TILE, typename TP, typename TO>
 __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf, int64_t n_out, int c_out,
                                                       const int32_t* __restrict__ omt, int stride, int K3,
-                                                      TO* __restrict__ y) {
+                                                      TO* y, const TO* residual, int relu) {
   static_assert((TILE * sizeof(TP)) % 16 == 0, "partial tile must be whole 16-byte vectors");
   constexpr int VP = TILE * sizeof(TP) / 16;
   const int tiles = c_out / TILE;
@@ -116,6 +118,15 @@ __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf
       }
     }
   }
+  if (residual) {
+    const TO* rsd = residual + i * (int64_t)c_out + (int64_t)t * TILE;
+#pragma unroll
+    for (int c = 0; c < TILE; ++c) acc[c] += to_f32<TO>(rsd[c]);
+  }
+  if (relu) {
+#pragma unroll
+    for (int c = 0; c < TILE; ++c) acc[c] = fmaxf(acc[c], 0.f);
+  }
   TO out[TILE];
 #pragma unroll
   for (int c = 0; c < TILE; ++c) out[c] = from_f32<TO>(acc[c]);
@@ -137,19 +148,20 @@ unsigned blocks_for(int64_t threads) { return (unsigned)((threads + kThreads - 1
 
 template <typename TP, typename TO>
 hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* omt, int stride, int K3, void* y,
-                     int tile, hipStream_t s) {
+                     int tile, const void* residual, int relu, hipStream_t s) {
   ProfScope ps(KN_SCATTER, s);
   const int64_t threads = n_out * (c_out / tile);
   const dim3 g(blocks_for(threads)), b(kThreads);
   const TP* p = static_cast<const TP*>(buf);
   TO* o = static_cast<TO*>(y);
+  const TO* r = static_cast<const TO*>(residual);
   switch (tile) {
-#define SPC_SC(T)                                                                          \
-  case T:                                                                                  \
-    if constexpr ((T * sizeof(TP)) % 16 == 0) {                                            \
-      hipLaunchKernelGGL((k_scatter<T, TP, TO>), g, b, 0, s, p, n_out, c_out, omt, stride, K3, o); \
-      return hipGetLastError();                                                            \
-    }                                                                                      \
+#define SPC_SC(T)                                                                                    \
+  case T:                                                                                            \
+    if constexpr ((T * sizeof(TP)) % 16 == 0) {                                                      \
+      hipLaunchKernelGGL((k_scatter<T, TP, TO>), g, b, 0, s, p, n_out, c_out, omt, stride, K3, o, r, relu); \
+      return hipGetLastError();                                                                      \
+    }                                                                                                \
     return hipErrorInvalidValue;
     SPC_SC(4)
     SPC_SC(8)
@@ -202,20 +214,46 @@ hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const 
 }
 
 hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out, const int32_t* omt,
-                          int mt_stride, int K3, void* y, int dtype, int tile, hipStream_t s) {
+                          int mt_stride, int K3, void* y, int dtype, int tile, const void* residual, int relu,
+                          hipStream_t s) {
   if (n_out <= 0) return hipSuccess;
   if (tile <= 0 || c_out % tile != 0) return hipErrorInvalidValue;
   // part_dtype / dtype: 0 = f32, 1 = f16, 2 = bf16
   if (part_dtype == 0) {
-    if (dtype == 0) return scatter_t<float, float>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, s);
-    if (dtype == 1) return scatter_t<float, __half>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, s);
-    if (dtype == 2) return scatter_t<float, __hip_bfloat16>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, s);
+    if (dtype == 0) return scatter_t<float, float>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
+    if (dtype == 1)
+      return scatter_t<float, __half>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
+    if (dtype == 2)
+      return scatter_t<float, __hip_bfloat16>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
   } else if (part_dtype == 1 && dtype == 1) {
-    return scatter_t<__half, __half>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, s);
+    return scatter_t<__half, __half>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
   } else if (part_dtype == 2 && dtype == 2) {
-    return scatter_t<__hip_bfloat16, __hip_bfloat16>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, s);
+    return scatter_t<__hip_bfloat16, __hip_bfloat16>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual,
+                                                     relu, s);
   }
   return hipErrorInvalidValue;
+}
+
+namespace {
+// out[i] = [a[i] (ca channels) | b[i] (cb channels)]; one thread per 16-byte vector of out.
+__global__ __launch_bounds__(kThreads) void k_concat(const uint4* a, int va, const uint4* b, int vb, uint4* out,
+                                                     int64_t n) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int vo = va + vb;
+  const int64_t i = gid / vo;
+  const int v = (int)(gid - i * vo);
+  if (i >= n) return;
+  out[gid] = (v < va) ? a[i * va + v] : b[i * vb + (v - va)];
+}
+}  // namespace
+
+hipError_t launch_concat(const void* a, int ca, const void* b, int cb, void* out, int64_t n, int elem, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int va = ca * elem / 16, vb = cb * elem / 16;
+  const int64_t threads = n * (va + vb);
+  hipLaunchKernelGGL(k_concat, dim3(blocks_for(threads)), dim3(kThreads), 0, s, static_cast<const uint4*>(a), va,
+                     static_cast<const uint4*>(b), vb, static_cast<uint4*>(out), n);
+  return hipGetLastError();
 }
 
 }  // namespace spc

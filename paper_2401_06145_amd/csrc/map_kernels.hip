@@ -489,14 +489,26 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
     chunks[wid] = (uint32_t)((hi - lo + a.Cq - 1) / a.Cq);
   }
   if (k == 0) {
-    bool dup = false;
+    // the source (and, for transposed maps, query) keys must be strictly increasing:
+    // equal neighbours are repeated coordinates, decreasing ones an unsorted input
+    // that was declared sorted
+    bool dup = false, unsorted = false;
     const int64_t s0 = b * (int64_t)a.B;
-    for (int64_t e = s0 + lane; e <= last; e += kWave) dup |= (e > 0 && a.skeys[e] == a.skeys[e - 1]);
+    for (int64_t e = s0 + lane; e <= last; e += kWave)
+      if (e > 0) {
+        dup |= a.skeys[e] == a.skeys[e - 1];
+        unsorted |= a.skeys[e] < a.skeys[e - 1];
+      }
     if (a.check_q) {
       const int64_t per = (nq + nb - 1) / nb;
-      for (int64_t e = b * per + lane; e < min((b + 1) * per, nq); e += kWave) dup |= (e > 0 && a.qkeys[e] == a.qkeys[e - 1]);
+      for (int64_t e = b * per + lane; e < min((b + 1) * per, nq); e += kWave)
+        if (e > 0) {
+          dup |= a.qkeys[e] == a.qkeys[e - 1];
+          unsorted |= a.qkeys[e] < a.qkeys[e - 1];
+        }
     }
     if (__ballot(dup) != 0 && lane == 0) atomicOr(&cb->err, kErrDup);
+    if (__ballot(unsorted) != 0 && lane == 0) atomicOr(&cb->err, kErrUnsorted);
   }
 }
 

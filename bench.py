@@ -2,8 +2,8 @@
 
 A step runs the whole hot path on one seeded LiDAR-like scene (about 120k voxels,
 submanifold K = 3, C_in = C_out = 64, float16): coordinate bounds, key packing and
-radix sort, the double-traversed binary search with pair compaction (Map), then
-metadata tables, gather, grouped MFMA GEMMs and scatter (GMaS).  Inputs are
+radix sort, the double-traversed binary search with pair compaction and the
+metadata tables (Map), then gather, grouped MFMA GEMMs and scatter (GMaS).  Inputs are
 resident in HBM before timing starts.  Prints one JSON line.
 
 Measurement:
@@ -28,8 +28,8 @@ sys.path.insert(0, ROOT)
 METRIC = "sparse-conv layer ms (Map + GMaS split); Map GB/s, GEMM TFLOP/s vs peak"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}
-MAP_PHASES = ("bounds", "sort", "outcoords", "backward", "balance", "forward", "readback")
-GMAS_PHASES = ("metadata", "gather", "gemm", "scatter")
+MAP_PHASES = ("bounds", "sort", "outcoords", "backward", "balance", "metadata", "forward", "readback")
+GMAS_PHASES = ("gather", "gemm", "scatter")
 
 
 def parse():
@@ -68,7 +68,6 @@ def kernel_models(n, n_out, pairs, L, k3, passes):
     """
     e = 4 if L.dtype == "f32" else 2
     ep = e  # GEMM partials are stored in the layer dtype
-    k3p = (k3 + 3) // 4 * 4
     P = max(passes, 1)
     # scans per step: one digit-offset scan per radix pass (256 x tiles of 2048 keys),
     # the chunk-count scan (K^3 x source blocks of 1024) and the match-count scan
@@ -81,14 +80,17 @@ def kernel_models(n, n_out, pairs, L, k3, passes):
         "k_radix_scatter": ("hbm", (16 * n + 12 * n + (P - 1) * 24 * n) / P),
         "k_radix_hist": ("hbm", (16 * n + (P - 1) * 8 * n) / P),
         "k_minmax": ("hbm", 16 * n),
-        # forward search: query keys and source keys once, one result word per query
+        # forward search: query keys and source keys once, one result word per (offset, query)
         "k_forward_count": ("hbm", 8 * n_out + 8 * n + 4 * k3 * n_out),
-        "k_forward_write": ("hbm", 4 * k3 * n_out + 4 * n_out + 4 * n + 8 * pairs),
+        # write pass: reads the results and the rows of the matches; writes the pair lists,
+        # the query-side table's matches (in place) and the whole source-side table
+        "k_forward_write": ("hbm", 4 * k3 * n_out + 4 * n_out + 4 * n + 12 * pairs + 4 * k3 * n),
         "k_backward": ("hbm", 8 * n_out),
-        "k_fill": ("hbm", 4 * (n + n_out) * k3p / 2),
-        "k_mt_pairs": ("hbm", 16 * pairs),
-        "k_gather": ("hbm", (n + pairs) * L.c_in * e + 4 * n * k3p),
-        "k_scatter": ("hbm", pairs * L.c_out * ep + n_out * L.c_out * e + 4 * n_out * k3p),
+        # source-side table fill (maps other than odd-K submanifold ones)
+        "k_fill": ("hbm", 4 * k3 * n),
+        # gather / scatter: feature rows, partial rows, one table entry per (offset, point), row map
+        "k_gather": ("hbm", (n + pairs) * L.c_in * e + 4 * n * (k3 + 1)),
+        "k_scatter": ("hbm", pairs * L.c_out * ep + n_out * L.c_out * e + 4 * n_out * (k3 + 1)),
         "k_gemm_bytes": ("hbm", pairs * (L.c_in * e + L.c_out * ep) + k3 * L.c_in * L.c_out * e),
         "k_gemm_flops": ("mfma", 2.0 * pairs * L.c_in * L.c_out),
     }

@@ -6,11 +6,13 @@
  * Gather-GEMM-Scatter (GMaS) step applies it to the features.
  *
  *   spconv_build_map   Map step: sorted coordinates, output coordinates (Eq. 1),
- *                      segmented query sorting (Section 5.1.1) and the
- *                      double-traversed binary search (Section 5.1.2).
- *   spconv_forward     GMaS step: metadata tables, autotunable-tile Gather
- *                      (Algorithm 1), reordered and grouped per-offset GEMMs on
- *                      MFMA (Section 5.2.2) and Scatter (Section 2.2, Step 2).
+ *                      segmented query sorting (Section 5.1.1), the
+ *                      double-traversed binary search (Section 5.1.2), and the
+ *                      GMaS metadata tables (Section 2.2), written as the
+ *                      search ranks its matches.
+ *   spconv_forward     GMaS step: autotunable-tile Gather (Algorithm 1),
+ *                      reordered and grouped per-offset GEMMs on MFMA
+ *                      (Section 5.2.2) and Scatter (Section 2.2, Step 2).
  *   spconv_free_map    releases a map's host object.
  *
  * Conventions shared by every entry point:
@@ -104,7 +106,9 @@ size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode,
  *   d_workspace  at least spconv_map_workspace_bytes(...) bytes, 256-byte aligned.
  * Pair indices are rows of the caller's arrays: input rows in the caller's order;
  * output rows in the caller's order for SUBM / UP and in sorted (b,x,y,z) order for
- * DOWN.  Synchronises `stream` twice (coordinate bounds, then per-offset counts).
+ * DOWN.  The map also holds the metadata tables of the GMaS step.  K^3 * max(n_in,
+ * n_out) must stay below 2^31 (int32 pair indices; SPCONV_EUNSUPPORTED otherwise).
+ * Synchronises `stream` twice (coordinate bounds, then per-offset counts).
  * On success *out_map owns a host object to release with spconv_free_map(). */
 int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords,
                      int64_t n_out, int K, int stride, int tensor_stride, int mode,
@@ -183,7 +187,8 @@ int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype,
  * Event timing: for every id whose bit is set in `mask`, the library records HIP
  * events on the caller's stream around that phase of spconv_build_map /
  * spconv_forward (ids 0..10: bounds, sort, outcoords, backward, balance, forward,
- * readback, metadata, gather, gemm, scatter) or around each launch of that kernel
+ * readback, metadata (the table fill of maps other than odd-K submanifold ones),
+ * gather, gemm, scatter) or around each launch of that kernel
  * (ids 16..31; spconv_profile_phase_name() gives the names, "" for unused ids).
  * mask = 0 turns timing off.  spconv_profile_read() waits for the recorded events
  * and writes the summed milliseconds and the number of timed intervals per id

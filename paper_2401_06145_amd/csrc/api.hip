@@ -21,6 +21,14 @@ struct spconv_map {
   const int32_t* pout = nullptr;
   std::vector<int64_t> counts;    // |M_k|
   std::vector<int64_t> ptr;       // prefix of counts, K3 + 1 entries
+  // metadata tables, offset-major over sorted positions (entry k * stride + p:
+  // buffer row of point p's pair at offset k, or -1), and the caller row of each
+  // sorted position (NULL: identity); NULL tables for a map without pairs
+  const int32_t* imt = nullptr;
+  const int32_t* omt = nullptr;
+  int64_t imt_stride = 0, omt_stride = 0;
+  const uint32_t* in_perm = nullptr;
+  const uint32_t* out_perm = nullptr;
   bool transposed = false;
 };
 
@@ -73,7 +81,7 @@ const char* prof_name(int id) {
       "bounds", "sort", "outcoords", "backward", "balance", "forward", "readback", "metadata", "gather", "gemm",
       "scatter", "", "", "", "", "",
       "k_minmax", "k_radix_hist", "k_radix_scatter", "k_scan", "k_copy", "k_down_keys", "k_unique", "k_backward",
-      "k_forward_count", "k_forward_write", "k_fill", "k_mt_pairs", "k_gather", "k_gemm", "k_scatter", "k_pack",
+      "k_forward_count", "k_forward_write", "k_fill", "", "k_gather", "k_gemm", "k_scatter", "k_pack",
       "", "", "", "", "", "", "", ""};
   return (id >= 0 && id < PROF_IDS) ? kNames[id] : "";
 }
@@ -172,7 +180,8 @@ struct MapBufs {
   uint32_t* bounds;
   uint32_t* chunks;
   uint32_t* istart;
-  int32_t* res;
+  int32_t* res;   // T_q, kept as the map's query-side metadata table
+  int32_t* ts;    // T_s, the source-side table
   uint32_t* item_cnt;
   uint32_t* item_off;
   int32_t* mm_partial;
@@ -231,6 +240,7 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   b->chunks = m.take<uint32_t>(nkb);
   b->istart = m.take<uint32_t>(nkb);
   b->res = m.take<int32_t>((int64_t)K3 * nq_max);
+  b->ts = m.take<int32_t>((int64_t)K3 * n_src);
   b->item_cnt = m.take<uint32_t>(b->max_items);
   b->item_off = m.take<uint32_t>(b->max_items);
   b->mm_partial = static_cast<int32_t*>(m.take_bytes(minmax_temp_bytes()));
@@ -288,6 +298,9 @@ int check_map_args(int64_t n_in, int64_t n_out, int K, int stride, int t, int mo
   if (stride < 1) return fail(SPCONV_EINVAL, "stride must be >= 1");
   if (n_in < 0 || n_out < 0) return fail(SPCONV_EINVAL, "negative size");
   if (n_in >= (int64_t)1 << 31 || n_out >= (int64_t)1 << 31) return fail(SPCONV_EUNSUPPORTED, "more than 2^31 rows");
+  // pair indices (and GEMM buffer rows) are int32: K^3 * max(n_in, n_out) bounds their count
+  if ((int64_t)K * K * K * std::max(n_in, n_out) >= (int64_t)1 << 31)
+    return fail(SPCONV_EUNSUPPORTED, "K^3 * rows must stay below 2^31");
   return SPCONV_OK;
 }
 
@@ -298,7 +311,6 @@ struct GmasPlan {
   int elem = 4, pelem = 4, part_dtype = 0;
   int t_gather = 0, t_scatter = 0;
   int grouping = SPCONV_GROUP_RAGGED;
-  int mt_stride = 0;
   int64_t rows_real = 0, rows_padded = 0;
   int n_launches = 0;
   std::vector<std::vector<GemmSeg>> launches;  // one entry per GEMM launch (group)
@@ -359,7 +371,6 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
     return fail(SPCONV_EINVAL, "t_scatter must be 4..64 (power of two), divide c_out and span whole 16-byte partial vectors");
   p->grouping = (opt && opt->grouping) ? opt->grouping - 1 : SPCONV_GROUP_RAGGED;
   if (p->grouping < 0 || p->grouping > 2) return fail(SPCONV_EINVAL, "grouping");
-  p->mt_stride = (m->K3 + 3) / 4 * 4;
 
   const int K3 = m->K3;
   p->rows_real = m->ptr[K3];
@@ -403,16 +414,12 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
 }
 
 struct FwdBufs {
-  int32_t* imt;
-  int32_t* omt;
   void* buf_in;
   void* buf_out;
 };
 
 size_t plan_forward_ws(void* base, const spconv_map* m, int c_in, int c_out, const GmasPlan& p, FwdBufs* b) {
   Bump a(base);
-  b->imt = a.take<int32_t>(m->n_in * p.mt_stride);
-  b->omt = a.take<int32_t>(m->n_out * p.mt_stride);
   b->buf_in = a.take_bytes((size_t)p.rows_real * c_in * p.elem);
   b->buf_out = a.take_bytes((size_t)p.rows_real * c_out * p.pelem);
   return align_up(a.off, 256);
@@ -537,6 +544,9 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   a.check_q = (mode == SPCONV_UP) ? 1 : 0;
   a.res = b.res;
   a.res_stride = nq_max;
+  a.ts = b.ts;
+  a.ts_stride = n_src;
+  a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
   {
     PhaseScope ph(PH_BACKWARD, s);
     hipError_t e = launch_backward(a, b.nb, b.bounds, b.chunks, b.cb, s);
@@ -546,6 +556,12 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     PhaseScope ph(PH_BALANCE, s);
     hipError_t e = scan_exclusive_u32(b.chunks, b.istart, (int64_t)K3 * b.nb, &b.cb->n_items, b.scan_tmp, s);
     if (e != hipSuccess) return bail(hip_fail(e, "balance"));
+  }
+  if (!a.sym) {
+    // sources without a partner at some offset: no query visits their entry
+    PhaseScope ph(PH_METADATA, s);
+    hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(b.ts), 0xFFFFFFFFu, (int64_t)K3 * n_src, s);
+    if (e != hipSuccess) return bail(hip_fail(e, "metadata fill"));
   }
   {
     PhaseScope ph(PH_FORWARD, s);
@@ -577,6 +593,27 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     }
     if (m->ptr[K3] != hc->n_pairs) return bail(fail(SPCONV_EHIP, "pair count mismatch"));
   }
+  // T_q is indexed by sorted query position, T_s by sorted source position.
+  // Inputs are the sources except for a direct UP map, whose inputs are the
+  // queries; presorted rows are their own sorted positions.
+  const uint32_t* src_perm = tu.presorted ? nullptr : b.sidx;
+  const uint32_t* q_perm = (mode == SPCONV_SUBM) ? src_perm
+                           : (mode == SPCONV_DOWN ? nullptr : (tu.presorted ? nullptr : b.qrow));
+  if (mode == SPCONV_UP) {
+    m->imt = b.res;
+    m->imt_stride = nq_max;
+    m->in_perm = q_perm;
+    m->omt = b.ts;
+    m->omt_stride = n_src;
+    m->out_perm = src_perm;
+  } else {
+    m->imt = b.ts;
+    m->imt_stride = n_src;
+    m->in_perm = src_perm;
+    m->omt = b.res;
+    m->omt_stride = nq_max;
+    m->out_perm = q_perm;
+  }
   *out_map = m;
   return SPCONV_OK;
 }
@@ -593,6 +630,9 @@ int spconv_map_transpose(const spconv_map* down, spconv_map** out_map) {
   m->n_out = down->n_in;
   m->pin = down->pout;
   m->pout = down->pin;
+  std::swap(m->imt, m->omt);
+  std::swap(m->imt_stride, m->omt_stride);
+  std::swap(m->in_perm, m->out_perm);
   m->out_coords = nullptr;  // the fine coordinates are the DOWN map's inputs (caller-owned)
   *out_map = m;
   return SPCONV_OK;
@@ -696,23 +736,14 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
   plan_forward_ws(d_workspace, m, c_in, c_out, p, &b);
   if (m->n_out == 0) return SPCONV_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int K3 = m->K3;
-  {
-    PhaseScope ph(PH_METADATA, s);
-    SPC_TRY(launch_mt_fill(b.imt, m->n_in, b.omt, m->n_out, p.mt_stride, s), "metadata fill");
-    if (p.rows_real > 0) {
-      OffsetTable t;
-      std::memset(&t, 0, sizeof(t));
-      t.K3 = K3;
-      for (int k = 0; k <= K3; ++k) t.pair_start[k] = m->ptr[k];
-      for (int k = 0; k < K3; ++k) t.row_base[k] = m->ptr[k];
-      SPC_TRY(launch_mt_pairs(m->pin, m->pout, p.rows_real, t, b.imt, b.omt, p.mt_stride, s), "metadata tables");
-    }
-  }
+  // a map without tables has no pairs: the scatter then writes zeros (plus the epilogue)
+  const int K3 = m->omt ? m->K3 : 0;
   if (p.rows_real > 0) {
     {
       PhaseScope ph(PH_GATHER, s);
-      SPC_TRY(launch_gather(d_x, m->n_in, c_in, p.elem, b.imt, p.mt_stride, K3, b.buf_in, p.t_gather, s), "gather");
+      SPC_TRY(launch_gather(d_x, m->n_in, c_in, p.elem, m->imt, m->imt_stride, m->in_perm, K3, b.buf_in, p.t_gather,
+                            s),
+              "gather");
     }
     {
       PhaseScope ph(PH_GEMM, s);
@@ -723,8 +754,8 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
   }
   {
     PhaseScope ph(PH_SCATTER, s);
-    SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, b.omt, p.mt_stride, K3, d_y, dtype, p.t_scatter,
-                           d_residual, relu, s),
+    SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, m->omt, m->omt_stride, m->out_perm, K3, d_y,
+                           dtype, p.t_scatter, d_residual, relu, s),
             "scatter");
   }
   return SPCONV_OK;

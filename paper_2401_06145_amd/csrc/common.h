@@ -78,7 +78,7 @@ enum ProfId : int {
   PH_METADATA, PH_GATHER, PH_GEMM, PH_SCATTER,
   // kernels
   KN_MINMAX = 16, KN_RADIX_HIST, KN_RADIX_SCATTER, KN_SCAN, KN_COPY, KN_DOWN_KEYS, KN_UNIQUE,
-  KN_BACKWARD, KN_FORWARD_COUNT, KN_FORWARD_WRITE, KN_FILL, KN_MT_PAIRS, KN_GATHER, KN_GEMM, KN_SCATTER,
+  KN_BACKWARD, KN_FORWARD_COUNT, KN_FORWARD_WRITE, KN_FILL, KN_UNUSED_27, KN_GATHER, KN_GEMM, KN_SCATTER,
   KN_PACK,
   PROF_IDS = 40
 };
@@ -133,8 +133,20 @@ struct SearchArgs {
   int Cq;                 // query block limit
   int swap_roles;         // UP: pairs are (query row, source row)
   int check_q;            // also check the query keys for repeats
-  int32_t* res;           // [K3][res_stride] per-query match (sorted source position or -1)
+  // Per-(offset, query) table T_q [K3][res_stride], indexed by sorted query
+  // position: the count pass stores the matching sorted source position or -1,
+  // the write pass replaces each match by its pair index (= GEMM buffer row).
+  int32_t* res;
   int64_t res_stride;
+  // Per-(offset, source) table T_s [K3][ts_stride], indexed by sorted source
+  // position: pair index or -1.  The write pass stores the matches; the -1
+  // entries come from a fill before it, or (sym != 0) from the write pass itself.
+  int32_t* ts;
+  int64_t ts_stride;
+  // Submanifold map with odd K: query q misses offset k exactly when source q
+  // has no partner at the mirrored offset K^3 - 1 - k, so the write pass marks
+  // that T_s entry instead of a separate fill.
+  int sym;
 };
 // Section 5.1.2, backward search fused with the per-(k, b) chunk counts of the
 // balancing step (and the duplicate-key check).
@@ -147,25 +159,18 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
                           int64_t max_items, int32_t* pin, int32_t* pout, ControlBlock* cb,
                           hipStream_t s);
 
-// gmas_kernels.hip
-struct OffsetTable {
-  int K3;
-  int64_t pair_start[kMaxOffsets + 1];  // prefix of |M_k| in the concatenated pair lists
-  int64_t row_base[kMaxOffsets];        // first buffer row of offset k
-};
-hipError_t launch_mt_fill(int32_t* imt, int64_t n_in, int32_t* omt, int64_t n_out, int stride,
-                          hipStream_t s);
-hipError_t launch_mt_pairs(const int32_t* pin, const int32_t* pout, int64_t m_total,
-                           const OffsetTable& t, int32_t* imt, int32_t* omt, int stride,
-                           hipStream_t s);
+// gmas_kernels.hip.  Metadata tables are offset-major over sorted positions:
+// entry [k * stride + p] is the buffer row of point p's pair at offset k, or -1;
+// perm[p] is the caller row of sorted position p (NULL: the identity).
 // Algorithm 1 gather with tile T channels per thread; elem = element bytes.
 hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const int32_t* imt,
-                         int mt_stride, int K3, void* buf_in, int tile, hipStream_t s);
-// Scatter: y[i] = sum_k buf_out[omt[i][k]] (float32 sum), tile T channels per thread.
-// Optional epilogue: y = relu?(sum + residual) (residual NULL: none).
+                         int64_t mt_stride, const uint32_t* perm, int K3, void* buf_in, int tile,
+                         hipStream_t s);
+// Scatter: y[perm[p]] = sum_k buf_out[omt[k][p]] (float32 sum, k ascending), tile T
+// channels per thread.  Optional epilogue: y = relu?(sum + residual) (residual NULL: none).
 hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out,
-                          const int32_t* omt, int mt_stride, int K3, void* y, int dtype, int tile,
-                          const void* residual, int relu, hipStream_t s);
+                          const int32_t* omt, int64_t mt_stride, const uint32_t* perm, int K3, void* y,
+                          int dtype, int tile, const void* residual, int relu, hipStream_t s);
 // out[i] = [a[i] | b[i]] for row-major a [n][ca], b [n][cb] (16-byte multiples).
 hipError_t launch_concat(const void* a, int ca, const void* b, int cb, void* out, int64_t n, int elem,
                          hipStream_t s);

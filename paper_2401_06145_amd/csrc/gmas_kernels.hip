@@ -1,62 +1,53 @@
 // Gather / Scatter of the GMaS step (Section 2.2, Step 2; Section 5.2.1).
 //
-// Metadata tables (Section 2.2): IMT[j][k] is the input-buffer row that input j
-// is copied to for offset k, OMT[i][k] the output-buffer row holding output i's
-// partial result for offset k; -1 where (j, k) / (i, k) has no pair.  For a
-// fixed point and offset there is at most one partner (q = p - delta), so each
-// table is a dense [rows][K^3] array, padded to a multiple of 4 entries per row.
+// Metadata tables (Section 2.2): the input table gives, for input point j and
+// offset k, the input-buffer row that j is copied to; the output table, for
+// output point i and offset k, the output-buffer row holding i's partial
+// result; -1 where (j, k) / (i, k) has no pair.  For a fixed point and offset
+// there is at most one partner (q = p - delta), so each table is dense.  The
+// Map step writes both while it ranks the pairs: they are stored offset-major
+// and indexed by the points' sorted positions, entry [k * stride + p], so the
+// map writes and the threads here read them with unit stride across points; a
+// permutation turns sorted positions back into caller rows.
 //
 // Gather follows Algorithm 1: one thread per (channel tile, input point) reads
-// its tile once and writes it to every buffer row listed in the point's IMT
-// row.  Scatter is its mirror image: one thread per (channel tile, output point)
-// sums the partials listed in the point's OMT row in float32 (offsets in
-// ascending order) and writes the tile once.  The tile size T (channels per
-// thread) is the paper's autotuned parameter.
+// its tile once and writes it to every buffer row listed for the point.
+// Scatter is its mirror image: one thread per (channel tile, output point)
+// sums the partials listed for the point in float32 (offsets in ascending
+// order) and writes the tile once.  The tile size T (channels per thread) is
+// the paper's autotuned parameter.
 #include "common.h"
 
 namespace spc {
 namespace {
 
 constexpr int kThreads = 256;
-
-__global__ __launch_bounds__(kThreads) void k_mt_pairs(const int32_t* pin, const int32_t* pout, int64_t m_total,
-                                                       OffsetTable t, int32_t* imt, int32_t* omt, int stride) {
-  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= m_total) return;
-  // offset k of pair m: last k with pair_start[k] <= m
-  int lo = 0, hi = t.K3 - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (t.pair_start[mid] <= m) lo = mid;
-    else hi = mid - 1;
-  }
-  const int k = lo;
-  const int32_t row = (int32_t)(t.row_base[k] + (m - t.pair_start[k]));
-  imt[(int64_t)pin[m] * stride + k] = row;
-  omt[(int64_t)pout[m] * stride + k] = row;
-}
+// metadata entries loaded ahead per thread (independent loads in flight)
+constexpr int kMtBatch = 8;
 
 // V = 16-byte vectors per thread (tile T = V * 16 / element bytes channels).
 template <int V>
 __global__ __launch_bounds__(kThreads) void k_gather(const uint4* __restrict__ x, int64_t n_in, int row_vec,
-                                                     const int32_t* __restrict__ imt, int stride, int K3,
+                                                     const int32_t* __restrict__ imt, int64_t stride,
+                                                     const uint32_t* __restrict__ perm, int K3,
                                                      uint4* __restrict__ buf) {
   const int tiles = row_vec / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t j = gid / tiles;
-  const int t = (int)(gid - j * tiles);
-  if (j >= n_in) return;
+  const int64_t p = gid / tiles;
+  const int t = (int)(gid - p * tiles);
+  if (p >= n_in) return;
+  const int64_t j = perm ? (int64_t)perm[p] : p;
   uint4 v[V];
   const uint4* src = x + j * row_vec + (int64_t)t * V;
 #pragma unroll
   for (int u = 0; u < V; ++u) v[u] = src[u];
-  const int4* mt = reinterpret_cast<const int4*>(imt + j * stride);
-  for (int k4 = 0; k4 < stride / 4; ++k4) {
-    const int4 r4 = mt[k4];
-    const int32_t r[4] = {r4.x, r4.y, r4.z, r4.w};
+  for (int k0 = 0; k0 < K3; k0 += kMtBatch) {
+    int32_t r[kMtBatch];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (r[e] >= 0 && k4 * 4 + e < K3) {
+    for (int e = 0; e < kMtBatch; ++e) r[e] = (k0 + e < K3) ? imt[(int64_t)(k0 + e) * stride + p] : -1;
+#pragma unroll
+    for (int e = 0; e < kMtBatch; ++e) {
+      if (r[e] >= 0) {
         uint4* dst = buf + (int64_t)r[e] * row_vec + (int64_t)t * V;
 #pragma unroll
         for (int u = 0; u < V; ++u) dst[u] = v[u];
@@ -88,32 +79,34 @@ __device__ __forceinline__ __hip_bfloat16 from_f32<__hip_bfloat16>(float v) { re
 // may alias y (each thread reads its tile before writing it).
 template <int TILE, typename TP, typename TO>
 __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf, int64_t n_out, int c_out,
-                                                      const int32_t* __restrict__ omt, int stride, int K3,
-                                                      TO* y, const TO* residual, int relu) {
+                                                      const int32_t* __restrict__ omt, int64_t stride,
+                                                      const uint32_t* __restrict__ perm, int K3, TO* y,
+                                                      const TO* residual, int relu) {
   static_assert((TILE * sizeof(TP)) % 16 == 0, "partial tile must be whole 16-byte vectors");
   constexpr int VP = TILE * sizeof(TP) / 16;
   const int tiles = c_out / TILE;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t i = gid / tiles;
-  const int t = (int)(gid - i * tiles);
-  if (i >= n_out) return;
+  const int64_t p = gid / tiles;
+  const int t = (int)(gid - p * tiles);
+  if (p >= n_out) return;
+  const int64_t i = perm ? (int64_t)perm[p] : p;
   float acc[TILE];
 #pragma unroll
   for (int c = 0; c < TILE; ++c) acc[c] = 0.f;
-  const int4* mt = reinterpret_cast<const int4*>(omt + i * stride);
-  for (int k4 = 0; k4 < stride / 4; ++k4) {
-    const int4 r4 = mt[k4];
-    const int32_t r[4] = {r4.x, r4.y, r4.z, r4.w};
+  for (int k0 = 0; k0 < K3; k0 += kMtBatch) {
+    int32_t r[kMtBatch];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (r[e] >= 0 && k4 * 4 + e < K3) {
+    for (int e = 0; e < kMtBatch; ++e) r[e] = (k0 + e < K3) ? omt[(int64_t)(k0 + e) * stride + p] : -1;
+#pragma unroll
+    for (int e = 0; e < kMtBatch; ++e) {
+      if (r[e] >= 0) {
         const uint4* src = reinterpret_cast<const uint4*>(buf + (int64_t)r[e] * c_out + (int64_t)t * TILE);
 #pragma unroll
         for (int u = 0; u < VP; ++u) {
           const uint4 v = src[u];
-          const TP* p = reinterpret_cast<const TP*>(&v);
+          const TP* pv = reinterpret_cast<const TP*>(&v);
 #pragma unroll
-          for (int c = 0; c < 16 / (int)sizeof(TP); ++c) acc[u * (16 / sizeof(TP)) + c] += to_f32<TP>(p[c]);
+          for (int c = 0; c < 16 / (int)sizeof(TP); ++c) acc[u * (16 / sizeof(TP)) + c] += to_f32<TP>(pv[c]);
         }
       }
     }
@@ -147,8 +140,8 @@ __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf
 unsigned blocks_for(int64_t threads) { return (unsigned)((threads + kThreads - 1) / kThreads); }
 
 template <typename TP, typename TO>
-hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* omt, int stride, int K3, void* y,
-                     int tile, const void* residual, int relu, hipStream_t s) {
+hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* omt, int64_t stride,
+                     const uint32_t* perm, int K3, void* y, int tile, const void* residual, int relu, hipStream_t s) {
   ProfScope ps(KN_SCATTER, s);
   const int64_t threads = n_out * (c_out / tile);
   const dim3 g(blocks_for(threads)), b(kThreads);
@@ -159,7 +152,7 @@ hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* o
 #define SPC_SC(T)                                                                                    \
   case T:                                                                                            \
     if constexpr ((T * sizeof(TP)) % 16 == 0) {                                                      \
-      hipLaunchKernelGGL((k_scatter<T, TP, TO>), g, b, 0, s, p, n_out, c_out, omt, stride, K3, o, r, relu); \
+      hipLaunchKernelGGL((k_scatter<T, TP, TO>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu); \
       return hipGetLastError();                                                                      \
     }                                                                                                \
     return hipErrorInvalidValue;
@@ -176,24 +169,9 @@ hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* o
 
 }  // namespace
 
-hipError_t launch_mt_fill(int32_t* imt, int64_t n_in, int32_t* omt, int64_t n_out, int stride, hipStream_t s) {
-  hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(imt), 0xFFFFFFFFu, n_in * stride, s);
-  if (e != hipSuccess) return e;
-  return launch_fill_u32(reinterpret_cast<uint32_t*>(omt), 0xFFFFFFFFu, n_out * stride, s);
-}
-
-hipError_t launch_mt_pairs(const int32_t* pin, const int32_t* pout, int64_t m_total, const OffsetTable& t,
-                           int32_t* imt, int32_t* omt, int stride, hipStream_t s) {
-  if (m_total <= 0) return hipSuccess;
-  ProfScope ps(KN_MT_PAIRS, s);
-  hipLaunchKernelGGL(k_mt_pairs, dim3(blocks_for(m_total)), dim3(kThreads), 0, s, pin, pout, m_total, t, imt, omt,
-                     stride);
-  return hipGetLastError();
-}
-
-hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const int32_t* imt, int mt_stride, int K3,
-                         void* buf_in, int tile, hipStream_t s) {
-  if (n_in <= 0) return hipSuccess;
+hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const int32_t* imt, int64_t mt_stride,
+                         const uint32_t* perm, int K3, void* buf_in, int tile, hipStream_t s) {
+  if (n_in <= 0 || K3 <= 0) return hipSuccess;
   const int row_vec = c_in * elem / 16;
   const int v = tile * elem / 16;
   if (v <= 0 || row_vec % v != 0) return hipErrorInvalidValue;
@@ -203,34 +181,38 @@ hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const 
   const uint4* xp = static_cast<const uint4*>(x);
   uint4* bp = static_cast<uint4*>(buf_in);
   switch (v) {
-    case 1: hipLaunchKernelGGL(k_gather<1>, g, b, 0, s, xp, n_in, row_vec, imt, mt_stride, K3, bp); break;
-    case 2: hipLaunchKernelGGL(k_gather<2>, g, b, 0, s, xp, n_in, row_vec, imt, mt_stride, K3, bp); break;
-    case 4: hipLaunchKernelGGL(k_gather<4>, g, b, 0, s, xp, n_in, row_vec, imt, mt_stride, K3, bp); break;
-    case 8: hipLaunchKernelGGL(k_gather<8>, g, b, 0, s, xp, n_in, row_vec, imt, mt_stride, K3, bp); break;
-    case 16: hipLaunchKernelGGL(k_gather<16>, g, b, 0, s, xp, n_in, row_vec, imt, mt_stride, K3, bp); break;
+#define SPC_G(V)                                                                                         \
+  case V:                                                                                                \
+    hipLaunchKernelGGL(k_gather<V>, g, b, 0, s, xp, n_in, row_vec, imt, mt_stride, perm, K3, bp); \
+    break;
+    SPC_G(1)
+    SPC_G(2)
+    SPC_G(4)
+    SPC_G(8)
+    SPC_G(16)
+#undef SPC_G
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out, const int32_t* omt,
-                          int mt_stride, int K3, void* y, int dtype, int tile, const void* residual, int relu,
-                          hipStream_t s) {
+                          int64_t mt_stride, const uint32_t* perm, int K3, void* y, int dtype, int tile,
+                          const void* residual, int relu, hipStream_t s) {
   if (n_out <= 0) return hipSuccess;
   if (tile <= 0 || c_out % tile != 0) return hipErrorInvalidValue;
   // part_dtype / dtype: 0 = f32, 1 = f16, 2 = bf16
+#define SPC_S(TP, TO) scatter_t<TP, TO>(buf_out, n_out, c_out, omt, mt_stride, perm, K3, y, tile, residual, relu, s)
   if (part_dtype == 0) {
-    if (dtype == 0) return scatter_t<float, float>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
-    if (dtype == 1)
-      return scatter_t<float, __half>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
-    if (dtype == 2)
-      return scatter_t<float, __hip_bfloat16>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
+    if (dtype == 0) return SPC_S(float, float);
+    if (dtype == 1) return SPC_S(float, __half);
+    if (dtype == 2) return SPC_S(float, __hip_bfloat16);
   } else if (part_dtype == 1 && dtype == 1) {
-    return scatter_t<__half, __half>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual, relu, s);
+    return SPC_S(__half, __half);
   } else if (part_dtype == 2 && dtype == 2) {
-    return scatter_t<__hip_bfloat16, __hip_bfloat16>(buf_out, n_out, c_out, omt, mt_stride, K3, y, tile, residual,
-                                                     relu, s);
+    return SPC_S(__hip_bfloat16, __hip_bfloat16);
   }
+#undef SPC_S
   return hipErrorInvalidValue;
 }
 

@@ -468,8 +468,10 @@ __device__ __forceinline__ int64_t wave_upper_bound(const T* a, int64_t n, V thr
 // with key(q) + dk in (pivot_{b-1}, pivot_b], pivot_b being the block's last
 // key.  One wave per (k, b) finds bounds[k][b] = #{q : key(q) + dk <= pivot_b}
 // and the same for pivot_{b-1}, and writes the number of <= Cq chunks the
-// query block splits into.  The k = 0 waves also check the sorted keys for
-// repeats (a point cloud is a set).
+// query block splits into.  The last block also takes the queries beyond its
+// pivot (they all miss), so that every (offset, query) pair is searched once and
+// the per-query tables come out complete.  The k = 0 waves also check the
+// sorted keys for repeats (a point cloud is a set).
 // ----------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb, uint32_t* bounds, uint32_t* chunks,
                                                        ControlBlock* cb) {
@@ -482,7 +484,8 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
   const int64_t dk = a.dk[k];
   // key(q) + dk <= pivot  <=>  key(q) <= pivot - dk, evaluated in signed 64 bits
   const int64_t last = min((b + 1) * (int64_t)a.B, a.n_src) - 1;
-  const int64_t hi = wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, (int64_t)a.skeys[last] - dk);
+  const int64_t hi =
+      (b == nb - 1) ? nq : wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, (int64_t)a.skeys[last] - dk);
   const int64_t lo = (b == 0) ? 0 : wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, (int64_t)a.skeys[b * a.B - 1] - dk);
   if (lane == 0) {
     bounds[wid] = (uint32_t)hi;
@@ -515,9 +518,12 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
 // ----------------------------------------------------------------------------
 // Forward binary search (Section 5.1.2).  One workgroup per load-balanced
 // query block (work item): the source block is staged in LDS and each lane
-// binary-searches its queries there.  COUNT pass: matches per work item.  WRITE
-// pass: the same search, matches ranked with wave ballots and written at the
-// scanned offset, so every offset's pairs come out in sorted-query order.
+// binary-searches its queries there, recording the match (or -1) in T_q.
+// COUNT pass: matches per work item.  WRITE pass: matches ranked with wave
+// ballots; pair e of the item goes to index o = item_off + e, so every
+// offset's pairs come out in sorted-query order, and o, the pair's GEMM buffer
+// row, is also stored in both metadata tables (T_q in place of the source
+// position, T_s at the source position).
 // ----------------------------------------------------------------------------
 struct ItemRange {
   int k;
@@ -590,14 +596,17 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
   int32_t* res = a.res + (int64_t)it.k * a.res_stride;
 
   const uint64_t dk = (uint64_t)a.dk[it.k];
-  int32_t r_in[ROUNDS], r_out[ROUNDS];
+  int32_t r_in[ROUNDS], r_out[ROUNDS], r_sp[ROUNDS];
   uint64_t bal[ROUNDS];
+  // mirrored offset's T_s row, for the misses of a symmetric map
+  int32_t* ts_mirror = a.ts + (int64_t)(a.K3 - 1 - it.k) * a.ts_stride;
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
     const int64_t qp = it.q0 + (int64_t)r * kThreads + tid;
     bool hit = false;
     r_in[r] = 0;
     r_out[r] = 0;
+    r_sp[r] = -1;
     if (qp < it.q1) {
       if (!WRITE) {
         const uint64_t key = a.qkeys[qp] + dk;
@@ -608,10 +617,13 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
         const int32_t sp = res[qp];
         if (sp >= 0) {
           hit = true;
+          r_sp[r] = sp;
           const int32_t src = (int32_t)a.sidx[sp];
           const int32_t qry = (int32_t)a.qrow[qp];
           r_in[r] = a.swap_roles ? qry : src;
           r_out[r] = a.swap_roles ? src : qry;
+        } else if (a.sym) {
+          ts_mirror[qp] = -1;
         }
       }
     }
@@ -634,12 +646,16 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
     return;
   }
   const uint64_t base = item_off[w];
+  int32_t* ts = a.ts + (int64_t)it.k * a.ts_stride;
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
     if ((bal[r] >> lane) & 1ull) {
       const uint64_t o = base + before[r] + (uint64_t)popc64(bal[r] & lanemask_lt());
+      const int64_t qp = it.q0 + (int64_t)r * kThreads + tid;
       pin[o] = r_in[r];
       pout[o] = r_out[r];
+      res[qp] = (int32_t)o;
+      ts[r_sp[r]] = (int32_t)o;
     }
   }
 }

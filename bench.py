@@ -69,18 +69,21 @@ def kernel_models(n, n_out, pairs, L, k3, passes):
     e = 4 if L.dtype == "f32" else 2
     ep = e  # GEMM partials are stored in the layer dtype
     P = max(passes, 1)
-    # scans per step: one digit-offset scan per radix pass (256 x tiles of 2048 keys),
-    # the chunk-count scan (K^3 x source blocks of 1024) and the match-count scan
+    # scans per step: the chunk-count scan of the balance step (K^3 x source blocks of
+    # 1024) and the match-count scan (one entry per work item), plus one digit-offset scan
+    # per radix pass when the sort has between 257 and 1023 tiles of 2048 keys
     nb = -(-n // 1024)
+    ntiles = -(-n // 2048)
     max_items = k3 * (nb + -(-n_out // 1024)) + 1
-    scan_lens = [256 * -(-n // 2048)] * P + [k3 * nb, max_items]
+    scan_lens = ([256 * ntiles] * P if 256 < ntiles < 1024 else []) + [k3 * nb, max_items]
     m = {
         "k_scan": ("hbm", 8.0 * sum(scan_lens) / len(scan_lens)),
         # radix passes: the first reads int32 coordinates (16 B/row), later ones key + row (12 B)
         "k_radix_scatter": ("hbm", (16 * n + 12 * n + (P - 1) * 24 * n) / P),
         "k_radix_hist": ("hbm", (16 * n + (P - 1) * 8 * n) / P),
         "k_minmax": ("hbm", 16 * n),
-        # forward search: query keys and source keys once, one result word per (offset, query)
+        # forward search, count pass: query keys and source keys once, one result word per
+        # (offset, query)
         "k_forward_count": ("hbm", 8 * n_out + 8 * n + 4 * k3 * n_out),
         # write pass: reads the results and the rows of the matches; writes the pair lists,
         # the query-side table's matches (in place) and the whole source-side table

@@ -582,7 +582,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     if (e != hipSuccess) return bail(hip_fail(e, "count read-back"));
     if (hc->err & kErrDup) return bail(fail(SPCONV_EDUP, "duplicate coordinates"));
     if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "work-item overflow in the balance step"));
-    if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "radix-sort look-back exceeded its wait bound"));
+    if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "a look-back exceeded its wait bound"));
     if (hc->err & kErrUnsorted)
       return bail(fail(SPCONV_EINVAL, "rows declared presorted are not in ascending (b, x, y, z) order"));
     if (hc->n_items > (uint32_t)b.max_items) return bail(fail(SPCONV_EHIP, "work items exceed the launch bound"));

@@ -328,11 +328,16 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
   }
 }
 
-// Small inputs (few tiles): per-tile digit histograms -> exclusive scan
-// (digit-major) -> stable scatter, three launches per pass.  With few tiles
-// every workgroup of a one-kernel pass would start at once and find no
-// inclusive prefix to stop its look-back, so this variant is faster there.
-template <bool FROM_COORDS>
+// Small inputs (few tiles): per-tile digit histograms, then a stable scatter.
+// With few tiles every workgroup of a one-kernel pass would start at once and
+// find no inclusive prefix to stop its look-back, so this variant is faster
+// there.  With up to kFusedScanTiles tiles the histograms are stored
+// tile-major and every scatter workgroup adds up the counts it needs itself
+// (two launches per pass); with more, a device scan over the digit-major
+// histograms gives the offsets (three launches).
+constexpr int64_t kFusedScanTiles = 256;
+
+template <bool FROM_COORDS, bool TILE_MAJOR>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, KeyLayout L,
                                                          int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
   __shared__ uint32_t h[256];
@@ -349,32 +354,100 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
     }
   }
   __syncthreads();
-  hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+  if (TILE_MAJOR)
+    hist[(int64_t)blockIdx.x * 256 + threadIdx.x] = h[threadIdx.x];
+  else
+    hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
-template <bool FROM_COORDS>
+// FUSED: `offs` holds tile-major histograms; the first position of digit d in
+// this tile is (keys of smaller digits) + (keys of digit d in earlier tiles).
+// Otherwise `offs` is the scanned digit-major histogram.
+template <bool FROM_COORDS, bool FUSED>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t* kin, const uint32_t* vin,
                                                             const int4* coords, KeyLayout L, uint64_t* kout,
                                                             uint32_t* vout, int64_t n, int shift,
                                                             const uint32_t* offs, int64_t ntiles) {
   __shared__ uint32_t run[256];
   __shared__ uint32_t wcnt[kWavesPerBlock][256];
+  __shared__ uint32_t s_wave[kWavesPerBlock];
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
-  run[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
+  const int64_t base = (int64_t)blockIdx.x * kRsTile;
+  // the tile's keys are loaded first, so that their latency overlaps the offset sums
+  uint64_t key[kRsItems];
+  uint32_t val[kRsItems];
+#pragma unroll
+  for (int r = 0; r < kRsItems; ++r) {
+    const int64_t i = base + r * kThreads + tid;
+    key[r] = 0;
+    val[r] = 0;
+    if (i < n) {
+      key[r] = load_key<FROM_COORDS>(kin, coords, L, i);
+      val[r] = FROM_COORDS ? (uint32_t)i : vin[i];
+    }
+  }
+  if (FUSED) {
+    // wave v sums tiles v, v + 4, ...; lane l covers digits 4l..4l+3 with 16-byte loads,
+    // so all of a wave's loads are independent and in flight together
+    const int lane = tid & (kWave - 1);
+    const int64_t tile = blockIdx.x;
+    const uint4* h4 = reinterpret_cast<const uint4*>(offs);
+    uint4 bef = make_uint4(0, 0, 0, 0), tot4 = make_uint4(0, 0, 0, 0);
+    for (int64_t t0 = wave; t0 < ntiles; t0 += 16 * kWavesPerBlock) {
+      uint4 v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int64_t t = t0 + (int64_t)u * kWavesPerBlock;
+        v[u] = (t < ntiles) ? h4[t * 64 + lane] : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int64_t t = t0 + (int64_t)u * kWavesPerBlock;
+        tot4.x += v[u].x; tot4.y += v[u].y; tot4.z += v[u].z; tot4.w += v[u].w;
+        if (t < tile) {
+          bef.x += v[u].x; bef.y += v[u].y; bef.z += v[u].z; bef.w += v[u].w;
+        }
+      }
+    }
+    // per-wave partial sums -> per-digit sums (thread d)
+    uint32_t* s_part = &wcnt[0][0];  // reused as [wave][digit] partials; cleared below
+    reinterpret_cast<uint4*>(s_part)[wave * 64 + lane] = tot4;
+    __syncthreads();
+    uint32_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) tot += s_part[w * 256 + tid];
+    __syncthreads();
+    reinterpret_cast<uint4*>(s_part)[wave * 64 + lane] = bef;
+    __syncthreads();
+    uint32_t before = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) before += s_part[w * 256 + tid];
+    // exclusive scan of the digit totals across the block
+    uint32_t x = tot;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const uint32_t y = __shfl_up(x, d, kWave);
+      if (lane >= d) x += y;
+    }
+    if (lane == kWave - 1) s_wave[wave] = x;
+    __syncthreads();
+    uint32_t dbase = x - tot;
+    for (int w = 0; w < wave; ++w) dbase += s_wave[w];
+    run[tid] = dbase + before;
+  } else {
+    run[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
+  }
 #pragma unroll
   for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][tid] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kRsTile;
+#pragma unroll
   for (int r = 0; r < kRsItems; ++r) {
     const int64_t i = base + r * kThreads + tid;
     const bool valid = i < n;
-    uint64_t key = 0;
-    uint32_t val = 0, d = 0, rank = 0;
+    uint32_t d = 0, rank = 0;
     if (valid) {
-      key = load_key<FROM_COORDS>(kin, coords, L, i);
-      val = FROM_COORDS ? (uint32_t)i : vin[i];
-      d = (uint32_t)(key >> shift) & 255u;
+      d = (uint32_t)(key[r] >> shift) & 255u;
       const uint64_t peers = match_digit(d);
       rank = (uint32_t)popc64(peers & lanemask_lt());
       if (rank == 0) wcnt[wave][d] = (uint32_t)popc64(peers);
@@ -383,8 +456,8 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
     if (valid) {
       uint32_t pos = run[d] + rank;
       for (int w = 0; w < wave; ++w) pos += wcnt[w][d];
-      kout[pos] = key;
-      vout[pos] = val;
+      kout[pos] = key[r];
+      vout[pos] = val[r];
     }
     __syncthreads();
     uint32_t add = 0;
@@ -748,6 +821,8 @@ hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, 
     if (e == hipSuccess) e = hipMemcpyAsync(vals_alt, vals, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return e;
   }
+  const bool fused = ntiles <= kFusedScanTiles;
+  const unsigned g = (unsigned)ntiles;
   for (int p = 0; p < passes; ++p) {
     const int shift = 8 * p;
     const bool first = (p == 0) && coords;
@@ -755,25 +830,33 @@ hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, 
     hipError_t e;
     {
       ProfScope ps(KN_RADIX_HIST, s);
-      if (first)
-        hipLaunchKernelGGL(k_radix_tile_hist<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, c4, L, n,
-                           shift, hist, ntiles);
-      else
-        hipLaunchKernelGGL(k_radix_tile_hist<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], nullptr,
-                           L, n, shift, hist, ntiles);
+#define SPC_H(FC, TM)                                                                                           \
+  hipLaunchKernelGGL((k_radix_tile_hist<FC, TM>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],      \
+                     FC ? c4 : nullptr, L, n, shift, hist, ntiles)
+      if (first) {
+        if (fused) SPC_H(true, true); else SPC_H(true, false);
+      } else {
+        if (fused) SPC_H(false, true); else SPC_H(false, false);
+      }
+#undef SPC_H
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
-    e = scan_exclusive_u32(hist, hist, 256 * ntiles, nullptr, scan_tmp, s);
-    if (e != hipSuccess) return e;
+    if (!fused) {
+      e = scan_exclusive_u32(hist, hist, 256 * ntiles, nullptr, scan_tmp, s);
+      if (e != hipSuccess) return e;
+    }
     {
       ProfScope ps(KN_RADIX_SCATTER, s);
-      if (first)
-        hipLaunchKernelGGL(k_radix_tile_scatter<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr,
-                           c4, L, kb[dst], vb[dst], n, shift, hist, ntiles);
-      else
-        hipLaunchKernelGGL(k_radix_tile_scatter<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src],
-                           vb[src], nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles);
+#define SPC_S(FC, FU)                                                                                           \
+  hipLaunchKernelGGL((k_radix_tile_scatter<FC, FU>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],   \
+                     FC ? nullptr : vb[src], FC ? c4 : nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles)
+      if (first) {
+        if (fused) SPC_S(true, true); else SPC_S(true, false);
+      } else {
+        if (fused) SPC_S(false, true); else SPC_S(false, false);
+      }
+#undef SPC_S
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

@@ -243,6 +243,22 @@ def test_large_cloud_one_kernel_sort_passes():
     assert np.array_equal(qd.out_coords().cpu().numpy(), q)
 
 
+def test_mid_cloud_scanned_sort_offsets():
+    """1M voxels: 489 radix tiles, between the per-workgroup offset sums and the
+    one-kernel passes, so each pass scans the digit-major histograms on the device.
+    Also about 50k forward-search work items; features checked on sampled rows."""
+    say("mid-size uniform cloud, 1M voxels")
+    c = scenes.uniform_cells(1_000_000, 400, 4343)
+    x = scenes.features(len(c), 16, "f16", 4344)
+    w = scenes.weights(3, 16, 16, "f16", 4345)
+    km, y = _conv_gpu(c, x, w, 3, dtype="f16")
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    assert_map_equal(km, okm)
+    rows = np.sort(np.random.default_rng(4346).choice(len(c), 4000, replace=False))
+    ref = oracle.features(scenes.to_f64(x, "f16"), scenes.to_f64(w, "f16"), okm, rows=rows)
+    assert rel_err(to_f64(y)[rows], ref) <= TOL["f16"]
+
+
 def test_deterministic_pairs():
     say("deterministic pair order")
     c = scenes.workload(1).coords

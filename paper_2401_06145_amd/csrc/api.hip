@@ -308,7 +308,7 @@ int check_map_args(int64_t n_in, int64_t n_out, int K, int stride, int t, int mo
 // GMaS plan: GEMM grouping (Section 5.2.2) and tiles (Algorithm 1)
 // ---------------------------------------------------------------------------
 struct GmasPlan {
-  int elem = 4, pelem = 4, part_dtype = 0;
+  int dtype = 0, elem = 4, pelem = 4, part_dtype = 0;
   int t_gather = 0, t_scatter = 0;
   int grouping = SPCONV_GROUP_RAGGED;
   int64_t rows_real = 0, rows_padded = 0;
@@ -346,6 +346,7 @@ std::vector<int> dp_groups(const std::vector<int>& order, const std::vector<int6
 int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_options* opt, GmasPlan* p) {
   if (!m) return fail(SPCONV_EINVAL, "map is NULL");
   if (dtype != SPCONV_F32 && dtype != SPCONV_F16 && dtype != SPCONV_BF16) return fail(SPCONV_EUNSUPPORTED, "dtype");
+  p->dtype = dtype;
   p->elem = elem_bytes(dtype);
   if (c_in < 1 || c_out < 1 || c_in > 1024 || c_out > 1024) return fail(SPCONV_EUNSUPPORTED, "channels must be in [1, 1024]");
   if ((c_in * p->elem) % 16 != 0) return fail(SPCONV_EUNSUPPORTED, "c_in rows must be whole 16-byte vectors");
@@ -414,12 +415,14 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
 }
 
 struct FwdBufs {
+  void* wt;  // transposed weights for the full-width GEMM, or NULL
   void* buf_in;
   void* buf_out;
 };
 
 size_t plan_forward_ws(void* base, const spconv_map* m, int c_in, int c_out, const GmasPlan& p, FwdBufs* b) {
   Bump a(base);
+  b->wt = gemm_wide(c_in, c_out, p.dtype, p.part_dtype) ? a.take_bytes((size_t)m->K3 * c_in * c_out * p.elem) : nullptr;
   b->buf_in = a.take_bytes((size_t)p.rows_real * c_in * p.elem);
   b->buf_out = a.take_bytes((size_t)p.rows_real * c_out * p.pelem);
   return align_up(a.off, 256);
@@ -747,8 +750,10 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
     }
     {
       PhaseScope ph(PH_GEMM, s);
+      if (b.wt) SPC_TRY(launch_transpose_w(d_w, b.wt, m->K3, c_in, c_out, s), "weight transpose");
       for (const auto& segs : p.launches)
-        SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), b.buf_in, d_w, b.buf_out, c_in, c_out, dtype, p.part_dtype, s),
+        SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), b.buf_in, d_w, b.wt, b.buf_out, c_in, c_out, dtype,
+                            p.part_dtype, s),
                 "grouped GEMM");
     }
   }

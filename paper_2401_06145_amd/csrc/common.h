@@ -184,8 +184,13 @@ struct GemmSeg {
   int64_t rows;
   int64_t height;
 };
+// Whether the full-width kernel applies (it needs the transposed weights).
+bool gemm_wide(int c_in, int c_out, int dtype, int part_dtype);
+// wt[k][n][c] = w[k][c][n] for 16-bit weights.
+hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_out, hipStream_t s);
 // Launches the segments (any number; split into launches of at most 64 segments).
-hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, void* buf_out,
-                       int c_in, int c_out, int dtype, int part_dtype, hipStream_t s);
+// wt: transposed weights (launch_transpose_w) or NULL for the general kernel.
+hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, const void* wt,
+                       void* buf_out, int c_in, int c_out, int dtype, int part_dtype, hipStream_t s);
 
 }  // namespace spc

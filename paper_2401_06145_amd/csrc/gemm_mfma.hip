@@ -15,6 +15,13 @@
 //   result:    row 4*(l/16)+i, column l%16, i = 0..3.
 // Group padding rows (segment height > rows) are fed as zeros: they cost MFMA
 // cycles, like the zero-padded batched GEMMs of the paper, but no memory traffic.
+//
+// Two kernels.  k_gemm_wide (f16 / bf16, c_in <= 256) gives a workgroup the full
+// output width whenever W_k^T fits the 160 KiB of LDS, so every buf_in row is
+// read from HBM once; it stages W_k^T from a transposed copy of the weights
+// with 16-byte copies, and each wave loads the next 16-row block of buf_in while
+// it multiplies the current one.  k_gemm is the general fallback (any c_in,
+// float32) with a narrower column slice per workgroup.
 #include "common.h"
 
 namespace spc {
@@ -145,6 +152,156 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmLaunchArgs g, const T* __
   }
 }
 
+constexpr int kWideThreads = 512;
+constexpr int kWideWaves = kWideThreads / kWave;
+constexpr size_t kLdsMax = 160 * 1024;
+
+// NT = 16-column tiles per workgroup; ksteps = padded c_in / 32 <= kMaxKsteps.
+// wt is W^T, [K^3][c_out][c_in] row-major.
+constexpr int kMaxKsteps = 8;
+template <typename T, typename TO, int NT>
+__global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, const T* __restrict__ A,
+                                                            const T* __restrict__ wt, TO* __restrict__ C, int c_in,
+                                                            int c_out, int ksteps, int ldk, int rows_per_tile) {
+  using M = Mfma<T>;
+  static_assert(M::KS == 32, "16-bit operands only");
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* lw = reinterpret_cast<T*>(smem);  // [BN][ldk], W_k^T slice
+  constexpr int BN = 16 * NT;
+  const int KP = 32 * ksteps;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+
+  int s = 0;
+  while (s + 1 < g.n_seg && g.tile_start[s + 1] <= (int)blockIdx.x) ++s;
+  const int k = g.k[s];
+  const int64_t row0 = g.row0[s];
+  const int rows = g.rows[s];
+  const int height = g.height[s];
+  const int tile = (int)blockIdx.x - g.tile_start[s];
+  const int n0 = blockIdx.y * BN;
+
+  // W_k^T rows n0 .. n0 + BN, 8 elements (16 bytes) per copy; columns past c_in are zero
+  const T* wk = wt + ((int64_t)k * c_out + n0) * c_in;
+  const int CH = KP / 8;  // 16-byte chunks per LDS row
+  for (int idx = tid; idx < BN * CH; idx += kWideThreads) {
+    const int n = idx / CH;
+    const int c = (idx - n * CH) * 8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (c < c_in) v = *reinterpret_cast<const uint4*>(wk + (int64_t)n * c_in + c);
+    *reinterpret_cast<uint4*>(lw + n * ldk + c) = v;
+  }
+  __syncthreads();
+
+  const int r_begin = tile * rows_per_tile;
+  const int r_end = min(r_begin + rows_per_tile, height);
+  const int sub = lane >> 4;
+  const int col = lane & 15;
+  typename M::frag cur[kMaxKsteps], nxt[kMaxKsteps];
+  auto load_block = [&](int m0, typename M::frag* f) {
+    const int row = m0 + col;
+    const bool real = row < rows;
+    const T* arow = A + (row0 + row) * (int64_t)c_in;
+#pragma unroll
+    for (int q = 0; q < kMaxKsteps; ++q) {
+      const int kk = 32 * q + 8 * sub;
+      f[q] = (q < ksteps && real && kk < c_in) ? M::load(arow + kk) : M::zero();
+    }
+  };
+  int m0 = r_begin + wave * 16;
+  if (m0 < r_end) load_block(m0, cur);
+  for (; m0 < r_end; m0 += 16 * kWideWaves) {
+    const int m1 = m0 + 16 * kWideWaves;
+    if (m1 < r_end) load_block(m1, nxt);
+    f32x4 acc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < kMaxKsteps; ++q) {
+      if (q >= ksteps) break;
+      const int kk = 32 * q + 8 * sub;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const typename M::frag a = M::load(lw + (16 * t + col) * ldk + kk);
+        acc[t] = M::mma(a, cur[q], acc[t]);
+      }
+    }
+    const int row = m0 + col;
+    if (row < rows) {
+      TO* crow = C + (row0 + row) * (int64_t)c_out + n0 + 4 * sub;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) store4(crow + 16 * t, acc[t]);
+    }
+#pragma unroll
+    for (int q = 0; q < kMaxKsteps; ++q) cur[q] = nxt[q];
+  }
+}
+
+// Column tiles per workgroup for the wide kernel: the widest instantiated divisor
+// of c_out / 16 whose W^T slice fits the LDS; 0 if the wide kernel does not apply.
+int wide_nt(int c_in, int c_out, int elem) {
+  if (elem != 2 || c_in > 32 * kMaxKsteps || c_in % 8 != 0 || c_out % 16 != 0) return 0;
+  const int kp = (c_in + 31) / 32 * 32;
+  const int ldk = kp + 8;
+  const int nt_all = c_out / 16;
+  for (int nt : {16, 12, 8, 6, 4, 3, 2, 1})
+    if (nt_all % nt == 0 && (size_t)16 * nt * ldk * 2 <= kLdsMax) return nt;
+  return 0;
+}
+
+template <typename T, typename TO>
+hipError_t gemm_wide_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const void* WT, void* C, int c_in,
+                       int c_out, int rows_per_tile, hipStream_t s) {
+  const int nt = wide_nt(c_in, c_out, 2);
+  const int ksteps = (c_in + 31) / 32;
+  const int ldk = 32 * ksteps + 8;
+  const size_t lds = (size_t)16 * nt * ldk * sizeof(T);
+  ProfScope ps(KN_GEMM, s);
+  const dim3 grid((unsigned)total_tiles, (unsigned)(c_out / 16 / nt));
+  const T* a = static_cast<const T*>(A);
+  const T* w = static_cast<const T*>(WT);
+  TO* c = static_cast<TO*>(C);
+  switch (nt) {
+#define SPC_W(N)                                                                                                \
+  case N:                                                                                                       \
+    hipLaunchKernelGGL((k_gemm_wide<T, TO, N>), grid, dim3(kWideThreads), lds, s, g, a, w, c, c_in, c_out,      \
+                       ksteps, ldk, rows_per_tile);                                                             \
+    return hipGetLastError();
+    SPC_W(1)
+    SPC_W(2)
+    SPC_W(3)
+    SPC_W(4)
+    SPC_W(6)
+    SPC_W(8)
+    SPC_W(12)
+    SPC_W(16)
+#undef SPC_W
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+// wt[k][n][c] = w[k][c][n] through a 32 x 32 LDS tile (16-bit elements).
+__global__ __launch_bounds__(256) void k_transpose_w(const uint16_t* __restrict__ w, uint16_t* __restrict__ wt,
+                                                     int c_in, int c_out) {
+  __shared__ uint16_t t[32][33];
+  const int k = blockIdx.z;
+  const int c0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+  const uint16_t* src = w + (int64_t)k * c_in * c_out;
+  uint16_t* dst = wt + (int64_t)k * c_in * c_out;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int r = ty; r < 32; r += 8) {
+    const int c = c0 + r, n = n0 + tx;
+    t[r][tx] = (c < c_in && n < c_out) ? src[(int64_t)c * c_out + n] : 0;
+  }
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8) {
+    const int n = n0 + r, c = c0 + tx;
+    if (n < c_out && c < c_in) dst[(int64_t)n * c_in + c] = t[tx][r];
+  }
+}
+
 template <typename T, typename TO>
 hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const void* W, void* C, int c_in,
                   int c_out, int rows_per_tile, hipStream_t s) {
@@ -188,14 +345,29 @@ hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const
 
 }  // namespace
 
-hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, void* buf_out, int c_in,
-                       int c_out, int dtype, int part_dtype, hipStream_t s) {
+bool gemm_wide(int c_in, int c_out, int dtype, int part_dtype) {
+  // built for 16-bit operands with partials of the same type, and f16 with f32 partials
+  const bool pair = part_dtype == dtype || (dtype == 1 && part_dtype == 0);
+  return dtype != 0 && pair && wide_nt(c_in, c_out, 2) > 0;
+}
+
+hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_out, hipStream_t s) {
+  const dim3 grid((unsigned)((c_out + 31) / 32), (unsigned)((c_in + 31) / 32), (unsigned)K3);
+  hipLaunchKernelGGL(k_transpose_w, grid, dim3(256), 0, s, static_cast<const uint16_t*>(w),
+                     static_cast<uint16_t*>(wt), c_in, c_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, const void* wt,
+                       void* buf_out, int c_in, int c_out, int dtype, int part_dtype, hipStream_t s) {
   if (c_out % 16 != 0) return hipErrorInvalidValue;
+  const bool wide = wt && gemm_wide(c_in, c_out, dtype, part_dtype);
   int64_t rows_all = 0;
   for (int i = 0; i < n_seg; ++i) rows_all += segs[i].height;
-  // enough workgroups to fill 256 CUs several times, at most 1024 rows each
-  int rows_per_tile = 64;
-  while (rows_per_tile < 1024 && rows_all / (rows_per_tile * 2) >= 2048) rows_per_tile *= 2;
+  // enough workgroups to fill 256 CUs several times; tiles are whole rounds of the
+  // workgroup's 16-row waves
+  int rows_per_tile = wide ? 16 * kWideWaves : 64;
+  while (rows_per_tile < 2048 && rows_all / (rows_per_tile * 2) >= 1024) rows_per_tile *= 2;
   for (int base = 0; base < n_seg; base += kMaxSegPerLaunch) {
     GemmLaunchArgs g{};
     g.n_seg = 0;
@@ -214,7 +386,15 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
     g.tile_start[g.n_seg] = tiles;
     if (tiles == 0) continue;
     hipError_t e = hipErrorInvalidValue;
-    if (dtype == 0 && part_dtype == 0)
+    if (wide) {
+      if (dtype == 1 && part_dtype == 0)
+        e = gemm_wide_t<__half, float>(g, tiles, buf_in, wt, buf_out, c_in, c_out, rows_per_tile, s);
+      else if (dtype == 1 && part_dtype == 1)
+        e = gemm_wide_t<__half, __half>(g, tiles, buf_in, wt, buf_out, c_in, c_out, rows_per_tile, s);
+      else if (dtype == 2 && part_dtype == 2)
+        e = gemm_wide_t<__hip_bfloat16, __hip_bfloat16>(g, tiles, buf_in, wt, buf_out, c_in, c_out, rows_per_tile,
+                                                        s);
+    } else if (dtype == 0 && part_dtype == 0)
       e = gemm_t<float, float>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);
     else if (dtype == 1 && part_dtype == 0)
       e = gemm_t<__half, float>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);

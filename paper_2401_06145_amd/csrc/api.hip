@@ -424,7 +424,8 @@ size_t plan_forward_ws(void* base, const spconv_map* m, int c_in, int c_out, con
   Bump a(base);
   b->wt = gemm_wide(c_in, c_out, p.dtype, p.part_dtype) ? a.take_bytes((size_t)m->K3 * c_in * c_out * p.elem) : nullptr;
   b->buf_in = a.take_bytes((size_t)p.rows_real * c_in * p.elem);
-  b->buf_out = a.take_bytes((size_t)p.rows_real * c_out * p.pelem);
+  // one spare row past the partials: the full-width GEMM's stores of rows without data
+  b->buf_out = a.take_bytes((size_t)(p.rows_real + 1) * c_out * p.pelem);
   return align_up(a.off, 256);
 }
 
@@ -752,8 +753,9 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
       PhaseScope ph(PH_GEMM, s);
       if (b.wt) SPC_TRY(launch_transpose_w(d_w, b.wt, m->K3, c_in, c_out, s), "weight transpose");
       for (const auto& segs : p.launches)
-        SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), b.buf_in, d_w, b.wt, b.buf_out, c_in, c_out, dtype,
-                            p.part_dtype, s),
+        SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), b.buf_in, d_w, b.wt, b.buf_out,
+                            static_cast<char*>(b.buf_out) + (size_t)p.rows_real * c_out * p.pelem, c_in, c_out,
+                            dtype, p.part_dtype, s),
                 "grouped GEMM");
     }
   }

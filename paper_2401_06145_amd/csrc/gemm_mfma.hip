@@ -22,6 +22,8 @@
 // with 16-byte copies, and each wave loads the next 16-row block of buf_in while
 // it multiplies the current one.  k_gemm is the general fallback (any c_in,
 // float32) with a narrower column slice per workgroup.
+#include <algorithm>
+
 #include "common.h"
 
 namespace spc {
@@ -156,22 +158,43 @@ constexpr int kWideThreads = 512;
 constexpr int kWideWaves = kWideThreads / kWave;
 constexpr size_t kLdsMax = 160 * 1024;
 
-// NT = 16-column tiles per workgroup; ksteps = padded c_in / 32 <= kMaxKsteps.
-// wt is W^T, [K^3][c_out][c_in] row-major.
-constexpr int kMaxKsteps = 8;
-template <typename T, typename TO, int NT>
+// Register blocking of the full-width kernel.  A wave computes MB 16-row blocks
+// times NTW 16-column tiles, so every W^T fragment it reads from LDS feeds MB
+// MFMAs; CG waves split the workgroup's NT = CG * NTW column tiles, the others
+// take further rows.  Measured on gfx950, blocking (MB > 1 or CG > 1) lowers the
+// occupancy more than it saves LDS traffic for these HBM-bound products, so
+// both are 1; the structure stays for other shapes.
+constexpr int wide_cg(int) { return 1; }
+constexpr int wide_mb(int, int) { return 1; }
+
+// NT = 16-column tiles per workgroup; KSTEPS >= c_in / 32 k-steps of 32 (k past
+// c_in is zero).  wt is W^T, [K^3][c_out][c_in] row-major; dump is one spare
+// row of c_out partials that absorbs the stores of rows without data.  Loads
+// never branch: lanes without data (rows past the segment, k past c_in) read a
+// valid dummy address and select zero, so the compiler keeps the next blocks'
+// loads in flight across the current blocks' MFMAs.
+template <typename T, typename TO, int NT, int KSTEPS>
 __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, const T* __restrict__ A,
-                                                            const T* __restrict__ wt, TO* __restrict__ C, int c_in,
-                                                            int c_out, int ksteps, int ldk, int rows_per_tile) {
+                                                            const T* __restrict__ wt, TO* __restrict__ C,
+                                                            TO* __restrict__ dump, int c_in, int c_out, int ldk,
+                                                            int rows_per_tile) {
   using M = Mfma<T>;
+  using F = typename M::frag;
   static_assert(M::KS == 32, "16-bit operands only");
+  constexpr int CG = wide_cg(NT);
+  constexpr int NTW = NT / CG;
+  constexpr int MB = wide_mb(NTW, KSTEPS);
+  constexpr int RG = kWideWaves / CG;   // row groups
+  constexpr int STEP = RG * MB * 16;    // rows per round of the workgroup
+  static_assert(NT % CG == 0, "column groups must split the tiles");
   extern __shared__ __align__(16) unsigned char smem[];
   T* lw = reinterpret_cast<T*>(smem);  // [BN][ldk], W_k^T slice
   constexpr int BN = 16 * NT;
-  const int KP = 32 * ksteps;
+  constexpr int KP = 32 * KSTEPS;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
+  const int cg = wave % CG, rg = wave / CG;
 
   int s = 0;
   while (s + 1 < g.n_seg && g.tile_start[s + 1] <= (int)blockIdx.x) ++s;
@@ -184,7 +207,7 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
 
   // W_k^T rows n0 .. n0 + BN, 8 elements (16 bytes) per copy; columns past c_in are zero
   const T* wk = wt + ((int64_t)k * c_out + n0) * c_in;
-  const int CH = KP / 8;  // 16-byte chunks per LDS row
+  constexpr int CH = KP / 8;  // 16-byte chunks per LDS row
   for (int idx = tid; idx < BN * CH; idx += kWideThreads) {
     const int n = idx / CH;
     const int c = (idx - n * CH) * 8;
@@ -198,88 +221,111 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   const int r_end = min(r_begin + rows_per_tile, height);
   const int sub = lane >> 4;
   const int col = lane & 15;
-  typename M::frag cur[kMaxKsteps], nxt[kMaxKsteps];
-  auto load_block = [&](int m0, typename M::frag* f) {
-    const int row = m0 + col;
-    const bool real = row < rows;
-    const T* arow = A + (row0 + row) * (int64_t)c_in;
+  const int nw = 16 * NTW * cg;  // this wave's first column within the slice
+  const T* lwp = lw + (nw + col) * ldk + 8 * sub;
+  const int row_lim = min(rows, r_end);  // rows of this tile that hold data
+  // raw: the next blocks as loaded (dummy data where masked); cur: the blocks in use
+  F raw[MB][KSTEPS], cur[MB][KSTEPS];
+  auto issue = [&](int mb) {
 #pragma unroll
-    for (int q = 0; q < kMaxKsteps; ++q) {
-      const int kk = 32 * q + 8 * sub;
-      f[q] = (q < ksteps && real && kk < c_in) ? M::load(arow + kk) : M::zero();
-    }
-  };
-  int m0 = r_begin + wave * 16;
-  if (m0 < r_end) load_block(m0, cur);
-  for (; m0 < r_end; m0 += 16 * kWideWaves) {
-    const int m1 = m0 + 16 * kWideWaves;
-    if (m1 < r_end) load_block(m1, nxt);
-    f32x4 acc[NT];
+    for (int b = 0; b < MB; ++b) {
+      const int row = mb + 16 * b + col;
+      const T* arow = A + (row0 + row) * (int64_t)c_in;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int q = 0; q < kMaxKsteps; ++q) {
-      if (q >= ksteps) break;
-      const int kk = 32 * q + 8 * sub;
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const typename M::frag a = M::load(lw + (16 * t + col) * ldk + kk);
-        acc[t] = M::mma(a, cur[q], acc[t]);
+      for (int q = 0; q < KSTEPS; ++q) {
+        const int kk = 32 * q + 8 * sub;
+        raw[b][q] = M::load((row < row_lim && kk < c_in) ? arow + kk : A);
       }
     }
-    const int row = m0 + col;
-    if (row < rows) {
-      TO* crow = C + (row0 + row) * (int64_t)c_out + n0 + 4 * sub;
+  };
+  auto take = [&](int mb) {
 #pragma unroll
-      for (int t = 0; t < NT; ++t) store4(crow + 16 * t, acc[t]);
+    for (int b = 0; b < MB; ++b) {
+      const bool row_ok = mb + 16 * b + col < row_lim;
+#pragma unroll
+      for (int q = 0; q < KSTEPS; ++q) cur[b][q] = (row_ok && 32 * q + 8 * sub < c_in) ? raw[b][q] : M::zero();
     }
+  };
+  int m0 = r_begin + rg * MB * 16;
+  issue(m0);
+  take(m0);
+  for (; m0 < r_end; m0 += STEP) {
+    const int m1 = m0 + STEP;
+    issue(m1);  // masked to the dummy address past the tile; lands during the MFMAs below
+    // keeps the W^T fragment reads inside the loop: hoisted, they would need
+    // 4 * NTW * KSTEPS registers and spill
+    asm volatile("" ::: "memory");
+    f32x4 acc[MB][NTW];
 #pragma unroll
-    for (int q = 0; q < kMaxKsteps; ++q) cur[q] = nxt[q];
+    for (int b = 0; b < MB; ++b)
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) acc[b][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < KSTEPS; ++q) {
+      F wf[NTW];
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) wf[t] = M::load(lwp + 16 * t * ldk + 32 * q);
+#pragma unroll
+      for (int t = 0; t < NTW; ++t)
+#pragma unroll
+        for (int b = 0; b < MB; ++b) acc[b][t] = M::mma(wf[t], cur[b][q], acc[b][t]);
+    }
+    // lanes without a row store into the dump row instead of branching, so the
+    // store count is fixed and the wait for the next blocks below skips the stores
+#pragma unroll
+    for (int b = 0; b < MB; ++b) {
+      const int row = m0 + 16 * b + col;
+      TO* crow = (row < row_lim ? C + (row0 + row) * (int64_t)c_out : dump) + n0 + nw + 4 * sub;
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) store4(crow + 16 * t, acc[b][t]);
+    }
+    take(m1);
   }
+}
+
+// k-steps instantiated for the wide kernel (c_in up to 256); others round up
+int wide_ksteps(int c_in) {
+  const int ks = (c_in + 31) / 32;
+  for (int c : {1, 2, 3, 4, 6, 8})
+    if (ks <= c) return c;
+  return 0;
 }
 
 // Column tiles per workgroup for the wide kernel: the widest instantiated divisor
 // of c_out / 16 whose W^T slice fits the LDS; 0 if the wide kernel does not apply.
 int wide_nt(int c_in, int c_out, int elem) {
-  if (elem != 2 || c_in > 32 * kMaxKsteps || c_in % 8 != 0 || c_out % 16 != 0) return 0;
-  const int kp = (c_in + 31) / 32 * 32;
-  const int ldk = kp + 8;
+  if (elem != 2 || c_in % 8 != 0 || c_out % 16 != 0) return 0;
+  const int ks = wide_ksteps(c_in);
+  if (ks == 0) return 0;
+  const int ldk = 32 * ks + 8;
   const int nt_all = c_out / 16;
   for (int nt : {16, 12, 8, 6, 4, 3, 2, 1})
     if (nt_all % nt == 0 && (size_t)16 * nt * ldk * 2 <= kLdsMax) return nt;
   return 0;
 }
 
+// Rows of one round of the workgroup (tiles are whole rounds).
+int wide_round_rows(int nt, int ks) {
+  const int cg = wide_cg(nt);
+  return kWideWaves / cg * wide_mb(nt / cg, ks) * 16;
+}
+
 template <typename T, typename TO>
-hipError_t gemm_wide_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const void* WT, void* C, int c_in,
-                       int c_out, int rows_per_tile, hipStream_t s) {
-  const int nt = wide_nt(c_in, c_out, 2);
-  const int ksteps = (c_in + 31) / 32;
-  const int ldk = 32 * ksteps + 8;
-  const size_t lds = (size_t)16 * nt * ldk * sizeof(T);
-  ProfScope ps(KN_GEMM, s);
-  const dim3 grid((unsigned)total_tiles, (unsigned)(c_out / 16 / nt));
-  const T* a = static_cast<const T*>(A);
-  const T* w = static_cast<const T*>(WT);
-  TO* c = static_cast<TO*>(C);
-  switch (nt) {
-#define SPC_W(N)                                                                                                \
-  case N:                                                                                                       \
-    hipLaunchKernelGGL((k_gemm_wide<T, TO, N>), grid, dim3(kWideThreads), lds, s, g, a, w, c, c_in, c_out,      \
-                       ksteps, ldk, rows_per_tile);                                                             \
-    return hipGetLastError();
-    SPC_W(1)
-    SPC_W(2)
-    SPC_W(3)
-    SPC_W(4)
-    SPC_W(6)
-    SPC_W(8)
-    SPC_W(12)
-    SPC_W(16)
+const void* wide_kernel(int nt, int ks) {
+#define SPC_W(N, KS_) \
+  if (nt == N && ks == KS_) return reinterpret_cast<const void*>(&k_gemm_wide<T, TO, N, KS_>);
+#define SPC_WK(N) SPC_W(N, 1) SPC_W(N, 2) SPC_W(N, 3) SPC_W(N, 4) SPC_W(N, 6) SPC_W(N, 8)
+  SPC_WK(1) SPC_WK(2) SPC_WK(3) SPC_WK(4) SPC_WK(6) SPC_WK(8) SPC_WK(12) SPC_WK(16)
+#undef SPC_WK
 #undef SPC_W
-    default:
-      return hipErrorInvalidValue;
-  }
+  return nullptr;
+}
+
+const void* wide_kernel_for(int dtype, int part_dtype, int nt, int ks) {
+  if (dtype == 1 && part_dtype == 0) return wide_kernel<__half, float>(nt, ks);
+  if (dtype == 1 && part_dtype == 1) return wide_kernel<__half, __half>(nt, ks);
+  if (dtype == 2 && part_dtype == 2) return wide_kernel<__hip_bfloat16, __hip_bfloat16>(nt, ks);
+  return nullptr;
 }
 
 // wt[k][n][c] = w[k][c][n] through a 32 x 32 LDS tile (16-bit elements).
@@ -359,15 +405,38 @@ hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_o
 }
 
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, const void* wt,
-                       void* buf_out, int c_in, int c_out, int dtype, int part_dtype, hipStream_t s) {
+                       void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype, hipStream_t s) {
   if (c_out % 16 != 0) return hipErrorInvalidValue;
-  const bool wide = wt && gemm_wide(c_in, c_out, dtype, part_dtype);
+  const bool wide = wt && dump_row && gemm_wide(c_in, c_out, dtype, part_dtype);
   int64_t rows_all = 0;
   for (int i = 0; i < n_seg; ++i) rows_all += segs[i].height;
-  // enough workgroups to fill 256 CUs several times; tiles are whole rounds of the
-  // workgroup's 16-row waves
-  int rows_per_tile = wide ? 16 * kWideWaves : 64;
-  while (rows_per_tile < 2048 && rows_all / (rows_per_tile * 2) >= 1024) rows_per_tile *= 2;
+  int rows_per_tile = 64;
+  const void* wfn = nullptr;
+  int nt = 0, ks = 0, ldk = 0;
+  size_t lds = 0;
+  if (wide) {
+    // about two tiles per workgroup slot: larger tiles amortise the W^T staging, and
+    // two rounds of them keep the last round's idle CUs few
+    nt = wide_nt(c_in, c_out, 2);
+    ks = wide_ksteps(c_in);
+    ldk = 32 * ks + 8;
+    lds = (size_t)16 * nt * ldk * 2;
+    wfn = wide_kernel_for(dtype, part_dtype, nt, ks);
+    if (!wfn) return hipErrorInvalidValue;
+    int per_cu = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wfn, kWideThreads, lds);
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    const int64_t slots = (int64_t)std::max(per_cu, 1) * std::max(cus, 1);
+    const int round = wide_round_rows(nt, ks);
+    const int64_t want = (rows_all + 2 * slots - 1) / (2 * slots);
+    rows_per_tile = (int)std::min<int64_t>(std::max<int64_t>((want + round - 1) / round, 1) * round, 16 * round);
+  } else {
+    // enough workgroups to fill 256 CUs several times, at most 1024 rows each
+    while (rows_per_tile < 1024 && rows_all / (rows_per_tile * 2) >= 2048) rows_per_tile *= 2;
+  }
   for (int base = 0; base < n_seg; base += kMaxSegPerLaunch) {
     GemmLaunchArgs g{};
     g.n_seg = 0;
@@ -387,13 +456,14 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
     if (tiles == 0) continue;
     hipError_t e = hipErrorInvalidValue;
     if (wide) {
-      if (dtype == 1 && part_dtype == 0)
-        e = gemm_wide_t<__half, float>(g, tiles, buf_in, wt, buf_out, c_in, c_out, rows_per_tile, s);
-      else if (dtype == 1 && part_dtype == 1)
-        e = gemm_wide_t<__half, __half>(g, tiles, buf_in, wt, buf_out, c_in, c_out, rows_per_tile, s);
-      else if (dtype == 2 && part_dtype == 2)
-        e = gemm_wide_t<__hip_bfloat16, __hip_bfloat16>(g, tiles, buf_in, wt, buf_out, c_in, c_out, rows_per_tile,
-                                                        s);
+      ProfScope ps(KN_GEMM, s);
+      const dim3 grid((unsigned)tiles, (unsigned)(c_out / 16 / nt));
+      const void* a = buf_in;
+      const void* wtp = wt;
+      void* c = buf_out;
+      void* d = dump_row;
+      void* args[] = {&g, &a, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile};
+      e = hipLaunchKernel(wfn, grid, dim3(kWideThreads), args, lds, s);
     } else if (dtype == 0 && part_dtype == 0)
       e = gemm_t<float, float>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);
     else if (dtype == 1 && part_dtype == 0)

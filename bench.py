@@ -100,6 +100,26 @@ def kernel_models(n, n_out, pairs, L, k3, passes):
     return m
 
 
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter record of this
+    workload (profiles/hbm_traffic_*.json), or None if there is none or the
+    kernel's sources changed since the counters were taken."""
+    import glob
+
+    from paper_2401_06145_amd import profsum
+
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "hbm_traffic_*.json"))):
+        with open(path) as fh:
+            rec = json.load(fh)
+        k = rec.get("kernels", {}).get(kernel)
+        if rec.get("workload") != workload or not k:
+            continue
+        if k.get("source_sha256") != profsum.source_hash(kernel):
+            return None
+        return k["fetch_bytes"] + k["write_bytes"]
+    return None
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
@@ -208,6 +228,8 @@ def main():
                 "frac": round(achieved / peak, 5), "traffic": None, "kernel": dominant,
                 "algorithmic_flops_per_launch": work}
     roof.update({"mean_launch_ms": round(mean_launch_ms, 6), "launches_per_step": launches_per_step})
+    tb = measured_traffic(dominant, wl.name)
+    roof["traffic"] = round(tb) if tb is not None else None
 
     map_ms = sum(ph_ms.get(p, 0.0) for p in MAP_PHASES)
     gmas_ms = sum(ph_ms.get(p, 0.0) for p in GMAS_PHASES)

@@ -1,0 +1,171 @@
+"""Summaries of rocprofv3 output for the committed profiles.
+
+  stats    kernel-trace statistics (``--kernel-trace --stats``, CSV output) as a
+           Markdown table, one row per kernel, with the command that produced it.
+  traffic  HBM bytes per dispatch from two counter runs (FETCH_SIZE, then
+           WRITE_SIZE, in KiB per dispatch), each scaled by what the same counter
+           reads for a plain device copy of known size.  Writes a Markdown table
+           and a JSON record that bench.py reads for the roofline's ``traffic``
+           field; the record keeps a hash of each kernel's sources, so a kernel
+           changed since the counters were taken reports no traffic.
+
+Kernel names are folded to the ids of the library's timing API (e.g. both radix
+scatter variants are ``k_radix_scatter``), so per-dispatch figures line up with
+bench.py's per-launch timings.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import hashlib
+import json
+import os
+import re
+import sys
+
+CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+
+# timing-API id -> source file holding the kernel
+SOURCES = {
+    "k_minmax": "map_kernels.hip", "k_radix_hist": "map_kernels.hip", "k_radix_scatter": "map_kernels.hip",
+    "k_pack": "map_kernels.hip", "k_down_keys": "map_kernels.hip", "k_unique": "map_kernels.hip",
+    "k_backward": "map_kernels.hip", "k_forward_count": "map_kernels.hip", "k_forward_write": "map_kernels.hip",
+    "k_fill": "map_kernels.hip", "k_scan": "scan.hip", "k_gather": "gmas_kernels.hip",
+    "k_scatter": "gmas_kernels.hip", "k_concat": "gmas_kernels.hip", "k_gemm": "gemm_mfma.hip",
+    "k_transpose_w": "gemm_mfma.hip",
+}
+
+FOLD = [
+    (r"k_radix_(tile_scatter|pass)\b", "k_radix_scatter"),
+    (r"k_radix_(tile_hist|upsweep)\b", "k_radix_hist"),
+    (r"k_forward<\d+, false>", "k_forward_count"),
+    (r"k_forward<\d+, true>", "k_forward_write"),
+    (r"k_gemm(_wide)?\b", "k_gemm"),
+    (r"k_tile_(scan|reduce)\b", "k_scan"),
+    (r"k_minmax_(partial|final)\b", "k_minmax"),
+    (r"k_unique_(flags|write)\b", "k_unique"),
+    (r"k_fill_u32\b", "k_fill"),
+]
+
+
+def fold(name: str) -> str:
+    for pat, rep in FOLD:
+        if re.search(pat, name):
+            return rep
+    m = re.search(r"::(k_\w+)", name)
+    if m:
+        return m.group(1)
+    return name.split("(")[0][:60]
+
+
+def source_hash(kid: str) -> str | None:
+    src = SOURCES.get(kid)
+    if not src:
+        return None
+    h = hashlib.sha256()
+    for f in ("common.h", src):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def cmd_stats(a) -> None:
+    rows = list(csv.DictReader(open(a.csv)))
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    out = [f"# {a.title}", "", f"Command: `{a.command}`", "",
+           "rocprofv3 kernel-trace statistics (all dispatches of the run, including the bench's",
+           "warm-up and breakdown passes).", "",
+           "| kernel | timing id | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name = r["Name"]
+        short = re.sub(r"\(.*", "", name.replace("spc::(anonymous namespace)::", "")).replace("void ", "")
+        out.append(f"| `{short[:70]}` | {fold(name)} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                   f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                   f"{float(r['TotalDurationNs']) / total * 100:.1f}% |")
+    # per timing id: the mean over all dispatches of the kernels folded into it
+    agg = collections.defaultdict(lambda: [0, 0.0])
+    for r in rows:
+        d = agg[fold(r["Name"])]
+        d[0] += int(r["Calls"])
+        d[1] += float(r["TotalDurationNs"])
+    out += ["", "Per timing id (what bench.py's per-launch means compare with):", "",
+            "| timing id | dispatches | mean us |", "|---|---|---|"]
+    for kid, (n, t) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        out.append(f"| {kid} | {n} | {t / n / 1e3:.2f} |")
+    print("\n".join(out))
+
+
+def _counter(path: str, counter: str) -> dict[str, list[float]]:
+    per = collections.defaultdict(list)
+    for r in csv.DictReader(open(path)):
+        if r.get("Counter_Name") == counter:
+            per[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return per
+
+
+def _copy_scale(path: str, counter: str, true_bytes: float) -> float:
+    per = _counter(path, counter)
+    # the copy's dispatches are the ones with the most traffic
+    name = max(per, key=lambda k: sum(per[k]) / len(per[k]))
+    kib = sum(per[name]) / len(per[name])
+    return true_bytes / (kib * 1024.0)
+
+
+def cmd_traffic(a) -> None:
+    nbytes = a.copy_mib * 1024 * 1024
+    fs = _copy_scale(a.copy_fetch, "FETCH_SIZE", nbytes)
+    ws = _copy_scale(a.copy_write, "WRITE_SIZE", nbytes)
+    fetch = _counter(a.fetch, "FETCH_SIZE")
+    write = _counter(a.write, "WRITE_SIZE")
+    agg = {}
+    for src, key in ((fetch, "fetch"), (write, "write")):
+        for name, vals in src.items():
+            kid = fold(name)
+            d = agg.setdefault(kid, {"fetch": [], "write": []})
+            d[key].extend(vals)
+    rec = {"command_fetch": a.command_fetch, "command_write": a.command_write, "workload": a.workload,
+           "fetch_scale": fs, "write_scale": ws, "copy_mib": a.copy_mib, "kernels": {}}
+    lines = [f"# {a.title}", "", f"Counter runs: `{a.command_fetch}` and `{a.command_write}`;",
+             f"calibration: the same two counters over a plain {a.copy_mib} MiB device copy "
+             f"(`{a.command_copy}`), giving scale factors FETCH x{fs:.3f}, WRITE x{ws:.3f}.", "",
+             "Bytes per dispatch (mean over the run's dispatches), after scaling.", "",
+             "| timing id | dispatches | HBM read MB | HBM write MB | total MB |", "|---|---|---|---|---|"]
+    for kid, d in sorted(agg.items(), key=lambda t: -(sum(t[1]["fetch"]) + sum(t[1]["write"]))):
+        if not d["fetch"] or not d["write"]:
+            continue
+        fb = sum(d["fetch"]) / len(d["fetch"]) * 1024 * fs
+        wb = sum(d["write"]) / len(d["write"]) * 1024 * ws
+        rec["kernels"][kid] = {"dispatches": len(d["fetch"]), "fetch_bytes": fb, "write_bytes": wb,
+                               "source_sha256": source_hash(kid)}
+        lines.append(f"| {kid} | {len(d['fetch'])} | {fb / 1e6:.3f} | {wb / 1e6:.3f} | {(fb + wb) / 1e6:.3f} |")
+    with open(a.json, "w") as fh:
+        json.dump(rec, fh, indent=1, sort_keys=True)
+    print("\n".join(lines))
+
+
+def main(argv=None) -> None:
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    sub = p.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    s.add_argument("--command", required=True)
+    s.add_argument("--title", required=True)
+    t = sub.add_parser("traffic")
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--copy-fetch", required=True)
+    t.add_argument("--copy-write", required=True)
+    t.add_argument("--copy-mib", type=int, required=True)
+    t.add_argument("--command-fetch", required=True)
+    t.add_argument("--command-write", required=True)
+    t.add_argument("--command-copy", required=True)
+    t.add_argument("--workload", required=True)
+    t.add_argument("--title", required=True)
+    t.add_argument("--json", required=True)
+    a = p.parse_args(argv)
+    (cmd_stats if a.cmd == "stats" else cmd_traffic)(a)
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:])

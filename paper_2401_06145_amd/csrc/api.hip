@@ -422,7 +422,9 @@ struct FwdBufs {
 
 size_t plan_forward_ws(void* base, const spconv_map* m, int c_in, int c_out, const GmasPlan& p, FwdBufs* b) {
   Bump a(base);
-  b->wt = gemm_wide(c_in, c_out, p.dtype, p.part_dtype) ? a.take_bytes((size_t)m->K3 * c_in * c_out * p.elem) : nullptr;
+  b->wt = (gemm_wide(c_in, c_out, p.dtype, p.part_dtype) && gemm_wide_transposed(c_in, c_out))
+              ? a.take_bytes((size_t)m->K3 * c_in * c_out * p.elem)
+              : nullptr;
   b->buf_in = a.take_bytes((size_t)p.rows_real * c_in * p.elem);
   // one spare row past the partials: the full-width GEMM's stores of rows without data
   b->buf_out = a.take_bytes((size_t)(p.rows_real + 1) * c_out * p.pelem);

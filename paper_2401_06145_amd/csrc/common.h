@@ -184,12 +184,14 @@ struct GemmSeg {
   int64_t rows;
   int64_t height;
 };
-// Whether the full-width kernel applies (it needs the transposed weights).
+// Whether the full-width kernel applies, and whether it wants the weights
+// transposed beforehand (large W_k; small ones are transposed while staging).
 bool gemm_wide(int c_in, int c_out, int dtype, int part_dtype);
+bool gemm_wide_transposed(int c_in, int c_out);
 // wt[k][n][c] = w[k][c][n] for 16-bit weights.
 hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_out, hipStream_t s);
 // Launches the segments (any number; split into launches of at most 64 segments).
-// wt: transposed weights (launch_transpose_w) or NULL for the general kernel;
+// wt: transposed weights (launch_transpose_w) or NULL;
 // dump_row: one spare row of c_out partials the full-width kernel may overwrite.
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, const void* wt,
                        void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,

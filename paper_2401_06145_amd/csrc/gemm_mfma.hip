@@ -168,14 +168,16 @@ constexpr int wide_cg(int) { return 1; }
 constexpr int wide_mb(int, int) { return 1; }
 
 // NT = 16-column tiles per workgroup; KSTEPS >= c_in / 32 k-steps of 32 (k past
-// c_in is zero).  wt is W^T, [K^3][c_out][c_in] row-major; dump is one spare
+// c_in is zero).  w is W, [K^3][c_in][c_out]; wt is NULL or W^T, [K^3][c_out][c_in]
+// (then W_k^T is staged from it with 16-byte copies); dump is one spare
 // row of c_out partials that absorbs the stores of rows without data.  Loads
 // never branch: lanes without data (rows past the segment, k past c_in) read a
 // valid dummy address and select zero, so the compiler keeps the next blocks'
 // loads in flight across the current blocks' MFMAs.
 template <typename T, typename TO, int NT, int KSTEPS>
 __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, const T* __restrict__ A,
-                                                            const T* __restrict__ wt, TO* __restrict__ C,
+                                                            const T* __restrict__ w, const T* __restrict__ wt,
+                                                            TO* __restrict__ C,
                                                             TO* __restrict__ dump, int c_in, int c_out, int ldk,
                                                             int rows_per_tile) {
   using M = Mfma<T>;
@@ -205,15 +207,27 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   const int tile = (int)blockIdx.x - g.tile_start[s];
   const int n0 = blockIdx.y * BN;
 
-  // W_k^T rows n0 .. n0 + BN, 8 elements (16 bytes) per copy; columns past c_in are zero
-  const T* wk = wt + ((int64_t)k * c_out + n0) * c_in;
-  constexpr int CH = KP / 8;  // 16-byte chunks per LDS row
-  for (int idx = tid; idx < BN * CH; idx += kWideThreads) {
-    const int n = idx / CH;
-    const int c = (idx - n * CH) * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (c < c_in) v = *reinterpret_cast<const uint4*>(wk + (int64_t)n * c_in + c);
-    *reinterpret_cast<uint4*>(lw + n * ldk + c) = v;
+  if (wt) {
+    // W_k^T rows n0 .. n0 + BN from the transposed copy, 8 elements (16 bytes) per
+    // copy; columns past c_in are zero
+    const T* wk = wt + ((int64_t)k * c_out + n0) * c_in;
+    constexpr int CH = KP / 8;  // 16-byte chunks per LDS row
+    for (int idx = tid; idx < BN * CH; idx += kWideThreads) {
+      const int n = idx / CH;
+      const int c = (idx - n * CH) * 8;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (c < c_in) v = *reinterpret_cast<const uint4*>(wk + (int64_t)n * c_in + c);
+      *reinterpret_cast<uint4*>(lw + n * ldk + c) = v;
+    }
+  } else {
+    // small W_k: transpose while staging, one element per thread and step (reads
+    // coalesced along n; the LDS row pitch keeps the 2-byte writes conflict-free)
+    const T* wk = w + (int64_t)k * c_in * c_out + n0;
+    for (int idx = tid; idx < BN * KP; idx += kWideThreads) {
+      const int c = idx / BN;
+      const int n = idx - c * BN;
+      lw[n * ldk + c] = (c < c_in) ? wk[(int64_t)c * c_out + n] : zero_elem<T>();
+    }
   }
   __syncthreads();
 
@@ -391,6 +405,8 @@ hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const
 
 }  // namespace
 
+bool gemm_wide_transposed(int c_in, int c_out) { return c_in * c_out >= 128 * 128; }
+
 bool gemm_wide(int c_in, int c_out, int dtype, int part_dtype) {
   // built for 16-bit operands with partials of the same type, and f16 with f32 partials
   const bool pair = part_dtype == dtype || (dtype == 1 && part_dtype == 0);
@@ -407,7 +423,7 @@ hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_o
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, const void* wt,
                        void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype, hipStream_t s) {
   if (c_out % 16 != 0) return hipErrorInvalidValue;
-  const bool wide = wt && dump_row && gemm_wide(c_in, c_out, dtype, part_dtype);
+  const bool wide = dump_row && gemm_wide(c_in, c_out, dtype, part_dtype);
   int64_t rows_all = 0;
   for (int i = 0; i < n_seg; ++i) rows_all += segs[i].height;
   int rows_per_tile = 64;
@@ -462,7 +478,8 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
       const void* wtp = wt;
       void* c = buf_out;
       void* d = dump_row;
-      void* args[] = {&g, &a, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile};
+      const void* wp = w;
+      void* args[] = {&g, &a, &wp, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile};
       e = hipLaunchKernel(wfn, grid, dim3(kWideThreads), args, lds, s);
     } else if (dtype == 0 && part_dtype == 0)
       e = gemm_t<float, float>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);

@@ -126,19 +126,22 @@ __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, Key
 }
 
 // ----------------------------------------------------------------------------
-// LSD radix sort of (u64 key, u32 value), 8-bit digits, stable, one kernel per
-// pass.  An up-front kernel counts the digits of every pass in one read
-// (per-block partials, no global atomics).  Each pass kernel then takes a tile
-// ticket, ranks its keys with wave64 ballots that match equal digits, publishes
-// its per-digit counts, and adds up the counts of all earlier tiles by looking
-// back over their published words.  Tiles are numbered in start order, so every
-// tile a workgroup waits for is already running; waits are bounded and report
-// an error flag instead of hanging.  The first pass may read int32 coordinates
-// and pack the keys itself.
+// LSD radix sort of (u64 key, u32 value), 8-bit digits, stable.  Large inputs
+// run one kernel per pass: an up-front kernel counts the digits of every pass
+// in one read (per-block partials, reduced by a second small kernel, no global
+// atomics); each pass kernel then takes a tile ticket, ranks its keys with
+// wave64 ballots that match equal digits, publishes its per-digit counts, and
+// adds up the counts of all earlier tiles by looking back over their published
+// words.  Tiles are numbered in start order, so every tile a workgroup waits
+// for is already running; waits are bounded and report an error flag instead
+// of hanging.  The first pass may read int32 coordinates and pack the keys
+// itself.  Every scatter goes through LDS: the tile is first ordered by digit
+// there, so that consecutive threads write consecutive addresses of a digit's
+// run.
 // ----------------------------------------------------------------------------
 constexpr int kRsItems = 8;
 constexpr int kRsTile = kThreads * kRsItems;
-constexpr int kRsUpBlocks = 64;
+constexpr int kRsUpBlocks = 512;
 constexpr int kRsMaxPasses = 8;
 constexpr uint32_t kStAgg = 1u << 30;   // word holds this tile's count of the digit
 constexpr uint32_t kStIncl = 2u << 30;  // word holds the count over tiles 0..this one
@@ -179,6 +182,116 @@ __device__ __forceinline__ uint64_t load_key(const uint64_t* keys, const int4* c
   }
 }
 
+// Exclusive scan of one value per thread over the 256-thread block (4 waves).
+__device__ __forceinline__ uint32_t block_excl256(uint32_t v, uint32_t* s_wave) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, kWave);
+    if (lane >= d) x += y;
+  }
+  if (lane == kWave - 1) s_wave[wave] = x;
+  __syncthreads();
+  uint32_t e = x - v;
+  for (int w = 0; w < wave; ++w) e += s_wave[w];
+  __syncthreads();  // s_wave may be reused
+  return e;
+}
+
+// LDS of one tile scatter.
+struct TileLds {
+  uint64_t key[kRsTile];
+  uint32_t val[kRsTile];
+  uint32_t ldig[256];  // tile-local first position of each digit
+  uint32_t lrun[256];  // next tile-local position of each digit
+  uint32_t gbase[256]; // global position of the tile's first key of each digit
+  uint32_t cnt[256];
+  uint32_t wcnt[kWavesPerBlock][256];
+  uint32_t s_wave[kWavesPerBlock];
+};
+
+// Counts this thread's valid keys into t.cnt (which must be zero).
+__device__ __forceinline__ void tile_count(TileLds& t, const uint64_t key[kRsItems], int64_t base, int64_t n,
+                                           int shift) {
+#pragma unroll
+  for (int r = 0; r < kRsItems; ++r) {
+    const int64_t i = base + r * kThreads + threadIdx.x;
+    if (i < n) {
+      const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
+      const uint64_t peers = match_digit(d);
+      if ((peers & lanemask_lt()) == 0) atomicAdd(&t.cnt[d], (uint32_t)popc64(peers));
+    }
+  }
+}
+
+// Stable scatter of one tile: keys are ranked round by round (index order) with
+// wave ballots.  STAGED: each key goes to its digit-ordered tile position in LDS,
+// then the tile is written out so that consecutive threads store consecutive
+// positions of a digit's run (pays off once the sort is bandwidth-bound).
+// Otherwise each key is stored at its global position straight away (fewer
+// steps, for small latency-bound sorts).  Needs t.gbase (and, STAGED, t.cnt:
+// the tile's digit counts) filled, and a barrier since.
+template <bool STAGED>
+__device__ __forceinline__ void tile_scatter(TileLds& t, const uint64_t key[kRsItems], const uint32_t val[kRsItems],
+                                             int64_t base, int64_t n, int shift, uint64_t* kout, uint32_t* vout) {
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave;
+  if (STAGED) {
+    const uint32_t ld = block_excl256(t.cnt[tid], t.s_wave);
+    t.ldig[tid] = ld;
+    t.lrun[tid] = ld;
+  } else {
+    t.lrun[tid] = t.gbase[tid];
+  }
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) t.wcnt[w][tid] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kRsItems; ++r) {
+    const int64_t i = base + r * kThreads + tid;
+    const bool valid = i < n;
+    uint32_t d = 0, rank = 0;
+    if (valid) {
+      d = (uint32_t)(key[r] >> shift) & 255u;
+      const uint64_t peers = match_digit(d);
+      rank = (uint32_t)popc64(peers & lanemask_lt());
+      if (rank == 0) t.wcnt[wave][d] = (uint32_t)popc64(peers);
+    }
+    __syncthreads();
+    if (valid) {
+      uint32_t pos = t.lrun[d] + rank;
+      for (int w = 0; w < wave; ++w) pos += t.wcnt[w][d];
+      if (STAGED) {
+        t.key[pos] = key[r];
+        t.val[pos] = val[r];
+      } else {
+        kout[pos] = key[r];
+        vout[pos] = val[r];
+      }
+    }
+    __syncthreads();
+    uint32_t add = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      add += t.wcnt[w][tid];
+      t.wcnt[w][tid] = 0;
+    }
+    t.lrun[tid] += add;
+    __syncthreads();
+  }
+  if (!STAGED) return;
+  const int tile_n = (int)min((int64_t)kRsTile, n - base);
+  for (int i = tid; i < tile_n; i += kThreads) {
+    const uint64_t k = t.key[i];
+    const uint32_t d = (uint32_t)(k >> shift) & 255u;
+    const uint32_t g = t.gbase[d] + (uint32_t)i - t.ldig[d];
+    kout[g] = k;
+    vout[g] = t.val[i];
+  }
+}
+
 template <bool FROM_COORDS>
 __global__ __launch_bounds__(kThreads) void k_radix_upsweep(const uint64_t* keys, const int4* coords, KeyLayout L,
                                                             int64_t n, int passes, uint32_t* gpart, uint32_t* status,
@@ -202,27 +315,50 @@ __global__ __launch_bounds__(kThreads) void k_radix_upsweep(const uint64_t* keys
   if (blockIdx.x == 0 && (int)threadIdx.x < passes) tickets[threadIdx.x] = 0u;
 }
 
+// One workgroup per pass: sums the up-front partials of its pass over the
+// gblocks blocks (4 partial sums per digit) and writes the exclusive scan over
+// digits, i.e. the first sorted position of each digit: gofs[pass][d].
+__global__ __launch_bounds__(1024) void k_radix_totals(const uint32_t* gpart, int gblocks, int passes,
+                                                        uint32_t* gofs) {
+  __shared__ uint32_t part[4][256];
+  __shared__ uint32_t s_wave[16];
+  const int p = blockIdx.x;
+  const int d = threadIdx.x & 255, q = threadIdx.x >> 8;
+  uint32_t s = 0;
+#pragma unroll 8
+  for (int g = q; g < gblocks; g += 4) s += gpart[((int64_t)g * passes + p) * 256 + d];
+  part[q][d] = s;
+  __syncthreads();
+  // every thread takes part in the scan (threads past the first 256 carry zeros),
+  // so every barrier is reached by the whole workgroup
+  const uint32_t tot = (q == 0) ? part[0][d] + part[1][d] + part[2][d] + part[3][d] : 0u;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  uint32_t x = tot;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
+  }
+  if (lane == kWave - 1) s_wave[wave] = x;
+  __syncthreads();
+  if (q == 0) {
+    uint32_t e = x - tot;
+    for (int w = 0; w < wave; ++w) e += s_wave[w];
+    gofs[p * 256 + d] = e;
+  }
+}
+
 template <bool FROM_COORDS>
 __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, const uint32_t* vin, const int4* coords,
                                                          KeyLayout L, uint64_t* kout, uint32_t* vout, int64_t n,
-                                                         int pass, int passes, const uint32_t* gpart, int gblocks,
-                                                         uint32_t* status, uint32_t* tickets, uint32_t* err) {
+                                                         int pass, const uint32_t* gofs, uint32_t* status,
+                                                         uint32_t* tickets, uint32_t* err) {
+  __shared__ TileLds t;
   __shared__ uint32_t s_tile;
-  __shared__ uint32_t cnt[256];
-  __shared__ uint32_t run[256];
-  __shared__ uint32_t wcnt[kWavesPerBlock][256];
-  __shared__ uint32_t s_wave[kWavesPerBlock];
   const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
   const int shift = 8 * pass;
   if (tid == 0) s_tile = atomicAdd(&tickets[pass], 1u);
-  cnt[tid] = 0;
-#pragma unroll
-  for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][tid] = 0;
-  // count of digit `tid` over all keys, from the up-front partials
-  uint32_t tot = 0;
-  for (int g = 0; g < gblocks; ++g) tot += gpart[((int64_t)g * passes + pass) * 256 + tid];
+  t.cnt[tid] = 0;
   __syncthreads();
   const int64_t tile = s_tile;
   const int64_t base = tile * kRsTile;
@@ -237,25 +373,13 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
     if (i < n) {
       key[r] = load_key<FROM_COORDS>(kin, coords, L, i);
       val[r] = FROM_COORDS ? (uint32_t)i : vin[i];
-      const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
-      const uint64_t peers = match_digit(d);
-      if ((peers & lanemask_lt()) == 0) atomicAdd(&cnt[d], (uint32_t)popc64(peers));
     }
   }
-  // exclusive scan of the global digit counts: first position of digit `tid`
-  uint32_t x = tot;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const uint32_t y = __shfl_up(x, d, kWave);
-    if (lane >= d) x += y;
-  }
-  if (lane == kWave - 1) s_wave[wave] = x;
+  tile_count(t, key, base, n, shift);
   __syncthreads();
-  uint32_t gofs = x - tot;
-  for (int w = 0; w < wave; ++w) gofs += s_wave[w];
 
   // publish this tile's count of digit `tid` and look back over earlier tiles
-  const uint32_t c = cnt[tid];
+  const uint32_t c = t.cnt[tid];
   uint32_t* st = status + (int64_t)pass * gridDim.x * 256;
   uint32_t excl = 0;
   if (tile == 0) {
@@ -294,38 +418,8 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
     }
     st_coherent(&st[tile * 256 + tid], kStIncl | (excl + c));
   }
-  run[tid] = gofs + excl;
-  __syncthreads();
-
-  // stable scatter: rounds in index order, ranks within a round from wave ballots
-#pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
-    const int64_t i = base + r * kThreads + tid;
-    const bool valid = i < n;
-    uint32_t d = 0, rank = 0;
-    if (valid) {
-      d = (uint32_t)(key[r] >> shift) & 255u;
-      const uint64_t peers = match_digit(d);
-      rank = (uint32_t)popc64(peers & lanemask_lt());
-      if (rank == 0) wcnt[wave][d] = (uint32_t)popc64(peers);
-    }
-    __syncthreads();
-    if (valid) {
-      uint32_t pos = run[d] + rank;
-      for (int w = 0; w < wave; ++w) pos += wcnt[w][d];
-      kout[pos] = key[r];
-      vout[pos] = val[r];
-    }
-    __syncthreads();
-    uint32_t add = 0;
-#pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) {
-      add += wcnt[w][tid];
-      wcnt[w][tid] = 0;
-    }
-    run[tid] += add;
-    __syncthreads();
-  }
+  t.gbase[tid] = gofs[pass * 256 + tid] + excl;
+  tile_scatter<true>(t, key, val, base, n, shift, kout, vout);
 }
 
 // Small inputs (few tiles): per-tile digit histograms, then a stable scatter.
@@ -368,9 +462,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
                                                             const int4* coords, KeyLayout L, uint64_t* kout,
                                                             uint32_t* vout, int64_t n, int shift,
                                                             const uint32_t* offs, int64_t ntiles) {
-  __shared__ uint32_t run[256];
-  __shared__ uint32_t wcnt[kWavesPerBlock][256];
-  __shared__ uint32_t s_wave[kWavesPerBlock];
+  __shared__ TileLds t;
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   const int64_t base = (int64_t)blockIdx.x * kRsTile;
@@ -398,20 +490,20 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
       uint4 v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
-        const int64_t t = t0 + (int64_t)u * kWavesPerBlock;
-        v[u] = (t < ntiles) ? h4[t * 64 + lane] : make_uint4(0, 0, 0, 0);
+        const int64_t tt = t0 + (int64_t)u * kWavesPerBlock;
+        v[u] = (tt < ntiles) ? h4[tt * 64 + lane] : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
-        const int64_t t = t0 + (int64_t)u * kWavesPerBlock;
+        const int64_t tt = t0 + (int64_t)u * kWavesPerBlock;
         tot4.x += v[u].x; tot4.y += v[u].y; tot4.z += v[u].z; tot4.w += v[u].w;
-        if (t < tile) {
+        if (tt < tile) {
           bef.x += v[u].x; bef.y += v[u].y; bef.z += v[u].z; bef.w += v[u].w;
         }
       }
     }
-    // per-wave partial sums -> per-digit sums (thread d)
-    uint32_t* s_part = &wcnt[0][0];  // reused as [wave][digit] partials; cleared below
+    // per-wave partial sums -> per-digit sums (thread d); wcnt serves as scratch
+    uint32_t* s_part = &t.wcnt[0][0];
     reinterpret_cast<uint4*>(s_part)[wave * 64 + lane] = tot4;
     __syncthreads();
     uint32_t tot = 0;
@@ -423,52 +515,12 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
     uint32_t before = 0;
 #pragma unroll
     for (int w = 0; w < kWavesPerBlock; ++w) before += s_part[w * 256 + tid];
-    // exclusive scan of the digit totals across the block
-    uint32_t x = tot;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-      const uint32_t y = __shfl_up(x, d, kWave);
-      if (lane >= d) x += y;
-    }
-    if (lane == kWave - 1) s_wave[wave] = x;
-    __syncthreads();
-    uint32_t dbase = x - tot;
-    for (int w = 0; w < wave; ++w) dbase += s_wave[w];
-    run[tid] = dbase + before;
+    t.gbase[tid] = block_excl256(tot, t.s_wave) + before;
   } else {
-    run[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
+    t.gbase[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
   }
-#pragma unroll
-  for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][tid] = 0;
   __syncthreads();
-#pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
-    const int64_t i = base + r * kThreads + tid;
-    const bool valid = i < n;
-    uint32_t d = 0, rank = 0;
-    if (valid) {
-      d = (uint32_t)(key[r] >> shift) & 255u;
-      const uint64_t peers = match_digit(d);
-      rank = (uint32_t)popc64(peers & lanemask_lt());
-      if (rank == 0) wcnt[wave][d] = (uint32_t)popc64(peers);
-    }
-    __syncthreads();
-    if (valid) {
-      uint32_t pos = run[d] + rank;
-      for (int w = 0; w < wave; ++w) pos += wcnt[w][d];
-      kout[pos] = key[r];
-      vout[pos] = val[r];
-    }
-    __syncthreads();
-    uint32_t add = 0;
-#pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) {
-      add += wcnt[w][tid];
-      wcnt[w][tid] = 0;
-    }
-    run[tid] += add;
-    __syncthreads();
-  }
+  tile_scatter<false>(t, key, val, base, n, shift, kout, vout);
 }
 
 // ----------------------------------------------------------------------------
@@ -798,8 +850,9 @@ size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 size_t radix_temp_bytes(int64_t n) {
   const int64_t ntiles = std::max<int64_t>(1, (n + kRsTile - 1) / kRsTile);
   const size_t gpart = (size_t)kRsUpBlocks * kRsMaxPasses * 256 * sizeof(uint32_t);
+  const size_t gofs = (size_t)kRsMaxPasses * 256 * sizeof(uint32_t);
   const size_t status = (size_t)kRsMaxPasses * ntiles * 256 * sizeof(uint32_t);
-  const size_t onesweep = align256(gpart) + align256(status) + 256;
+  const size_t onesweep = align256(gpart) + align256(gofs) + align256(status) + 256;
   const size_t tiled = align256((size_t)256 * ntiles * sizeof(uint32_t)) + scan_temp_bytes(256 * ntiles);
   return std::max(onesweep, tiled);
 }
@@ -878,7 +931,9 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
     return radix_sort_tiled(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
   const size_t gpart_bytes = (size_t)kRsUpBlocks * kRsMaxPasses * 256 * sizeof(uint32_t);
   uint32_t* gpart = static_cast<uint32_t*>(d_temp);
-  uint32_t* status = reinterpret_cast<uint32_t*>(static_cast<char*>(d_temp) + ((gpart_bytes + 255) & ~(size_t)255));
+  uint32_t* gofs = reinterpret_cast<uint32_t*>(static_cast<char*>(d_temp) + align256(gpart_bytes));
+  uint32_t* status = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(gofs) +
+                                                 align256((size_t)kRsMaxPasses * 256 * sizeof(uint32_t)));
   const int64_t status_words = (int64_t)passes * ntiles * 256;
   uint32_t* tickets = reinterpret_cast<uint32_t*>(
       reinterpret_cast<char*>(status) +
@@ -895,6 +950,10 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
       hipLaunchKernelGGL(k_radix_upsweep<false>, dim3(gblocks), dim3(kThreads), 0, s, keys, nullptr, L, n, passes,
                          gpart, status, status_words, tickets);
     e = hipGetLastError();
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(k_radix_totals, dim3(passes), dim3(1024), 0, s, gpart, gblocks, passes, gofs);
+      e = hipGetLastError();
+    }
   }
   if (e != hipSuccess) return e;
   // ping-pong so that the last pass lands in (keys, vals)
@@ -916,10 +975,10 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
       ProfScope ps(KN_RADIX_SCATTER, s);
       if (first)
         hipLaunchKernelGGL(k_radix_pass<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr, c4, L,
-                           kb[dst], vb[dst], n, p, passes, gpart, gblocks, status, tickets, err);
+                           kb[dst], vb[dst], n, p, gofs, status, tickets, err);
       else
         hipLaunchKernelGGL(k_radix_pass<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], vb[src],
-                           nullptr, L, kb[dst], vb[dst], n, p, passes, gpart, gblocks, status, tickets, err);
+                           nullptr, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

@@ -70,7 +70,9 @@ def measure(n: int, side: int, rounds: int, K: int = 3):
     per_launch = {
         "k_radix_scatter": (16 * n + 12 * n + (passes - 1) * 24 * n) / max(passes, 1),
         "k_forward_count": 8 * n + 8 * n + 4 * k3 * n,
-        "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 8 * pairs,
+        # reads the results and the rows of the matches; writes the pair lists, the
+        # query-side table's matches and the whole source-side table
+        "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 12 * pairs + 4 * k3 * n,
     }
     row = {"voxels": n, "grid": side, "pairs": pairs, "map_ms": round(map_ms, 4),
            "phases_ms": {k: round(v, 4) for k, v in phases.items()},

@@ -571,12 +571,12 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   }
   {
     PhaseScope ph(PH_FORWARD, s);
-    hipError_t e = launch_forward(a, false, b.bounds, b.nb, b.istart, b.item_cnt, nullptr, b.max_items, b.pin,
-                                  b.pout, b.cb, s);
+    hipError_t e = launch_forward(a, false, b.bounds, b.chunks, b.nb, b.istart, b.item_cnt, nullptr, b.max_items,
+                                  b.pin, b.pout, b.cb, s);
     if (e == hipSuccess) e = scan_exclusive_u32(b.item_cnt, b.item_off, b.max_items, &b.cb->n_pairs, b.scan_tmp, s);
     if (e == hipSuccess)
-      e = launch_forward(a, true, b.bounds, b.nb, b.istart, b.item_cnt, b.item_off, b.max_items, b.pin, b.pout,
-                         b.cb, s);
+      e = launch_forward(a, true, b.bounds, b.chunks, b.nb, b.istart, b.item_cnt, b.item_off, b.max_items, b.pin,
+                         b.pout, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "forward search"));
   }
   {

@@ -154,8 +154,8 @@ hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, ui
                            ControlBlock* cb, hipStream_t s);
 // Forward search over the balanced work items: count pass (write = false) fills
 // item_cnt; write pass places pairs at item_off and fills cb->seg_pair_start.
-hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, int64_t nb,
-                          const uint32_t* istart, uint32_t* item_cnt, const uint32_t* item_off,
+hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, const uint32_t* chunks,
+                          int64_t nb, const uint32_t* istart, uint32_t* item_cnt, const uint32_t* item_off,
                           int64_t max_items, int32_t* pin, int32_t* pout, ControlBlock* cb,
                           hipStream_t s);
 

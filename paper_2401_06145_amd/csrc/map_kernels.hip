@@ -641,14 +641,14 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
 }
 
 // ----------------------------------------------------------------------------
-// Forward binary search (Section 5.1.2).  One workgroup per load-balanced
-// query block (work item): the source block is staged in LDS and each lane
-// binary-searches its queries there, recording the match (or -1) in T_q.
-// COUNT pass: matches per work item.  WRITE pass: matches ranked with wave
-// ballots; pair e of the item goes to index o = item_off + e, so every
-// offset's pairs come out in sorted-query order, and o, the pair's GEMM buffer
-// row, is also stored in both metadata tables (T_q in place of the source
-// position, T_s at the source position).
+// Forward binary search (Section 5.1.2) over the load-balanced work items
+// (query chunks of at most Cq queries of one (offset, source block) pair): the
+// source block is staged in LDS and each lane binary-searches its queries
+// there, recording the match (or -1) in T_q.  Count pass: matches per work
+// item.  Write pass: matches ranked with wave ballots; pair e of the item goes
+// to index o = item_off + e, so every offset's pairs come out in sorted-query
+// order, and o, the pair's GEMM buffer row, is also stored in both metadata
+// tables (T_q in place of the source position, T_s at the source position).
 // ----------------------------------------------------------------------------
 struct ItemRange {
   int k;
@@ -683,44 +683,34 @@ __device__ __forceinline__ int lds_lower(const uint64_t* lkey, int nB, int log2B
   return pos;
 }
 
-template <int ROUNDS, bool WRITE>
-__global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32_t* bounds, int64_t nb,
-                                                      const uint32_t* istart, uint32_t* item_cnt,
-                                                      const uint32_t* item_off, int32_t* pin, int32_t* pout,
-                                                      ControlBlock* cb, int log2B) {
-  extern __shared__ __align__(16) unsigned char smem[];
+// Forward search, write pass: one workgroup per work item.  The count pass left
+// each query's result in T_q (matching sorted source position, or -1); matches
+// are ranked with wave ballots from the item's scanned match offset, so every
+// offset's pairs come out in sorted-query order, and pair index o (the pair's
+// GEMM buffer row) replaces the source position in T_q and is stored in T_s.
+template <int ROUNDS>
+__global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const uint32_t* bounds, int64_t nb,
+                                                            const uint32_t* istart, const uint32_t* item_off,
+                                                            int32_t* pin, int32_t* pout, ControlBlock* cb) {
   __shared__ int64_t s_kb;
   __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
-  uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
   const int64_t w = blockIdx.x;
   const int64_t n_items = cb->n_items;
 
-  if (WRITE && w == 0 && tid <= a.K3) {
+  if (w == 0 && tid <= a.K3) {
     // per-offset pair counts: the items of offset k are [istart[k nb], istart[(k+1) nb])
     const int k = tid;
     const int64_t first = (k < a.K3) ? (int64_t)istart[(int64_t)k * nb] : n_items;
     const uint64_t off = (first < n_items) ? (uint64_t)item_off[first] : (uint64_t)cb->n_pairs;
     cb->seg_pair_start[k] = (uint32_t)off;
   }
-  if (w >= n_items) {  // workgroup-uniform; idle items count zero matches
-    if (!WRITE && tid == 0) item_cnt[w] = 0;
-    return;
-  }
+  if (w >= n_items) return;  // workgroup-uniform: the grid is sized for the worst case
 
   const ItemRange it = locate_item(a, w, nb, bounds, istart, &s_kb);
-  const int64_t s0 = it.b * (int64_t)a.B;
-  const int nB = (int)min((int64_t)a.B, a.n_src - s0);
-  if (!WRITE) {
-    for (int e = tid; e < nB; e += kThreads) lkey[e] = a.skeys[s0 + e];
-    __syncthreads();
-  }
-  // dense per-query result of this offset: sorted source position, or -1
   int32_t* res = a.res + (int64_t)it.k * a.res_stride;
-
-  const uint64_t dk = (uint64_t)a.dk[it.k];
   int32_t r_in[ROUNDS], r_out[ROUNDS], r_sp[ROUNDS];
   uint64_t bal[ROUNDS];
   // mirrored offset's T_s row, for the misses of a symmetric map
@@ -733,23 +723,16 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
     r_out[r] = 0;
     r_sp[r] = -1;
     if (qp < it.q1) {
-      if (!WRITE) {
-        const uint64_t key = a.qkeys[qp] + dk;
-        const int pos = lds_lower(lkey, nB, log2B, key);
-        hit = pos < nB && lkey[pos] == key;
-        res[qp] = hit ? (int32_t)(s0 + pos) : -1;
-      } else {
-        const int32_t sp = res[qp];
-        if (sp >= 0) {
-          hit = true;
-          r_sp[r] = sp;
-          const int32_t src = (int32_t)a.sidx[sp];
-          const int32_t qry = (int32_t)a.qrow[qp];
-          r_in[r] = a.swap_roles ? qry : src;
-          r_out[r] = a.swap_roles ? src : qry;
-        } else if (a.sym) {
-          ts_mirror[qp] = -1;
-        }
+      const int32_t sp = res[qp];
+      if (sp >= 0) {
+        hit = true;
+        r_sp[r] = sp;
+        const int32_t src = (int32_t)a.sidx[sp];
+        const int32_t qry = (int32_t)a.qrow[qp];
+        r_in[r] = a.swap_roles ? qry : src;
+        r_out[r] = a.swap_roles ? src : qry;
+      } else if (a.sym) {
+        ts_mirror[qp] = -1;
       }
     }
     bal[r] = __ballot(hit);
@@ -766,10 +749,6 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
       total += s_cnt[r][v];
     }
   }
-  if (!WRITE) {
-    if (tid == 0) item_cnt[w] = total;
-    return;
-  }
   const uint64_t base = item_off[w];
   int32_t* ts = a.ts + (int64_t)it.k * a.ts_stride;
 #pragma unroll
@@ -785,25 +764,90 @@ __global__ __launch_bounds__(kThreads) void k_forward(SearchArgs a, const uint32
   }
 }
 
-template <bool WRITE>
-hipError_t forward_t(int rounds, unsigned grid, size_t lds, hipStream_t s, const SearchArgs& a,
-                     const uint32_t* bounds, int64_t nb, const uint32_t* istart, uint32_t* item_cnt,
-                     const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb, int log2B) {
-  ProfScope ps(WRITE ? KN_FORWARD_WRITE : KN_FORWARD_COUNT, s);
-  switch (rounds) {
-#define SPC_F(R)                                                                                                    \
-  case R:                                                                                                           \
-    hipLaunchKernelGGL((k_forward<R, WRITE>), dim3(grid), dim3(kThreads), lds, s, a, bounds, nb, istart, item_cnt, \
-                       item_off, pin, pout, cb, log2B);                                                             \
-    break;
-    SPC_F(1)
-    SPC_F(2)
-    SPC_F(4)
-    SPC_F(8)
-#undef SPC_F
-    default:
-      return hipErrorInvalidValue;
+// Forward search, count pass, with source-block reuse: one workgroup per
+// (source block b, group of G offsets) stages block b in LDS once and then runs
+// every work item of (k, b) for the offsets k of its group, chunk by chunk (the
+// items and their order are those of the balance step).  Each chunk stores its
+// queries' results and its match count.  With few source blocks the groups are
+// small, so that the grid still fills the GPU; with many, one workgroup takes
+// all K^3 offsets of its block and reads it from HBM once instead of K^3 times.
+template <int ROUNDS>
+__global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const uint32_t* bounds,
+                                                            const uint32_t* chunks, int64_t nb,
+                                                            const uint32_t* istart, uint32_t* item_cnt,
+                                                            int64_t max_items, int G, ControlBlock* cb, int log2B) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
+  uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int64_t b = (int64_t)blockIdx.x % nb;
+  const int g = (int)((int64_t)blockIdx.x / nb);
+  const int64_t n_items = cb->n_items;
+  // items past the last one count zero: the match-count scan runs over max_items
+  for (int64_t i = n_items + (int64_t)blockIdx.x * kThreads + tid; i < max_items; i += (int64_t)gridDim.x * kThreads)
+    item_cnt[i] = 0;
+
+  const int64_t s0 = b * (int64_t)a.B;
+  const int nB = (int)min((int64_t)a.B, a.n_src - s0);
+  for (int e = tid; e < nB; e += kThreads) lkey[e] = a.skeys[s0 + e];
+  __syncthreads();
+
+  const int k_end = min(a.K3, (g + 1) * G);
+  for (int k = g * G; k < k_end; ++k) {
+    const int64_t kb = (int64_t)k * nb + b;
+    const int64_t q_lo = (b == 0) ? 0 : (int64_t)bounds[kb - 1];
+    const int64_t q_hi = bounds[kb];
+    const uint32_t nch = chunks[kb];
+    const int64_t first = istart[kb];
+    int32_t* res = a.res + (int64_t)k * a.res_stride;
+    const uint64_t dk = (uint64_t)a.dk[k];
+    for (uint32_t c = 0; c < nch; ++c) {
+      const int64_t q0 = q_lo + (int64_t)c * a.Cq;
+      const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
+#pragma unroll
+      for (int r = 0; r < ROUNDS; ++r) {
+        const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+        bool hit = false;
+        if (qp < q1) {
+          const uint64_t key = a.qkeys[qp] + dk;
+          const int pos = lds_lower(lkey, nB, log2B, key);
+          hit = pos < nB && lkey[pos] == key;
+          res[qp] = hit ? (int32_t)(s0 + pos) : -1;
+        }
+        const uint64_t bal = __ballot(hit);
+        if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal);
+      }
+      __syncthreads();
+      if (tid == 0 && first + c < max_items) {
+        uint32_t total = 0;
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r)
+#pragma unroll
+          for (int v = 0; v < kWavesPerBlock; ++v) total += s_cnt[r][v];
+        item_cnt[first + c] = total;
+      }
+      __syncthreads();  // s_cnt is rewritten by the next chunk
+    }
   }
+}
+
+template <int ROUNDS>
+hipError_t forward_count_t(unsigned grid, size_t lds, hipStream_t s, const SearchArgs& a, const uint32_t* bounds,
+                           const uint32_t* chunks, int64_t nb, const uint32_t* istart, uint32_t* item_cnt,
+                           int64_t max_items, int G, ControlBlock* cb, int log2B) {
+  hipLaunchKernelGGL((k_forward_count<ROUNDS>), dim3(grid), dim3(kThreads), lds, s, a, bounds, chunks, nb, istart,
+                     item_cnt, max_items, G, cb, log2B);
+  return hipGetLastError();
+}
+
+template <int ROUNDS>
+hipError_t forward_write_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds, int64_t nb,
+                           const uint32_t* istart, const uint32_t* item_off, int32_t* pin, int32_t* pout,
+                           ControlBlock* cb) {
+  hipLaunchKernelGGL((k_forward_write<ROUNDS>), dim3(grid), dim3(kThreads), 0, s, a, bounds, nb, istart, item_off,
+                     pin, pout, cb);
   return hipGetLastError();
 }
 
@@ -1019,17 +1063,40 @@ hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, ui
   return hipGetLastError();
 }
 
-hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, int64_t nb, const uint32_t* istart,
-                          uint32_t* item_cnt, const uint32_t* item_off, int64_t max_items, int32_t* pin,
-                          int32_t* pout, ControlBlock* cb, hipStream_t s) {
+// Workgroups the count pass aims for when choosing its offset groups.
+constexpr int64_t kCountTargetGroups = 8192;
+
+hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, const uint32_t* chunks, int64_t nb,
+                          const uint32_t* istart, uint32_t* item_cnt, const uint32_t* item_off, int64_t max_items,
+                          int32_t* pin, int32_t* pout, ControlBlock* cb, hipStream_t s) {
   int log2B = 0;
   while ((1 << log2B) < a.B) ++log2B;
-  const size_t lds = write ? 0 : (size_t)a.B * sizeof(uint64_t);
   const int rounds = a.Cq / kThreads;
-  const unsigned grid = (unsigned)(max_items > 0 ? max_items : 1);
-  if (write)
-    return forward_t<true>(rounds, grid, lds, s, a, bounds, nb, istart, item_cnt, item_off, pin, pout, cb, log2B);
-  return forward_t<false>(rounds, grid, lds, s, a, bounds, nb, istart, item_cnt, item_off, pin, pout, cb, log2B);
+  if (write) {
+    const unsigned grid = (unsigned)(max_items > 0 ? max_items : 1);
+    ProfScope ps(KN_FORWARD_WRITE, s);
+    switch (rounds) {
+      case 1: return forward_write_t<1>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
+      case 2: return forward_write_t<2>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
+      case 4: return forward_write_t<4>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
+      case 8: return forward_write_t<8>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (nb <= 0) return hipSuccess;
+  const int64_t ngroups0 = std::min<int64_t>(a.K3, std::max<int64_t>(1, (kCountTargetGroups + nb - 1) / nb));
+  const int G = (int)((a.K3 + ngroups0 - 1) / ngroups0);
+  const int64_t ngroups = (a.K3 + G - 1) / G;
+  const unsigned grid = (unsigned)(nb * ngroups);
+  const size_t lds = (size_t)a.B * sizeof(uint64_t);
+  ProfScope ps(KN_FORWARD_COUNT, s);
+  switch (rounds) {
+    case 1: return forward_count_t<1>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 2: return forward_count_t<2>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 4: return forward_count_t<4>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 8: return forward_count_t<8>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace spc

@@ -39,8 +39,8 @@ SOURCES = {
 FOLD = [
     (r"k_radix_(tile_scatter|pass)\b", "k_radix_scatter"),
     (r"k_radix_(tile_hist|upsweep)\b", "k_radix_hist"),
-    (r"k_forward<\d+, false>", "k_forward_count"),
-    (r"k_forward<\d+, true>", "k_forward_write"),
+    (r"k_forward_count\b", "k_forward_count"),
+    (r"k_forward_write\b", "k_forward_write"),
     (r"k_gemm(_wide)?\b", "k_gemm"),
     (r"k_tile_(scan|reduce)\b", "k_scan"),
     (r"k_minmax_(partial|final)\b", "k_minmax"),

@@ -159,9 +159,10 @@ __device__ __forceinline__ void st_coherent(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Lanes of the wave whose digit equals this lane's digit (among active lanes).
-__device__ __forceinline__ uint64_t match_digit(uint32_t d) {
-  uint64_t m = __ballot(1);
+// Lanes of the wave whose digit equals this lane's digit, among the active lanes
+// that pass `valid`.
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid = true) {
+  uint64_t m = __ballot(valid);
 #pragma unroll
   for (int b = 0; b < 8; ++b) {
     const bool bit = (d >> b) & 1u;
@@ -204,65 +205,89 @@ __device__ __forceinline__ uint32_t block_excl256(uint32_t v, uint32_t* s_wave) 
 struct TileLds {
   uint64_t key[kRsTile];
   uint32_t val[kRsTile];
-  uint32_t ldig[256];  // tile-local first position of each digit
-  uint32_t lrun[256];  // next tile-local position of each digit
-  uint32_t gbase[256]; // global position of the tile's first key of each digit
-  uint32_t cnt[256];
-  uint32_t wcnt[kWavesPerBlock][256];
+  uint32_t ldig[256];   // tile-local first position of each digit
+  uint32_t gbase[256];  // global position of the tile's first key of each digit
+  uint32_t cnt[256];    // the tile's count of each digit
+  uint32_t wc[kWavesPerBlock][256];  // per-wave digit counts, then each wave's first position
   uint32_t s_wave[kWavesPerBlock];
 };
 
-// Counts this thread's valid keys into t.cnt (which must be zero).
-__device__ __forceinline__ void tile_count(TileLds& t, const uint64_t key[kRsItems], int64_t base, int64_t n,
-                                           int shift) {
+// Tile layout: wave w holds keys base + w * kRsWaveKeys + r * 64 + lane, r < kRsItems,
+// so each wave owns a contiguous run of the tile and can rank it on its own.
+constexpr int kRsWaveKeys = kWave * kRsItems;
+__device__ __forceinline__ int64_t tile_index(int64_t base, int r) {
+  return base + (int64_t)(threadIdx.x / kWave) * kRsWaveKeys + (int64_t)r * kWave + (threadIdx.x & (kWave - 1));
+}
+
+template <bool FROM_COORDS>
+__device__ __forceinline__ void tile_load(const uint64_t* kin, const uint32_t* vin, const int4* coords,
+                                          const KeyLayout& L, int64_t base, int64_t n, uint64_t key[kRsItems],
+                                          uint32_t val[kRsItems]) {
 #pragma unroll
   for (int r = 0; r < kRsItems; ++r) {
-    const int64_t i = base + r * kThreads + threadIdx.x;
+    const int64_t i = tile_index(base, r);
+    key[r] = 0;
+    val[r] = 0;
     if (i < n) {
-      const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
-      const uint64_t peers = match_digit(d);
-      if ((peers & lanemask_lt()) == 0) atomicAdd(&t.cnt[d], (uint32_t)popc64(peers));
+      key[r] = load_key<FROM_COORDS>(kin, coords, L, i);
+      val[r] = FROM_COORDS ? (uint32_t)i : vin[i];
     }
   }
 }
 
-// Stable scatter of one tile: keys are ranked round by round (index order) with
-// wave ballots.  STAGED: each key goes to its digit-ordered tile position in LDS,
-// then the tile is written out so that consecutive threads store consecutive
-// positions of a digit's run (pays off once the sort is bandwidth-bound).
-// Otherwise each key is stored at its global position straight away (fewer
-// steps, for small latency-bound sorts).  Needs t.gbase (and, STAGED, t.cnt:
-// the tile's digit counts) filled, and a barrier since.
+// Stable ranks within the wave's run: rank[r] = number of earlier keys of the
+// wave with the same digit.  Leaves the wave's digit counts in t.wc[wave] (which
+// must be zero).  No workgroup barrier: a wave's LDS accesses complete in order,
+// so every lane reads a counter before its digit's leader bumps it.
+__device__ __forceinline__ void tile_rank(TileLds& t, const uint64_t key[kRsItems], int64_t base, int64_t n,
+                                          int shift, uint32_t rank[kRsItems]) {
+  const int wave = threadIdx.x / kWave;
+#pragma unroll
+  for (int r = 0; r < kRsItems; ++r) {
+    const bool valid = tile_index(base, r) < n;
+    const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
+    const uint64_t peers = match_digit(d, valid);
+    rank[r] = 0;
+    if (valid) {
+      const uint32_t before = (uint32_t)popc64(peers & lanemask_lt());
+      rank[r] = t.wc[wave][d] + before;
+      if (before == 0) t.wc[wave][d] += (uint32_t)popc64(peers);
+    }
+  }
+}
+
+// Places a ranked tile.  Needs t.wc (per-wave counts) and t.gbase, a barrier
+// since, and for STAGED t.cnt.  STAGED: each key goes to its digit-ordered tile
+// position in LDS, then the tile is written out so that consecutive threads
+// store consecutive positions of a digit's run (pays off once the sort is
+// bandwidth-bound).  Otherwise each key is stored at its global position
+// straight away (fewer steps, for small latency-bound sorts).
 template <bool STAGED>
-__device__ __forceinline__ void tile_scatter(TileLds& t, const uint64_t key[kRsItems], const uint32_t val[kRsItems],
-                                             int64_t base, int64_t n, int shift, uint64_t* kout, uint32_t* vout) {
+__device__ __forceinline__ void tile_place(TileLds& t, const uint64_t key[kRsItems], const uint32_t val[kRsItems],
+                                           const uint32_t rank[kRsItems], int64_t base, int64_t n, int shift,
+                                           uint64_t* kout, uint32_t* vout) {
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
+  uint32_t start;  // first position of digit tid in this tile: tile-local (STAGED) or global
   if (STAGED) {
-    const uint32_t ld = block_excl256(t.cnt[tid], t.s_wave);
-    t.ldig[tid] = ld;
-    t.lrun[tid] = ld;
+    start = block_excl256(t.cnt[tid], t.s_wave);
+    t.ldig[tid] = start;
   } else {
-    t.lrun[tid] = t.gbase[tid];
+    start = t.gbase[tid];
   }
+  // each wave's first position of digit tid
 #pragma unroll
-  for (int w = 0; w < kWavesPerBlock; ++w) t.wcnt[w][tid] = 0;
+  for (int w = 0; w < kWavesPerBlock; ++w) {
+    const uint32_t c = t.wc[w][tid];
+    t.wc[w][tid] = start;
+    start += c;
+  }
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < kRsItems; ++r) {
-    const int64_t i = base + r * kThreads + tid;
-    const bool valid = i < n;
-    uint32_t d = 0, rank = 0;
-    if (valid) {
-      d = (uint32_t)(key[r] >> shift) & 255u;
-      const uint64_t peers = match_digit(d);
-      rank = (uint32_t)popc64(peers & lanemask_lt());
-      if (rank == 0) t.wcnt[wave][d] = (uint32_t)popc64(peers);
-    }
-    __syncthreads();
-    if (valid) {
-      uint32_t pos = t.lrun[d] + rank;
-      for (int w = 0; w < wave; ++w) pos += t.wcnt[w][d];
+    if (tile_index(base, r) < n) {
+      const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
+      const uint32_t pos = t.wc[wave][d] + rank[r];
       if (STAGED) {
         t.key[pos] = key[r];
         t.val[pos] = val[r];
@@ -271,17 +296,9 @@ __device__ __forceinline__ void tile_scatter(TileLds& t, const uint64_t key[kRsI
         vout[pos] = val[r];
       }
     }
-    __syncthreads();
-    uint32_t add = 0;
-#pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) {
-      add += t.wcnt[w][tid];
-      t.wcnt[w][tid] = 0;
-    }
-    t.lrun[tid] += add;
-    __syncthreads();
   }
   if (!STAGED) return;
+  __syncthreads();
   const int tile_n = (int)min((int64_t)kRsTile, n - base);
   for (int i = tid; i < tile_n; i += kThreads) {
     const uint64_t k = t.key[i];
@@ -358,28 +375,24 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
   const int tid = threadIdx.x;
   const int shift = 8 * pass;
   if (tid == 0) s_tile = atomicAdd(&tickets[pass], 1u);
-  t.cnt[tid] = 0;
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
   __syncthreads();
   const int64_t tile = s_tile;
   const int64_t base = tile * kRsTile;
 
   uint64_t key[kRsItems];
   uint32_t val[kRsItems];
-#pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
-    const int64_t i = base + r * kThreads + tid;
-    key[r] = 0;
-    val[r] = 0;
-    if (i < n) {
-      key[r] = load_key<FROM_COORDS>(kin, coords, L, i);
-      val[r] = FROM_COORDS ? (uint32_t)i : vin[i];
-    }
-  }
-  tile_count(t, key, base, n, shift);
+  uint32_t rank[kRsItems];
+  tile_load<FROM_COORDS>(kin, vin, coords, L, base, n, key, val);
+  tile_rank(t, key, base, n, shift, rank);
   __syncthreads();
 
   // publish this tile's count of digit `tid` and look back over earlier tiles
-  const uint32_t c = t.cnt[tid];
+  uint32_t c = 0;
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) c += t.wc[w][tid];
+  t.cnt[tid] = c;
   uint32_t* st = status + (int64_t)pass * gridDim.x * 256;
   uint32_t excl = 0;
   if (tile == 0) {
@@ -419,7 +432,8 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
     st_coherent(&st[tile * 256 + tid], kStIncl | (excl + c));
   }
   t.gbase[tid] = gofs[pass * 256 + tid] + excl;
-  tile_scatter<true>(t, key, val, base, n, shift, kout, vout);
+  __syncthreads();
+  tile_place<true>(t, key, val, rank, base, n, shift, kout, vout);
 }
 
 // Small inputs (few tiles): per-tile digit histograms, then a stable scatter.
@@ -466,19 +480,13 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   const int64_t base = (int64_t)blockIdx.x * kRsTile;
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
   // the tile's keys are loaded first, so that their latency overlaps the offset sums
   uint64_t key[kRsItems];
   uint32_t val[kRsItems];
-#pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
-    const int64_t i = base + r * kThreads + tid;
-    key[r] = 0;
-    val[r] = 0;
-    if (i < n) {
-      key[r] = load_key<FROM_COORDS>(kin, coords, L, i);
-      val[r] = FROM_COORDS ? (uint32_t)i : vin[i];
-    }
-  }
+  uint32_t rank[kRsItems];
+  tile_load<FROM_COORDS>(kin, vin, coords, L, base, n, key, val);
   if (FUSED) {
     // wave v sums tiles v, v + 4, ...; lane l covers digits 4l..4l+3 with 16-byte loads,
     // so all of a wave's loads are independent and in flight together
@@ -502,8 +510,9 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
         }
       }
     }
-    // per-wave partial sums -> per-digit sums (thread d); wcnt serves as scratch
-    uint32_t* s_part = &t.wcnt[0][0];
+    // per-wave partial sums -> per-digit sums (thread d); the key stage serves as
+    // scratch (this kernel writes keys straight to their global positions)
+    uint32_t* s_part = reinterpret_cast<uint32_t*>(t.key);
     reinterpret_cast<uint4*>(s_part)[wave * 64 + lane] = tot4;
     __syncthreads();
     uint32_t tot = 0;
@@ -519,8 +528,10 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
   } else {
     t.gbase[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
   }
+  __syncthreads();  // wc cleared
+  tile_rank(t, key, base, n, shift, rank);
   __syncthreads();
-  tile_scatter<false>(t, key, val, base, n, shift, kout, vout);
+  tile_place<false>(t, key, val, rank, base, n, shift, kout, vout);
 }
 
 // ----------------------------------------------------------------------------

@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 METRIC = "sparse-conv layer ms (Map + GMaS split); Map GB/s, GEMM TFLOP/s vs peak"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}
-MAP_PHASES = ("bounds", "sort", "outcoords", "backward", "balance", "metadata", "forward", "readback")
+MAP_PHASES = ("bounds", "sort", "hash", "outcoords", "backward", "balance", "metadata", "forward", "readback")
 GMAS_PHASES = ("gather", "gemm", "scatter")
 
 

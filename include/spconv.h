@@ -81,7 +81,12 @@ typedef struct {
   int presorted;     /* spconv_build_map: 1 = the input rows are already unique and in ascending
                         (b, x, y, z) order (e.g. a DOWN map's outputs), so the sort is skipped
                         (Section 5.1.1); checked on the device (SPCONV_EINVAL if not sorted) */
-  int reserved[8];
+  int search;        /* spconv_build_map, SPCONV_SUBM only: 0 = sorted arrays and the double-
+                        traversed binary search (Section 5.1, default); 1 = a GPU hash table over
+                        the input coordinates probed once per (output, offset), the prior-art
+                        Map of Section 2.2 Step 1, kept as an ablation.  Same pairs (as sets),
+                        listed in caller-row order within each offset */
+  int reserved[7];
 } spconv_options;
 
 typedef struct spconv_map spconv_map; /* opaque host-side object */
@@ -128,7 +133,8 @@ const int32_t* spconv_map_out_coords(const spconv_map* m);
 /* h_counts[k] = |M_k| for k in [0, K^3). */
 int spconv_map_counts(const spconv_map* m, int64_t* h_counts);
 /* Device pointers to offset k's pairs: (*d_in_idx)[e] meets (*d_out_idx)[e] through
- * W_k, e in [0, *count).  Order inside one offset: ascending sorted query position. */
+ * W_k, e in [0, *count).  Order inside one offset: ascending sorted query position
+ * (caller-row order for maps built with the hash-table search). */
 int spconv_map_pairs(const spconv_map* m, int k, const int32_t** d_in_idx,
                      const int32_t** d_out_idx, int64_t* count);
 /* Stream-ordered copies into caller buffers: all pairs, offset-major (offset k's

@@ -79,10 +79,10 @@ struct Bump {
 const char* prof_name(int id) {
   static const char* kNames[PROF_IDS] = {
       "bounds", "sort", "outcoords", "backward", "balance", "forward", "readback", "metadata", "gather", "gemm",
-      "scatter", "", "", "", "", "",
+      "scatter", "hash", "", "", "", "",
       "k_minmax", "k_radix_hist", "k_radix_scatter", "k_scan", "k_copy", "k_down_keys", "k_unique", "k_backward",
       "k_forward_count", "k_forward_write", "k_fill", "", "k_gather", "k_gemm", "k_scatter", "k_pack",
-      "", "", "", "", "", "", "", ""};
+      "k_hash_insert", "k_hash_probe", "", "", "", "", "", ""};
   return (id >= 0 && id < PROF_IDS) ? kNames[id] : "";
 }
 struct PhaseRec {
@@ -184,6 +184,9 @@ struct MapBufs {
   int32_t* ts;    // T_s, the source-side table
   uint32_t* item_cnt;
   uint32_t* item_off;
+  uint64_t* hkeys;  // hash-table search only
+  uint32_t* hvals;
+  int log2cap;
   int32_t* mm_partial;
   void* scan_tmp;
   int64_t max_items;
@@ -194,6 +197,7 @@ struct Tunables {
   int B = 1024;
   int Cq = 1024;
   bool presorted = false;
+  bool hash = false;  // hash-table search instead of the sorted-array search
 };
 
 int read_tunables(const spconv_options* opt, Tunables* t) {
@@ -210,6 +214,8 @@ int read_tunables(const spconv_options* opt, Tunables* t) {
     t->Cq = opt->Cq;
   }
   t->presorted = opt->presorted != 0;
+  if (opt->search < 0 || opt->search > 1) return fail(SPCONV_EINVAL, "search must be 0 or 1");
+  t->hash = opt->search == 1;
   return SPCONV_OK;
 }
 
@@ -245,6 +251,17 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   b->item_off = m.take<uint32_t>(b->max_items);
   b->mm_partial = static_cast<int32_t*>(m.take_bytes(minmax_temp_bytes()));
   b->scan_tmp = m.take_bytes(scan_temp_bytes(std::max(std::max(nkb, n_src), b->max_items)));
+  b->log2cap = 0;
+  b->hkeys = nullptr;
+  b->hvals = nullptr;
+  if (tu.hash) {
+    // 2^log2cap >= 2 n slots: load at most 1/2
+    int lg = 2;
+    while (((int64_t)1 << lg) < 2 * std::max<int64_t>(n_src, 1)) ++lg;
+    b->log2cap = lg;
+    b->hkeys = m.take<uint64_t>((int64_t)1 << lg);
+    b->hvals = m.take<uint32_t>((int64_t)1 << lg);
+  }
   return align_up(m.off, 256);
 }
 
@@ -462,6 +479,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   if (mode != SPCONV_UP) n_out = 0;
   Tunables tu;
   if ((st = read_tunables(opt, &tu)) != SPCONV_OK) return st;
+  if (tu.hash && mode != SPCONV_SUBM) return fail(SPCONV_EUNSUPPORTED, "the hash-table search covers SPCONV_SUBM only");
   const int K3 = K * K * K;
   const int64_t n_src = (mode == SPCONV_UP) ? n_out : n_in;
   const int64_t nq_max = n_in;
@@ -509,7 +527,11 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     if (e != hipSuccess) return bail(hip_fail(e, "coordinate bounds"));
     if ((st = make_layout(h->minmax, h->minmax + 4, K, stride, tensor_stride, &L)) != SPCONV_OK) return bail(st);
   }
-  {
+  if (tu.hash) {
+    PhaseScope ph(PH_HASH, s);
+    hipError_t e = launch_hash_build(d_in_coords, n_in, L, b.hkeys, b.hvals, b.log2cap, b.skeys, b.sidx, &b.cb->err, s);
+    if (e != hipSuccess) return bail(hip_fail(e, "hash build"));
+  } else {
     PhaseScope ph(PH_SORT, s);
     // sorted inputs (a previous layer's outputs) only need their keys packed (Section 5.1.1)
     hipError_t e = tu.presorted ? launch_pack(src_coords, n_src, L, b.skeys, b.sidx, s)
@@ -553,14 +575,17 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   a.ts = b.ts;
   a.ts_stride = n_src;
   a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
+  // the hash-table search treats all queries of an offset as one block
+  const int64_t nb = tu.hash ? 1 : b.nb;
   {
     PhaseScope ph(PH_BACKWARD, s);
-    hipError_t e = launch_backward(a, b.nb, b.bounds, b.chunks, b.cb, s);
+    hipError_t e = tu.hash ? launch_hash_items(K3, nq_max, tu.Cq, b.bounds, b.chunks, s)
+                           : launch_backward(a, b.nb, b.bounds, b.chunks, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "backward search"));
   }
   {
     PhaseScope ph(PH_BALANCE, s);
-    hipError_t e = scan_exclusive_u32(b.chunks, b.istart, (int64_t)K3 * b.nb, &b.cb->n_items, b.scan_tmp, s);
+    hipError_t e = scan_exclusive_u32(b.chunks, b.istart, (int64_t)K3 * nb, &b.cb->n_items, b.scan_tmp, s);
     if (e != hipSuccess) return bail(hip_fail(e, "balance"));
   }
   if (!a.sym) {
@@ -571,11 +596,12 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   }
   {
     PhaseScope ph(PH_FORWARD, s);
-    hipError_t e = launch_forward(a, false, b.bounds, b.chunks, b.nb, b.istart, b.item_cnt, nullptr, b.max_items,
-                                  b.pin, b.pout, b.cb, s);
+    hipError_t e = tu.hash ? launch_hash_count(a, b.hkeys, b.hvals, b.log2cap, b.item_cnt, b.max_items, b.cb, s)
+                           : launch_forward(a, false, b.bounds, b.chunks, b.nb, b.istart, b.item_cnt, nullptr,
+                                            b.max_items, b.pin, b.pout, b.cb, s);
     if (e == hipSuccess) e = scan_exclusive_u32(b.item_cnt, b.item_off, b.max_items, &b.cb->n_pairs, b.scan_tmp, s);
     if (e == hipSuccess)
-      e = launch_forward(a, true, b.bounds, b.chunks, b.nb, b.istart, b.item_cnt, b.item_off, b.max_items, b.pin,
+      e = launch_forward(a, true, b.bounds, b.chunks, nb, b.istart, b.item_cnt, b.item_off, b.max_items, b.pin,
                          b.pout, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "forward search"));
   }
@@ -587,7 +613,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return bail(hip_fail(e, "count read-back"));
     if (hc->err & kErrDup) return bail(fail(SPCONV_EDUP, "duplicate coordinates"));
-    if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "work-item overflow in the balance step"));
+    if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "overflow of the work items or of the hash table"));
     if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "a look-back exceeded its wait bound"));
     if (hc->err & kErrUnsorted)
       return bail(fail(SPCONV_EINVAL, "rows declared presorted are not in ascending (b, x, y, z) order"));
@@ -602,7 +628,8 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   // T_q is indexed by sorted query position, T_s by sorted source position.
   // Inputs are the sources except for a direct UP map, whose inputs are the
   // queries; presorted rows are their own sorted positions.
-  const uint32_t* src_perm = tu.presorted ? nullptr : b.sidx;
+  // (hash-table maps index the inputs in caller order: no permutation)
+  const uint32_t* src_perm = (tu.presorted || tu.hash) ? nullptr : b.sidx;
   const uint32_t* q_perm = (mode == SPCONV_SUBM) ? src_perm
                            : (mode == SPCONV_DOWN ? nullptr : (tu.presorted ? nullptr : b.qrow));
   if (mode == SPCONV_UP) {

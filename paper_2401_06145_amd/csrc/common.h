@@ -75,11 +75,11 @@ struct ControlBlock {
 enum ProfId : int {
   // phases (host-visible steps, including the read-back synchronisations)
   PH_BOUNDS = 0, PH_SORT, PH_OUTCOORDS, PH_BACKWARD, PH_BALANCE, PH_FORWARD, PH_READBACK,
-  PH_METADATA, PH_GATHER, PH_GEMM, PH_SCATTER,
+  PH_METADATA, PH_GATHER, PH_GEMM, PH_SCATTER, PH_HASH,
   // kernels
   KN_MINMAX = 16, KN_RADIX_HIST, KN_RADIX_SCATTER, KN_SCAN, KN_COPY, KN_DOWN_KEYS, KN_UNIQUE,
   KN_BACKWARD, KN_FORWARD_COUNT, KN_FORWARD_WRITE, KN_FILL, KN_UNUSED_27, KN_GATHER, KN_GEMM, KN_SCATTER,
-  KN_PACK,
+  KN_PACK, KN_HASH_INSERT, KN_HASH_PROBE,
   PROF_IDS = 40
 };
 struct ProfScope {
@@ -158,6 +158,20 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
                           int64_t nb, const uint32_t* istart, uint32_t* item_cnt, const uint32_t* item_off,
                           int64_t max_items, int32_t* pin, int32_t* pout, ControlBlock* cb,
                           hipStream_t s);
+
+// Hash-table search (the prior-art Map, kept as an ablation): open addressing
+// with linear probing over 64-bit keys, 2^log2cap slots (load <= 1/2).
+constexpr uint64_t kHashEmpty = ~0ull;
+// Clears the table, packs every input row (caller order) into keys[i] with
+// idx[i] = i, and inserts (key, i); repeated keys set kErrDup in *err.
+hipError_t launch_hash_build(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* hkeys, uint32_t* hvals,
+                             int log2cap, uint64_t* keys, uint32_t* idx, uint32_t* err, hipStream_t s);
+// Work items of the probe: one query block of all n_q queries per offset
+// (bounds[k] = n_q, chunks[k] = its number of Cq chunks), i.e. one source block.
+hipError_t launch_hash_items(int K3, int64_t n_q, int Cq, uint32_t* bounds, uint32_t* chunks, hipStream_t s);
+// Probe pass: res[k][q] = matching input row or -1, item_cnt = matches per item.
+hipError_t launch_hash_count(const SearchArgs& a, const uint64_t* hkeys, const uint32_t* hvals, int log2cap,
+                             uint32_t* item_cnt, int64_t max_items, ControlBlock* cb, hipStream_t s);
 
 // gmas_kernels.hip.  Metadata tables are offset-major over sorted positions:
 // entry [k * stride + p] is the buffer row of point p's pair at offset k, or -1;

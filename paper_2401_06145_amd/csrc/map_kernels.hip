@@ -862,6 +862,109 @@ hipError_t forward_write_t(unsigned grid, hipStream_t s, const SearchArgs& a, co
   return hipGetLastError();
 }
 
+// ----------------------------------------------------------------------------
+// Hash-table search (the prior-art Map of Section 2.2, Step 1), kept as an
+// ablation of the sorted-array search.  Inputs are inserted in caller order into
+// an open-addressing table (linear probing, load <= 1/2); every (offset, output)
+// pair then probes it once.  Probe and insert walks are bounded by the table
+// size, so no wave loops forever.
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t hash_slot(uint64_t key, int log2cap) {
+  return (key * 0x9E3779B97F4A7C15ull) >> (64 - log2cap);
+}
+
+__global__ __launch_bounds__(kThreads) void k_hash_insert(const int4* c, int64_t n, KeyLayout L, uint64_t* hkeys,
+                                                          uint32_t* hvals, int log2cap, uint64_t* keys, uint32_t* idx,
+                                                          uint32_t* err) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int4 v = c[i];
+  const int32_t a[4] = {v.x, v.y, v.z, v.w};
+  const uint64_t key = pack_key(L, a);
+  keys[i] = key;
+  idx[i] = (uint32_t)i;
+  const uint64_t mask = (1ull << log2cap) - 1ull;
+  uint64_t slot = hash_slot(key, log2cap);
+  for (uint64_t step = 0; step <= mask; ++step) {
+    const unsigned long long prev =
+        atomicCAS(reinterpret_cast<unsigned long long*>(&hkeys[slot]), (unsigned long long)kHashEmpty,
+                  (unsigned long long)key);
+    if (prev == kHashEmpty) {
+      hvals[slot] = (uint32_t)i;
+      return;
+    }
+    if (prev == key) {  // a point cloud is a set
+      atomicOr(err, kErrDup);
+      return;
+    }
+    slot = (slot + 1) & mask;
+  }
+  atomicOr(err, kErrOverflow);  // table full: cannot happen at load 1/2
+}
+
+__global__ void k_hash_items(int K3, int64_t n_q, int Cq, uint32_t* bounds, uint32_t* chunks) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= K3) return;
+  bounds[k] = (uint32_t)n_q;
+  chunks[k] = (uint32_t)((n_q + Cq - 1) / Cq);
+}
+
+// One workgroup per work item (offset k, chunk c of Cq queries).
+template <int ROUNDS>
+__global__ __launch_bounds__(kThreads) void k_hash_count(SearchArgs a, const uint64_t* __restrict__ hkeys,
+                                                         const uint32_t* __restrict__ hvals, int log2cap,
+                                                         uint32_t* item_cnt, int64_t max_items, ControlBlock* cb) {
+  __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int64_t w = blockIdx.x;
+  const int64_t n_items = cb->n_items;
+  if (w >= n_items) {  // workgroup-uniform; idle items count zero matches
+    if (tid == 0 && w < max_items) item_cnt[w] = 0;
+    return;
+  }
+  const int64_t cpk = (a.n_q + a.Cq - 1) / a.Cq;  // chunks per offset
+  const int k = (int)(w / cpk);
+  const int64_t q0 = (w - (int64_t)k * cpk) * a.Cq;
+  const int64_t q1 = min(q0 + (int64_t)a.Cq, a.n_q);
+  const uint64_t dk = (uint64_t)a.dk[k];
+  const uint64_t mask = (1ull << log2cap) - 1ull;
+  int32_t* res = a.res + (int64_t)k * a.res_stride;
+#pragma unroll
+  for (int r = 0; r < ROUNDS; ++r) {
+    const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+    bool hit = false;
+    if (qp < q1) {
+      const uint64_t key = a.qkeys[qp] + dk;
+      uint64_t slot = hash_slot(key, log2cap);
+      int32_t found = -1;
+      for (uint64_t step = 0; step <= mask; ++step) {
+        const uint64_t kk = hkeys[slot];
+        if (kk == key) {
+          found = (int32_t)hvals[slot];
+          break;
+        }
+        if (kk == kHashEmpty) break;
+        slot = (slot + 1) & mask;
+      }
+      hit = found >= 0;
+      res[qp] = found;
+    }
+    const uint64_t bal = __ballot(hit);
+    if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t total = 0;
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r)
+#pragma unroll
+      for (int v = 0; v < kWavesPerBlock; ++v) total += s_cnt[r][v];
+    item_cnt[w] = total;
+  }
+}
+
 }  // namespace
 
 // ----------------------------------------------------------------------------
@@ -1108,6 +1211,44 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
     case 8: return forward_count_t<8>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_hash_build(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* hkeys, uint32_t* hvals,
+                             int log2cap, uint64_t* keys, uint32_t* idx, uint32_t* err, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(hkeys), 0xFFFFFFFFu, (int64_t)2 << log2cap, s);
+  if (e != hipSuccess) return e;
+  ProfScope ps(KN_HASH_INSERT, s);
+  hipLaunchKernelGGL(k_hash_insert, dim3(grid_for(n)), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(coords), n,
+                     L, hkeys, hvals, log2cap, keys, idx, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_hash_items(int K3, int64_t n_q, int Cq, uint32_t* bounds, uint32_t* chunks, hipStream_t s) {
+  hipLaunchKernelGGL(k_hash_items, dim3(1), dim3(128), 0, s, K3, n_q, Cq, bounds, chunks);
+  return hipGetLastError();
+}
+
+hipError_t launch_hash_count(const SearchArgs& a, const uint64_t* hkeys, const uint32_t* hvals, int log2cap,
+                             uint32_t* item_cnt, int64_t max_items, ControlBlock* cb, hipStream_t s) {
+  if (max_items <= 0) return hipSuccess;
+  ProfScope ps(KN_HASH_PROBE, s);
+  const unsigned grid = (unsigned)max_items;
+  switch (a.Cq / kThreads) {
+#define SPC_H(R)                                                                                                   \
+  case R:                                                                                                          \
+    hipLaunchKernelGGL((k_hash_count<R>), dim3(grid), dim3(kThreads), 0, s, a, hkeys, hvals, log2cap, item_cnt,   \
+                       max_items, cb);                                                                             \
+    break;
+    SPC_H(1)
+    SPC_H(2)
+    SPC_H(4)
+    SPC_H(8)
+#undef SPC_H
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace spc

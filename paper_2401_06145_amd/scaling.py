@@ -26,18 +26,19 @@ from paper_2401_06145_amd import scenes  # noqa: E402
 HBM_PEAK_GBS = 8000.0
 
 
-def measure(n: int, side: int, rounds: int, K: int = 3):
+def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = False):
     dev = torch.device("cuda:0")
     c = scenes.uniform_cells_large(n, side, 5000 + n % 997) if n > 1_000_000 else scenes.uniform_cells(n, side, 5000)
     coords = torch.from_numpy(c).to(dev)
-    ws = torch.empty(B.spconv_map_workspace_bytes(n, 0, K, B.SPCONV_SUBM), dtype=torch.uint8, device=dev)
+    opt = B.Options.make(search=1) if hash_search else None
+    ws = torch.empty(B.spconv_map_workspace_bytes(n, 0, K, B.SPCONV_SUBM, opt), dtype=torch.uint8, device=dev)
 
     def build():
-        h = B.spconv_build_map(coords, None, K, 1, 1, B.SPCONV_SUBM, None, ws)
+        h = B.spconv_build_map(coords, None, K, 1, 1, B.SPCONV_SUBM, opt, ws)
         B.spconv_free_map(h)
         return h
 
-    h = B.spconv_build_map(coords, None, K, 1, 1, B.SPCONV_SUBM, None, ws)
+    h = B.spconv_build_map(coords, None, K, 1, 1, B.SPCONV_SUBM, opt, ws)
     pairs = sum(B.spconv_map_counts(h))
     B.spconv_free_map(h)
     for _ in range(2):
@@ -57,7 +58,8 @@ def measure(n: int, side: int, rounds: int, K: int = 3):
     ph = timed(B.PHASES_ALL)
     phases = {k: v[0] / rounds for k, v in ph.items() if not k.startswith("k_") and v[1] > 0}
     kern = {}
-    for name in ("k_radix_scatter", "k_radix_hist", "k_backward", "k_forward_count", "k_forward_write"):
+    for name in ("k_radix_scatter", "k_radix_hist", "k_backward", "k_forward_count", "k_forward_write",
+                 "k_hash_insert", "k_hash_probe"):
         ms, cnt = timed(1 << ids[name])[name]
         if cnt:
             kern[name] = (ms / cnt, cnt / rounds)
@@ -74,7 +76,8 @@ def measure(n: int, side: int, rounds: int, K: int = 3):
         # query-side table's matches and the whole source-side table
         "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 12 * pairs + 4 * k3 * n,
     }
-    row = {"voxels": n, "grid": side, "pairs": pairs, "map_ms": round(map_ms, 4),
+    row = {"voxels": n, "grid": side, "search": "hash" if hash_search else "sorted", "pairs": pairs,
+           "map_ms": round(map_ms, 4),
            "phases_ms": {k: round(v, 4) for k, v in phases.items()},
            "map_gbps_compulsory": round(map_bytes / (map_ms * 1e-3) / 1e9, 1),
            "sort_gbps": round(28 * n / (sort_ms * 1e-3) / 1e9, 1) if sort_ms else None,
@@ -93,12 +96,15 @@ def main(argv=None):
     p.add_argument("--sizes", type=int, nargs="+",
                    default=[10_000, 100_000, 1_000_000, 2_000_000, 4_000_000, 8_000_000, 16_000_000])
     p.add_argument("--rounds", type=int, default=10)
+    p.add_argument("--search", choices=["sorted", "hash", "both"], default="both",
+                   help="sorted-array search (the method), hash-table search (ablation), or both")
     a = p.parse_args(argv)
     if not torch.cuda.is_available():
         raise SystemExit("the sweep needs a GPU")
     for n in a.sizes:
         side = 400 if n <= 1_000_000 else 800
-        print(json.dumps(measure(n, side, a.rounds)), flush=True)
+        for hs in ((False, True) if a.search == "both" else ((a.search == "hash"),)):
+            print(json.dumps(measure(n, side, a.rounds, hash_search=hs)), flush=True)
 
 
 if __name__ == "__main__":

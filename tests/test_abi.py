@@ -39,6 +39,10 @@ def test_workspace_bytes_host_only():
     assert B.spconv_map_workspace_bytes(10, 0, 3, 7) == 0                    # bad mode
     bad = B.Options.make(B=100)
     assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, bad) == 0
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(search=2)) == 0
+    # the hash-table search adds its table (2^11 slots of 12 bytes for 1000 inputs)
+    hashed = B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(search=1))
+    assert hashed >= B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM) + 2048 * 12
 
 
 @pytest.mark.parametrize("K,stride,mode,status", [

@@ -321,6 +321,48 @@ def test_error_duplicates_and_range():
     assert ei.value.status == B.SPCONV_ERANGE
 
 
+# ----------------------------------------------------------------------------
+# Hash-table search (the prior-art Map, an ablation of the sorted-array search)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("K", [1, 2, 3, 5])
+def test_hash_search_subm_small(K):
+    say(f"hash-table search K={K}")
+    c = _cloud(70 + K, 4000, -10, 10)
+    x = scenes.features(len(c), 16, "f32", 71)
+    w = scenes.weights(K, 16, 16, "f32", 72)
+    km, y = _conv_gpu(c, x, w, K, opt=B.Options.make(search=1, Cq=256))
+    okm = oracle.kernel_map(c, None, K, 1, "subm")
+    assert_map_equal(km, okm)
+    assert rel_err(to_f64(y), oracle.features(x, w, okm)) <= TOL["f32"]
+
+
+def test_hash_search_lidar_matches_sorted_search():
+    say("hash-table search on the 120k LiDAR layer")
+    wl = scenes.workload(1)
+    L = wl.layers[0]
+    x = scenes.features(len(wl.coords), L.c_in, L.dtype, 2001)
+    w = scenes.weights(L.K, L.c_in, L.c_out, L.dtype, 3001)
+    kh, yh = _conv_gpu(wl.coords, x, w, L.K, dtype=L.dtype, opt=B.Options.make(search=1))
+    ks, ys = _conv_gpu(wl.coords, x, w, L.K, dtype=L.dtype)
+    assert_map_equal(kh, oracle.kernel_map(wl.coords, None, L.K, 1, "subm"))
+    assert list(kh.counts()) == list(ks.counts())
+    # same pairs, summed in the same offset order: the outputs agree exactly
+    assert torch.equal(yh, ys)
+
+
+def test_hash_search_errors():
+    say("hash-table search errors")
+    dup = to_dev(np.array([[0, 1, 2, 3], [0, 5, 5, 5], [0, 1, 2, 3]], np.int32))
+    with pytest.raises(B.SpconvError) as ei:
+        B.KernelMap.build(dup, 3, opt=B.Options.make(search=1))
+    assert ei.value.status == B.SPCONV_EDUP
+    c = to_dev(_cloud(73, 200, -4, 4))
+    with pytest.raises(B.SpconvError) as ei:
+        B.KernelMap.build(c, 2, 2, 1, "down", opt=B.Options.make(search=1))
+    assert ei.value.status == B.SPCONV_EUNSUPPORTED
+
+
 def test_error_forward_args():
     say("forward argument errors")
     c = _cloud(50, 100, -3, 3)

@@ -37,7 +37,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", type=int, default=1, help="scene recipe (1 = LiDAR 120k, 3 = indoor 300k)")
+    p.add_argument("--workload", type=int, default=1,
+                   help="scene recipe (1 = LiDAR 120k, 3 = indoor 300k, 4 = UNet-style network on two LiDAR scenes)")
     p.add_argument("--channels", type=int, default=None, help="channel width for recipe 3")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--grouping", type=int, default=None)
@@ -129,6 +130,9 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
+    if args.workload == 4:
+        bench_network(args)
+        return
     import torch
 
     from paper_2401_06145_amd import binding as B
@@ -269,6 +273,57 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))
+
+
+def bench_network(args):
+    """One step = one forward of the UNet-style network on the two-scene batch (241,686
+    voxels at level 0, float16, 46 convolutions): every kernel map is built inside the
+    step (cached per coordinate set within the step, as the network reuses them), then
+    every layer runs.  Reports ms per forward and the time split by phase and kernel."""
+    import torch
+
+    from paper_2401_06145_amd import binding as B
+    from paper_2401_06145_amd import net, scenes
+
+    dev = torch.device("cuda:0")
+    wl = scenes.workload(4)
+    coords = torch.from_numpy(wl.coords).to(dev)
+    x0 = torch.from_numpy(scenes.features(len(wl.coords), net.STEM_C, "f16", 2004)).to(dev)
+    ops = net.unet_ops()
+    weights = net.UNet(coords).w  # device weights, built once (model parameters)
+
+    def step():
+        model = net.UNet(coords, ops=ops, weights=weights)
+        return model.forward(x0)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    B.spconv_profile_read(reset=True)
+    B.spconv_profile_enable(B.PHASES_ALL)
+    R = 3
+    for _ in range(R):
+        step()
+    torch.cuda.synchronize()
+    B.spconv_profile_enable(False)
+    prof = B.spconv_profile_read(reset=True)
+    ph_ms = {k: v[0] / R for k, v in prof.items() if not k.startswith("k_") and v[1] > 0}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    n_conv = sum(1 for o in ops if o.kind == "conv")
+    print(json.dumps({
+        "metric": "UNet-style network forward ms (maps built inside the step)", "value": round(ms, 4), "unit": "ms",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "config": {"workload": wl.name, "voxels": len(wl.coords), "convolutions": n_conv},
+        "map_ms": round(sum(ph_ms.get(p, 0.0) for p in MAP_PHASES), 4),
+        "gmas_ms": round(sum(ph_ms.get(p, 0.0) for p in GMAS_PHASES), 4),
+        "phases_ms": {k: round(v, 4) for k, v in ph_ms.items()},
+        "roofline": None, "cpu_baseline": None}))
 
 
 def cpu_baseline(coords, x, w, L):

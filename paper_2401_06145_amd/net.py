@@ -1,9 +1,10 @@
-"""A UNet-style sparse network built from the library's layers (the paper's
-networks, Section 6.1, are of this kind; this one follows the recipe used as a
-parity workload: two LiDAR-like scenes in one batch, float16).
+"""Sparse networks built from the library's layers (the paper's networks,
+Section 6.1, are of these kinds): a UNet-style network (the recipe used as a
+parity workload: two LiDAR-like scenes in one batch, float16) and a
+SparseResNet21-style encoder with odd-K strided downsampling.
 
-Wiring (channels C_in -> C_out; every conv is followed by ReLU, except the last
-conv of a residual block, where ReLU follows the add):
+UNet wiring (channels C_in -> C_out; every conv is followed by ReLU, except the
+last conv of a residual block, where ReLU follows the add):
   stem      two submanifold K=3 convs at level 0, 32 -> 32 -> 32
   encoder   4 stages (levels 1..4): K=2 s=2 downsample C_prev -> C, then two
             residual blocks of two K=3 convs; C = 32, 64, 128, 256
@@ -85,14 +86,41 @@ def unet_ops(weight_seed: int = 30_000) -> list[Op]:
     return ops
 
 
+RES_C = (32, 64, 128, 256)
+
+
+def resnet_ops(weight_seed: int = 40_000) -> list[Op]:
+    """A SparseResNet21-style encoder (the paper's other network family, Section 6.1):
+    a submanifold K=3 stem (32 -> 32), then 4 stages of a K=3 stride-2 convolution
+    (odd-K strided downsampling; C_prev -> C) and two basic residual blocks of two K=3
+    convolutions each, C = 32, 64, 128, 256: 21 convolutions."""
+    ops: list[Op] = []
+
+    def conv(out, inp, level, K, mode, c_in, c_out, relu=True, residual=None):
+        ops.append(Op("conv", out, inp, level, K, mode, c_in, c_out, relu, residual, seed=weight_seed + len(ops)))
+
+    conv("stem", "x0", 0, 3, "subm", STEM_C, RES_C[0])
+    prev, c_prev = "stem", RES_C[0]
+    for i, c in enumerate(RES_C, start=1):
+        conv(f"s{i}_d", prev, i - 1, 3, "down", c_prev, c)
+        cur = f"s{i}_d"
+        for r in range(2):
+            conv(f"s{i}_b{r}_h", cur, i, 3, "subm", c, c)
+            conv(f"s{i}_b{r}", f"s{i}_b{r}_h", i, 3, "subm", c, c, relu=True, residual=cur)
+            cur = f"s{i}_b{r}"
+        prev, c_prev = cur, c
+    return ops
+
+
 def weights_for(op: Op, dtype: str = "f16") -> np.ndarray:
     return scenes.weights(op.K, op.c_in, op.c_out, dtype, op.seed)
 
 
-class UNet:
-    """GPU runner: builds and caches the kernel maps, then runs the op list."""
+class Network:
+    """GPU runner of an op list: builds and caches the kernel maps, then runs the ops."""
 
-    def __init__(self, coords: torch.Tensor, dtype: torch.dtype = torch.float16, ops: list[Op] | None = None):
+    def __init__(self, coords: torch.Tensor, dtype: torch.dtype = torch.float16, ops: list[Op] | None = None,
+                 weights: dict | None = None):
         self.dev = coords.device
         self.dtype = dtype
         self.ops = ops or unet_ops()
@@ -100,8 +128,8 @@ class UNet:
         self.maps: dict = {}
         self.fwd: dict = {}
         dname = {torch.float16: "f16", torch.bfloat16: "bf16", torch.float32: "f32"}[dtype]
-        self.w = {}
-        for op in self.ops:
+        self.w = weights if weights is not None else {}
+        for op in self.ops if weights is None else []:
             if op.kind == "conv":
                 w = weights_for(op, dname)
                 t = torch.from_numpy(w.view(np.int16) if dname == "bf16" else w)
@@ -150,3 +178,6 @@ class UNet:
                 res = t[op.residual] if op.residual else None
                 t[op.out] = self.fwd[key](t[op.inp], self.w[op.out], residual=res, relu=op.relu)
         return t if keep else {"out": t[self.ops[-1].out]}
+
+
+UNet = Network  # the default op list is the UNet above

@@ -16,7 +16,7 @@
 // Group padding rows (segment height > rows) are fed as zeros: they cost MFMA
 // cycles, like the zero-padded batched GEMMs of the paper, but no memory traffic.
 //
-// Two kernels.  k_gemm_wide (f16 / bf16, c_in <= 256) gives a workgroup the full
+// Two kernels.  k_gemm_wide (f16 / bf16, c_in <= 512) gives a workgroup the full
 // output width whenever W_k^T fits the 160 KiB of LDS, so every buf_in row is
 // read from HBM once; it stages W_k^T from a transposed copy of the weights
 // with 16-byte copies, and each wave loads the next 16-row block of buf_in while
@@ -297,13 +297,16 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   }
 }
 
-// k-steps instantiated for the wide kernel (c_in up to 256); others round up
+// k-steps instantiated for the wide kernel (c_in up to 512); others round up
 int wide_ksteps(int c_in) {
   const int ks = (c_in + 31) / 32;
-  for (int c : {1, 2, 3, 4, 6, 8})
+  for (int c : {1, 2, 3, 4, 6, 8, 12, 16})
     if (ks <= c) return c;
   return 0;
 }
+
+// Instantiated (NT, KSTEPS) pairs: the W^T slice fits the LDS.
+constexpr bool wide_fits(int nt, int ks) { return (size_t)16 * nt * (32 * ks + 8) * 2 <= kLdsMax; }
 
 // Column tiles per workgroup for the wide kernel: the widest instantiated divisor
 // of c_out / 16 whose W^T slice fits the LDS; 0 if the wide kernel does not apply.
@@ -326,9 +329,12 @@ int wide_round_rows(int nt, int ks) {
 
 template <typename T, typename TO>
 const void* wide_kernel(int nt, int ks) {
-#define SPC_W(N, KS_) \
-  if (nt == N && ks == KS_) return reinterpret_cast<const void*>(&k_gemm_wide<T, TO, N, KS_>);
-#define SPC_WK(N) SPC_W(N, 1) SPC_W(N, 2) SPC_W(N, 3) SPC_W(N, 4) SPC_W(N, 6) SPC_W(N, 8)
+#define SPC_W(N, KS_)                                                                   \
+  if constexpr (wide_fits(N, KS_)) {                                                     \
+    if (nt == N && ks == KS_) return reinterpret_cast<const void*>(&k_gemm_wide<T, TO, N, KS_>); \
+  }
+#define SPC_WK(N) \
+  SPC_W(N, 1) SPC_W(N, 2) SPC_W(N, 3) SPC_W(N, 4) SPC_W(N, 6) SPC_W(N, 8) SPC_W(N, 12) SPC_W(N, 16)
   SPC_WK(1) SPC_WK(2) SPC_WK(3) SPC_WK(4) SPC_WK(6) SPC_WK(8) SPC_WK(12) SPC_WK(16)
 #undef SPC_WK
 #undef SPC_W

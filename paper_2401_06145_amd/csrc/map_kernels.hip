@@ -139,8 +139,10 @@ __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, Key
 // there, so that consecutive threads write consecutive addresses of a digit's
 // run.
 // ----------------------------------------------------------------------------
-constexpr int kRsItems = 8;
+constexpr int kRsItems = 8;                   // keys per thread of a one-kernel pass
 constexpr int kRsTile = kThreads * kRsItems;
+constexpr int kRsItemsSmall = 4;              // keys per thread of the small sorts' passes
+constexpr int kRsTileSmall = kThreads * kRsItemsSmall;
 constexpr int kRsUpBlocks = 512;
 constexpr int kRsMaxPasses = 8;
 constexpr uint32_t kStAgg = 1u << 30;   // word holds this tile's count of the digit
@@ -201,10 +203,11 @@ __device__ __forceinline__ uint32_t block_excl256(uint32_t v, uint32_t* s_wave) 
   return e;
 }
 
-// LDS of one tile scatter.
+// LDS of one tile scatter of ITEMS keys per thread.
+template <int ITEMS>
 struct TileLds {
-  uint64_t key[kRsTile];
-  uint32_t val[kRsTile];
+  uint64_t key[kThreads * ITEMS];
+  uint32_t val[kThreads * ITEMS];
   uint32_t ldig[256];   // tile-local first position of each digit
   uint32_t gbase[256];  // global position of the tile's first key of each digit
   uint32_t cnt[256];    // the tile's count of each digit
@@ -212,20 +215,20 @@ struct TileLds {
   uint32_t s_wave[kWavesPerBlock];
 };
 
-// Tile layout: wave w holds keys base + w * kRsWaveKeys + r * 64 + lane, r < kRsItems,
-// so each wave owns a contiguous run of the tile and can rank it on its own.
-constexpr int kRsWaveKeys = kWave * kRsItems;
+// Tile layout: wave w holds keys base + w * 64 ITEMS + r * 64 + lane, r < ITEMS, so
+// each wave owns a contiguous run of the tile and can rank it on its own.
+template <int ITEMS>
 __device__ __forceinline__ int64_t tile_index(int64_t base, int r) {
-  return base + (int64_t)(threadIdx.x / kWave) * kRsWaveKeys + (int64_t)r * kWave + (threadIdx.x & (kWave - 1));
+  return base + (int64_t)(threadIdx.x / kWave) * (kWave * ITEMS) + (int64_t)r * kWave + (threadIdx.x & (kWave - 1));
 }
 
-template <bool FROM_COORDS>
+template <bool FROM_COORDS, int ITEMS>
 __device__ __forceinline__ void tile_load(const uint64_t* kin, const uint32_t* vin, const int4* coords,
-                                          const KeyLayout& L, int64_t base, int64_t n, uint64_t key[kRsItems],
-                                          uint32_t val[kRsItems]) {
+                                          const KeyLayout& L, int64_t base, int64_t n, uint64_t key[ITEMS],
+                                          uint32_t val[ITEMS]) {
 #pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
-    const int64_t i = tile_index(base, r);
+  for (int r = 0; r < ITEMS; ++r) {
+    const int64_t i = tile_index<ITEMS>(base, r);
     key[r] = 0;
     val[r] = 0;
     if (i < n) {
@@ -239,12 +242,13 @@ __device__ __forceinline__ void tile_load(const uint64_t* kin, const uint32_t* v
 // wave with the same digit.  Leaves the wave's digit counts in t.wc[wave] (which
 // must be zero).  No workgroup barrier: a wave's LDS accesses complete in order,
 // so every lane reads a counter before its digit's leader bumps it.
-__device__ __forceinline__ void tile_rank(TileLds& t, const uint64_t key[kRsItems], int64_t base, int64_t n,
-                                          int shift, uint32_t rank[kRsItems]) {
+template <int ITEMS>
+__device__ __forceinline__ void tile_rank(TileLds<ITEMS>& t, const uint64_t key[ITEMS], int64_t base, int64_t n,
+                                          int shift, uint32_t rank[ITEMS]) {
   const int wave = threadIdx.x / kWave;
 #pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
-    const bool valid = tile_index(base, r) < n;
+  for (int r = 0; r < ITEMS; ++r) {
+    const bool valid = tile_index<ITEMS>(base, r) < n;
     const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
     const uint64_t peers = match_digit(d, valid);
     rank[r] = 0;
@@ -262,9 +266,9 @@ __device__ __forceinline__ void tile_rank(TileLds& t, const uint64_t key[kRsItem
 // store consecutive positions of a digit's run (pays off once the sort is
 // bandwidth-bound).  Otherwise each key is stored at its global position
 // straight away (fewer steps, for small latency-bound sorts).
-template <bool STAGED>
-__device__ __forceinline__ void tile_place(TileLds& t, const uint64_t key[kRsItems], const uint32_t val[kRsItems],
-                                           const uint32_t rank[kRsItems], int64_t base, int64_t n, int shift,
+template <bool STAGED, int ITEMS>
+__device__ __forceinline__ void tile_place(TileLds<ITEMS>& t, const uint64_t key[ITEMS], const uint32_t val[ITEMS],
+                                           const uint32_t rank[ITEMS], int64_t base, int64_t n, int shift,
                                            uint64_t* kout, uint32_t* vout) {
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
@@ -284,8 +288,8 @@ __device__ __forceinline__ void tile_place(TileLds& t, const uint64_t key[kRsIte
   }
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
-    if (tile_index(base, r) < n) {
+  for (int r = 0; r < ITEMS; ++r) {
+    if (tile_index<ITEMS>(base, r) < n) {
       const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
       const uint32_t pos = t.wc[wave][d] + rank[r];
       if (STAGED) {
@@ -299,7 +303,7 @@ __device__ __forceinline__ void tile_place(TileLds& t, const uint64_t key[kRsIte
   }
   if (!STAGED) return;
   __syncthreads();
-  const int tile_n = (int)min((int64_t)kRsTile, n - base);
+  const int tile_n = (int)min((int64_t)(kThreads * ITEMS), n - base);
   for (int i = tid; i < tile_n; i += kThreads) {
     const uint64_t k = t.key[i];
     const uint32_t d = (uint32_t)(k >> shift) & 255u;
@@ -370,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
                                                          KeyLayout L, uint64_t* kout, uint32_t* vout, int64_t n,
                                                          int pass, const uint32_t* gofs, uint32_t* status,
                                                          uint32_t* tickets, uint32_t* err) {
-  __shared__ TileLds t;
+  __shared__ TileLds<kRsItems> t;
   __shared__ uint32_t s_tile;
   const int tid = threadIdx.x;
   const int shift = 8 * pass;
@@ -384,8 +388,8 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
   uint64_t key[kRsItems];
   uint32_t val[kRsItems];
   uint32_t rank[kRsItems];
-  tile_load<FROM_COORDS>(kin, vin, coords, L, base, n, key, val);
-  tile_rank(t, key, base, n, shift, rank);
+  tile_load<FROM_COORDS, kRsItems>(kin, vin, coords, L, base, n, key, val);
+  tile_rank<kRsItems>(t, key, base, n, shift, rank);
   __syncthreads();
 
   // publish this tile's count of digit `tid` and look back over earlier tiles
@@ -433,7 +437,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
   }
   t.gbase[tid] = gofs[pass * 256 + tid] + excl;
   __syncthreads();
-  tile_place<true>(t, key, val, rank, base, n, shift, kout, vout);
+  tile_place<true, kRsItems>(t, key, val, rank, base, n, shift, kout, vout);
 }
 
 // Small inputs (few tiles): per-tile digit histograms, then a stable scatter.
@@ -445,15 +449,15 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
 // histograms gives the offsets (three launches).
 constexpr int64_t kFusedScanTiles = 256;
 
-template <bool FROM_COORDS, bool TILE_MAJOR>
+template <bool FROM_COORDS, bool TILE_MAJOR, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, KeyLayout L,
                                                          int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kRsTile;
+  const int64_t base = (int64_t)blockIdx.x * (kThreads * ITEMS);
 #pragma unroll
-  for (int r = 0; r < kRsItems; ++r) {
+  for (int r = 0; r < ITEMS; ++r) {
     const int64_t i = base + r * kThreads + threadIdx.x;
     if (i < n) {
       const uint32_t d = (uint32_t)(load_key<FROM_COORDS>(keys, coords, L, i) >> shift) & 255u;
@@ -471,22 +475,22 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
 // FUSED: `offs` holds tile-major histograms; the first position of digit d in
 // this tile is (keys of smaller digits) + (keys of digit d in earlier tiles).
 // Otherwise `offs` is the scanned digit-major histogram.
-template <bool FROM_COORDS, bool FUSED>
+template <bool FROM_COORDS, bool FUSED, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t* kin, const uint32_t* vin,
                                                             const int4* coords, KeyLayout L, uint64_t* kout,
                                                             uint32_t* vout, int64_t n, int shift,
                                                             const uint32_t* offs, int64_t ntiles) {
-  __shared__ TileLds t;
+  __shared__ TileLds<ITEMS> t;
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
-  const int64_t base = (int64_t)blockIdx.x * kRsTile;
+  const int64_t base = (int64_t)blockIdx.x * (kThreads * ITEMS);
 #pragma unroll
   for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
   // the tile's keys are loaded first, so that their latency overlaps the offset sums
-  uint64_t key[kRsItems];
-  uint32_t val[kRsItems];
-  uint32_t rank[kRsItems];
-  tile_load<FROM_COORDS>(kin, vin, coords, L, base, n, key, val);
+  uint64_t key[ITEMS];
+  uint32_t val[ITEMS];
+  uint32_t rank[ITEMS];
+  tile_load<FROM_COORDS, ITEMS>(kin, vin, coords, L, base, n, key, val);
   if (FUSED) {
     // wave v sums tiles v, v + 4, ...; lane l covers digits 4l..4l+3 with 16-byte loads,
     // so all of a wave's loads are independent and in flight together
@@ -529,9 +533,9 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
     t.gbase[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
   }
   __syncthreads();  // wc cleared
-  tile_rank(t, key, base, n, shift, rank);
+  tile_rank<ITEMS>(t, key, base, n, shift, rank);
   __syncthreads();
-  tile_place<false>(t, key, val, rank, base, n, shift, kout, vout);
+  tile_place<false, ITEMS>(t, key, val, rank, base, n, shift, kout, vout);
 }
 
 // ----------------------------------------------------------------------------
@@ -1011,15 +1015,22 @@ size_t radix_temp_bytes(int64_t n) {
   const size_t gofs = (size_t)kRsMaxPasses * 256 * sizeof(uint32_t);
   const size_t status = (size_t)kRsMaxPasses * ntiles * 256 * sizeof(uint32_t);
   const size_t onesweep = align256(gpart) + align256(gofs) + align256(status) + 256;
-  const size_t tiled = align256((size_t)256 * ntiles * sizeof(uint32_t)) + scan_temp_bytes(256 * ntiles);
+  // the small sorts use tiles of kRsTileSmall keys when that keeps their offsets fused
+  const int64_t tiles_small = std::max<int64_t>(1, (n + kRsTileSmall - 1) / kRsTileSmall);
+  const int64_t tiles_tiled = std::max(ntiles, tiles_small);
+  const size_t tiled = align256((size_t)256 * tiles_tiled * sizeof(uint32_t)) + scan_temp_bytes(256 * tiles_tiled);
   return std::max(onesweep, tiled);
 }
 
 namespace {
-// Small inputs: three launches per pass (tile histograms, scan, scatter).
-hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
-                            uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
-  const int64_t ntiles = (n + kRsTile - 1) / kRsTile;
+// Small inputs: tile histograms, then the scatter (with a device scan between
+// them once there are too many tiles to sum in each workgroup).  ITEMS keys per
+// thread: smaller tiles shorten each workgroup's chain while the launch is
+// latency-bound.
+template <int ITEMS>
+hipError_t radix_sort_tiled_t(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+                              uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
+  const int64_t ntiles = (n + kThreads * ITEMS - 1) / (kThreads * ITEMS);
   uint32_t* hist = static_cast<uint32_t*>(d_temp);
   void* scan_tmp = static_cast<char*>(d_temp) + align256((size_t)256 * ntiles * sizeof(uint32_t));
   const int4* c4 = reinterpret_cast<const int4*>(coords);
@@ -1042,7 +1053,7 @@ hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, 
     {
       ProfScope ps(KN_RADIX_HIST, s);
 #define SPC_H(FC, TM)                                                                                           \
-  hipLaunchKernelGGL((k_radix_tile_hist<FC, TM>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],      \
+  hipLaunchKernelGGL((k_radix_tile_hist<FC, TM, ITEMS>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],      \
                      FC ? c4 : nullptr, L, n, shift, hist, ntiles)
       if (first) {
         if (fused) SPC_H(true, true); else SPC_H(true, false);
@@ -1060,7 +1071,7 @@ hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, 
     {
       ProfScope ps(KN_RADIX_SCATTER, s);
 #define SPC_S(FC, FU)                                                                                           \
-  hipLaunchKernelGGL((k_radix_tile_scatter<FC, FU>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],   \
+  hipLaunchKernelGGL((k_radix_tile_scatter<FC, FU, ITEMS>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],   \
                      FC ? nullptr : vb[src], FC ? c4 : nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles)
       if (first) {
         if (fused) SPC_S(true, true); else SPC_S(true, false);
@@ -1075,6 +1086,14 @@ hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, 
   }
   return hipSuccess;
 }
+
+hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+                            uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
+  if ((n + kRsTileSmall - 1) / kRsTileSmall <= kFusedScanTiles)
+    return radix_sort_tiled_t<kRsItemsSmall>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
+  return radix_sort_tiled_t<kRsItems>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
+}
+
 }  // namespace
 
 hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,

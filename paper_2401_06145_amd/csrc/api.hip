@@ -518,14 +518,19 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   KeyLayout L;
   {
     PhaseScope ph(PH_BOUNDS, s);
+    int np = 0;
     hipError_t e = launch_minmax(d_in_coords, n_in, d_out_coords, mode == SPCONV_UP ? n_out : 0, b.mm_partial,
-                                 b.cb, s);
-    ControlBlock* h = static_cast<ControlBlock*>(staging(65536));
+                                 b.cb, &np, s);
+    int32_t* h = static_cast<int32_t*>(staging(65536));
     if (!h) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
-    if (e == hipSuccess) e = hipMemcpyAsync(h, b.cb, sizeof(ControlBlock), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(h, b.mm_partial, (size_t)np * 8 * sizeof(int32_t), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return bail(hip_fail(e, "coordinate bounds"));
-    if ((st = make_layout(h->minmax, h->minmax + 4, K, stride, tensor_stride, &L)) != SPCONV_OK) return bail(st);
+    int32_t mm[8];
+    for (int f = 0; f < 8; ++f) mm[f] = h[f];
+    for (int i = 1; i < np; ++i)
+      for (int f = 0; f < 8; ++f) mm[f] = (f < 4) ? std::min(mm[f], h[i * 8 + f]) : std::max(mm[f], h[i * 8 + f]);
+    if ((st = make_layout(mm, mm + 4, K, stride, tensor_stride, &L)) != SPCONV_OK) return bail(st);
   }
   if (tu.hash) {
     PhaseScope ph(PH_HASH, s);

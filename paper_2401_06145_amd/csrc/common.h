@@ -60,7 +60,6 @@ enum : uint32_t {
 // Small control block in device memory, read back once at the end of a map build.
 constexpr int kMaxOffsets = 125;  // K <= 5
 struct ControlBlock {
-  int32_t minmax[8];      // min b,x,y,z then max b,x,y,z (coordinate bounds pass)
   uint32_t err;           // kErr* flags
   uint32_t n_q;           // number of distinct output coordinates (DOWN)
   uint32_t n_items;       // forward-search work items of the balance step
@@ -100,9 +99,10 @@ hipError_t scan_exclusive_u32(const uint32_t* d_in, uint32_t* d_out, int64_t n, 
 // map_kernels.hip
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
 size_t minmax_temp_bytes();
-// Coordinate bounds of a[0..na) and b[0..nb) into cb->minmax; also resets cb.
+// Per-block coordinate bounds of a[0..na) and b[0..nb): *n_partial rows of 8
+// int32 (min b,x,y,z then max b,x,y,z) in `partial`; also resets cb's counters.
 hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t nb, int32_t* partial,
-                         ControlBlock* cb, hipStream_t s);
+                         ControlBlock* cb, int* n_partial, hipStream_t s);
 hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals,
                        hipStream_t s);
 size_t radix_temp_bytes(int64_t n);

@@ -34,8 +34,17 @@ unsigned grid_for(int64_t n, int per_block = kThreads, int64_t cap = 1 << 20) {
 // ----------------------------------------------------------------------------
 constexpr int kMinmaxBlocks = 256;
 
+// Per-block bounds of the coordinates; the host reduces the partials (it has to
+// wait for them anyway, to lay out the keys).  Block 0 also resets the control
+// block's counters for this build.
 __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int64_t na, const int4* b, int64_t nb,
-                                                             int32_t* partial) {
+                                                             int32_t* partial, ControlBlock* cb) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    cb->err = 0;
+    cb->n_q = 0;
+    cb->n_items = 0;
+    cb->n_pairs = 0;
+  }
   int32_t mn[4] = {INT_MAX, INT_MAX, INT_MAX, INT_MAX};
   int32_t mx[4] = {INT_MIN, INT_MIN, INT_MIN, INT_MIN};
   const int64_t n = na + nb;
@@ -74,43 +83,6 @@ __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int6
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_minmax_final(const int32_t* partial, int nblocks, ControlBlock* cb) {
-  // one partial per thread (nblocks <= kMinmaxBlocks == kThreads), then wave and block reduce
-  int32_t r[8];
-#pragma unroll
-  for (int f = 0; f < 8; ++f) r[f] = (f < 4) ? INT_MAX : INT_MIN;
-  if ((int)threadIdx.x < nblocks) {
-#pragma unroll
-    for (int f = 0; f < 8; ++f) r[f] = partial[threadIdx.x * 8 + f];
-  }
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) {
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      const int32_t o = __shfl_xor(r[f], off, kWave);
-      r[f] = (f < 4) ? min(r[f], o) : max(r[f], o);
-    }
-  }
-  __shared__ int32_t s[kWavesPerBlock][8];
-  const int wave = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) {
-#pragma unroll
-    for (int f = 0; f < 8; ++f) s[wave][f] = r[f];
-  }
-  __syncthreads();
-  const int f = threadIdx.x;
-  if (f < 8) {
-    int32_t v = s[0][f];
-    for (int w = 1; w < kWavesPerBlock; ++w) v = (f < 4) ? min(v, s[w][f]) : max(v, s[w][f]);
-    cb->minmax[f] = v;
-  }
-  if (f == 0) {
-    cb->err = 0;
-    cb->n_q = 0;
-    cb->n_items = 0;
-    cb->n_pairs = 0;
-  }
-}
 
 // ----------------------------------------------------------------------------
 // Key packing helpers
@@ -602,6 +574,36 @@ __device__ __forceinline__ int64_t wave_upper_bound(const T* a, int64_t n, V thr
   return lo + popc64(__ballot(pred));
 }
 
+// Two such searches of the same array in lock step (two independent loads per
+// lane and round), so that they cost the latency of one.
+template <typename T, typename V>
+__device__ __forceinline__ void wave_upper_bound2(const T* a, int64_t n, V thr1, V thr2, int64_t* r1, int64_t* r2) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int64_t lo1 = 0, hi1 = n, lo2 = 0, hi2 = n;
+  while (hi1 - lo1 > kWave || hi2 - lo2 > kWave) {
+    const int64_t st1 = (hi1 - lo1 + kWave - 1) / kWave, st2 = (hi2 - lo2 + kWave - 1) / kWave;
+    const int64_t p1 = lo1 + (int64_t)(lane + 1) * st1 - 1, p2 = lo2 + (int64_t)(lane + 1) * st2 - 1;
+    const bool a1 = hi1 - lo1 > kWave && p1 < hi1 && (V)a[p1] <= thr1;
+    const bool a2 = hi2 - lo2 > kWave && p2 < hi2 && (V)a[p2] <= thr2;
+    const int c1 = popc64(__ballot(a1)), c2 = popc64(__ballot(a2));
+    if (hi1 - lo1 > kWave) {
+      const int64_t nlo = lo1 + (int64_t)c1 * st1;
+      hi1 = min(lo1 + (int64_t)(c1 + 1) * st1 - 1, hi1);
+      lo1 = nlo;
+    }
+    if (hi2 - lo2 > kWave) {
+      const int64_t nlo = lo2 + (int64_t)c2 * st2;
+      hi2 = min(lo2 + (int64_t)(c2 + 1) * st2 - 1, hi2);
+      lo2 = nlo;
+    }
+  }
+  const int64_t q1 = lo1 + lane, q2 = lo2 + lane;
+  const bool b1 = q1 < hi1 && (V)a[q1] <= thr1;
+  const bool b2 = q2 < hi2 && (V)a[q2] <= thr2;
+  *r1 = lo1 + popc64(__ballot(b1));
+  *r2 = lo2 + popc64(__ballot(b2));
+}
+
 // ----------------------------------------------------------------------------
 // Backward binary search (Section 5.1.2) fused with the balancing count.  For
 // source block b and offset k the query block is the run of sorted queries q
@@ -610,8 +612,9 @@ __device__ __forceinline__ int64_t wave_upper_bound(const T* a, int64_t n, V thr
 // and the same for pivot_{b-1}, and writes the number of <= Cq chunks the
 // query block splits into.  The last block also takes the queries beyond its
 // pivot (they all miss), so that every (offset, query) pair is searched once and
-// the per-query tables come out complete.  The k = 0 waves also check the
-// sorted keys for repeats (a point cloud is a set).
+// the per-query tables come out complete.  For transposed maps the k = 0 waves
+// also check the sorted query keys for repeats (a point cloud is a set); the
+// count pass checks the source keys in LDS.
 // ----------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb, uint32_t* bounds, uint32_t* chunks,
                                                        ControlBlock* cb) {
@@ -624,32 +627,27 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
   const int64_t dk = a.dk[k];
   // key(q) + dk <= pivot  <=>  key(q) <= pivot - dk, evaluated in signed 64 bits
   const int64_t last = min((b + 1) * (int64_t)a.B, a.n_src) - 1;
-  const int64_t hi =
-      (b == nb - 1) ? nq : wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, (int64_t)a.skeys[last] - dk);
-  const int64_t lo = (b == 0) ? 0 : wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, (int64_t)a.skeys[b * a.B - 1] - dk);
+  // hi: the last block also takes every query past its pivot; lo: none before block 0
+  // (a bound without a neighbouring pivot uses a threshold that every key, or no
+  // key, passes)
+  const int64_t thr_hi = (b == nb - 1) ? INT64_MAX : (int64_t)a.skeys[last] - dk;
+  const int64_t thr_lo = (b == 0) ? INT64_MIN : (int64_t)a.skeys[b * a.B - 1] - dk;
+  int64_t hi, lo;
+  wave_upper_bound2<uint64_t, int64_t>(a.qkeys, nq, thr_hi, thr_lo, &hi, &lo);
   if (lane == 0) {
     bounds[wid] = (uint32_t)hi;
     chunks[wid] = (uint32_t)((hi - lo + a.Cq - 1) / a.Cq);
   }
-  if (k == 0) {
-    // the source (and, for transposed maps, query) keys must be strictly increasing:
-    // equal neighbours are repeated coordinates, decreasing ones an unsorted input
-    // that was declared sorted
+  if (k == 0 && a.check_q) {
+    // the query keys of a transposed map (the coarse inputs) must be strictly
+    // increasing too; the count pass checks the source keys
     bool dup = false, unsorted = false;
-    const int64_t s0 = b * (int64_t)a.B;
-    for (int64_t e = s0 + lane; e <= last; e += kWave)
+    const int64_t per = (nq + nb - 1) / nb;
+    for (int64_t e = b * per + lane; e < min((b + 1) * per, nq); e += kWave)
       if (e > 0) {
-        dup |= a.skeys[e] == a.skeys[e - 1];
-        unsorted |= a.skeys[e] < a.skeys[e - 1];
+        dup |= a.qkeys[e] == a.qkeys[e - 1];
+        unsorted |= a.qkeys[e] < a.qkeys[e - 1];
       }
-    if (a.check_q) {
-      const int64_t per = (nq + nb - 1) / nb;
-      for (int64_t e = b * per + lane; e < min((b + 1) * per, nq); e += kWave)
-        if (e > 0) {
-          dup |= a.qkeys[e] == a.qkeys[e - 1];
-          unsorted |= a.qkeys[e] < a.qkeys[e - 1];
-        }
-    }
     if (__ballot(dup) != 0 && lane == 0) atomicOr(&cb->err, kErrDup);
     if (__ballot(unsorted) != 0 && lane == 0) atomicOr(&cb->err, kErrUnsorted);
   }
@@ -808,6 +806,20 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
   const int nB = (int)min((int64_t)a.B, a.n_src - s0);
   for (int e = tid; e < nB; e += kThreads) lkey[e] = a.skeys[s0 + e];
   __syncthreads();
+  if (g == 0) {
+    // the sorted source keys must be strictly increasing: equal neighbours are
+    // repeated coordinates, decreasing ones an unsorted input declared sorted
+    bool dup = false, unsorted = false;
+    for (int e = tid; e < nB; e += kThreads) {
+      const uint64_t prev = (e > 0) ? lkey[e - 1] : (s0 > 0 ? a.skeys[s0 - 1] : 0ull);
+      if (e > 0 || s0 > 0) {
+        dup |= lkey[e] == prev;
+        unsorted |= lkey[e] < prev;
+      }
+    }
+    if (__ballot(dup) != 0 && lane == 0) atomicOr(&cb->err, kErrDup);
+    if (__ballot(unsorted) != 0 && lane == 0) atomicOr(&cb->err, kErrUnsorted);
+  }
 
   const int k_end = min(a.K3, (g + 1) * G);
   for (int k = g * G; k < k_end; ++k) {
@@ -984,14 +996,12 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
 size_t minmax_temp_bytes() { return (size_t)kMinmaxBlocks * 8 * sizeof(int32_t); }
 
 hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t nb, int32_t* partial,
-                         ControlBlock* cb, hipStream_t s) {
+                         ControlBlock* cb, int* n_partial, hipStream_t s) {
   ProfScope ps(KN_MINMAX, s);
   const unsigned g = grid_for(na + nb, kThreads * 8, kMinmaxBlocks);
+  *n_partial = (int)g;
   hipLaunchKernelGGL(k_minmax_partial, dim3(g), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(a), na,
-                     reinterpret_cast<const int4*>(b), nb, partial);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_minmax_final, dim3(1), dim3(kThreads), 0, s, partial, (int)g, cb);
+                     reinterpret_cast<const int4*>(b), nb, partial, cb);
   return hipGetLastError();
 }
 

@@ -3,8 +3,10 @@
 A step runs the whole hot path on one seeded LiDAR-like scene (about 120k voxels,
 submanifold K = 3, C_in = C_out = 64, float16): coordinate bounds, key packing and
 radix sort, the double-traversed binary search with pair compaction and the
-metadata tables (Map), then gather, grouped MFMA GEMMs and scatter (GMaS).  Inputs are
-resident in HBM before timing starts.  Prints one JSON line.
+metadata tables (Map), then gather, grouped MFMA GEMMs and scatter (GMaS).  By default
+the gather is fused into the GEMMs' operand loads (each GEMM reads its pairs' input rows
+directly); the breakdown also times the layer with Algorithm 1's separate gather kernel
+and buffer.  Inputs are resident in HBM before timing starts.  Prints one JSON line.
 
 Measurement:
   1. an untimed pass with HIP events around every phase and kernel launch gives
@@ -42,6 +44,9 @@ def parse():
     p.add_argument("--channels", type=int, default=None, help="channel width for recipe 3")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--grouping", type=int, default=None)
+    p.add_argument("--gather", choices=("fused", "buffer"), default="fused",
+                   help="GEMM operand rows: loaded directly by the GEMM (fused, the library default) or "
+                        "gathered into a buffer first (Algorithm 1)")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of this many MiB (HBM counter calibration)")
     return p.parse_args()
@@ -61,7 +66,7 @@ def copy_calibration(mib: int) -> None:
                       "dispatches": 3}))
 
 
-def kernel_models(n, n_out, pairs, L, k3, passes):
+def kernel_models(n, n_out, pairs, L, k3, passes, fused=True):
     """Algorithmic (compulsory) bytes or flops per launch of each kernel.
 
     Returns name -> (bound, amount).  See the measurement section of the design
@@ -95,7 +100,10 @@ def kernel_models(n, n_out, pairs, L, k3, passes):
         # gather / scatter: feature rows, partial rows, one table entry per (offset, point), row map
         "k_gather": ("hbm", (n + pairs) * L.c_in * e + 4 * n * (k3 + 1)),
         "k_scatter": ("hbm", pairs * L.c_out * ep + n_out * L.c_out * e + 4 * n_out * (k3 + 1)),
-        "k_gemm_bytes": ("hbm", pairs * (L.c_in * e + L.c_out * ep) + k3 * L.c_in * L.c_out * e),
+        # GEMM: A rows (the gathered buffer, or with the fused gather each input row once
+        # plus one row index per pair), partial rows, weights
+        "k_gemm_bytes": ("hbm", (pairs * L.c_in * e if not fused else n * L.c_in * e + 4 * pairs)
+                         + pairs * L.c_out * ep + k3 * L.c_in * L.c_out * e),
         "k_gemm_flops": ("mfma", 2.0 * pairs * L.c_in * L.c_out),
     }
     return m
@@ -150,7 +158,11 @@ def main():
     x = torch.from_numpy(x_np).to(dev)
     w = torch.from_numpy(w_np).to(dev)
     mode = B.MODES[L.mode]
-    opt = B.Options.make(grouping=args.grouping) if args.grouping is not None else None
+    gather = B.GATHER_FUSED if args.gather == "fused" else B.GATHER_BUFFER
+    opt = B.Options.make(grouping=args.grouping, gather=gather)
+    # the other gather form, timed in the breakdown pass for comparison
+    alt_gather = B.GATHER_BUFFER if gather == B.GATHER_FUSED else B.GATHER_FUSED
+    alt_opt = B.Options.make(grouping=args.grouping, gather=alt_gather)
     map_ws = torch.empty(B.spconv_map_workspace_bytes(n, 0, L.K, mode, opt), dtype=torch.uint8, device=dev)
     h = B.spconv_build_map(coords, None, L.K, L.stride, 1, mode, opt, map_ws)
     counts = B.spconv_map_counts(h)
@@ -158,13 +170,15 @@ def main():
     n_out = int(B.lib().spconv_map_n_out(h))
     fwd_ws = torch.empty(B.spconv_forward_workspace_bytes(h, L.c_in, L.c_out, B.DTYPES[tdt], opt),
                          dtype=torch.uint8, device=dev)
+    alt_ws = torch.empty(B.spconv_forward_workspace_bytes(h, L.c_in, L.c_out, B.DTYPES[tdt], alt_opt),
+                         dtype=torch.uint8, device=dev)
     plan = B.spconv_forward_plan(h, L.c_in, L.c_out, B.DTYPES[tdt], opt)
     B.spconv_free_map(h)
     y = torch.empty((n_out, L.c_out), dtype=tdt, device=dev)
 
-    def step():
+    def step(fopt=opt, ws=fwd_ws):
         hm = B.spconv_build_map(coords, None, L.K, L.stride, 1, mode, opt, map_ws)
-        B.spconv_forward(hm, x, w, y, L.c_in, L.c_out, B.DTYPES[tdt], opt, fwd_ws)
+        B.spconv_forward(hm, x, w, y, L.c_in, L.c_out, B.DTYPES[tdt], fopt, ws)
         B.spconv_free_map(hm)
 
     for _ in range(args.warmup):
@@ -176,17 +190,22 @@ def main():
     R = 10
     ids = B.profile_ids()
 
-    def timed_pass(mask):
+    def timed_pass(mask, alt=False):
         B.spconv_profile_read(reset=True)
         B.spconv_profile_enable(mask)
         for _ in range(R):
-            step()
+            if alt:
+                step(alt_opt, alt_ws)
+            else:
+                step()
         torch.cuda.synchronize()
         B.spconv_profile_enable(False)
         return B.spconv_profile_read(reset=True)
 
     prof = timed_pass(B.PHASES_ALL)
     ph_ms = {k: v[0] / R for k, v in prof.items() if not k.startswith("k_")}
+    alt_prof = timed_pass(B.PHASES_ALL, alt=True)
+    alt_gmas = {p: alt_prof[p][0] / R for p in GMAS_PHASES}
     kern = {}
     for name, kid in ids.items():
         if name.startswith("k_"):
@@ -211,7 +230,7 @@ def main():
 
     k3 = L.K ** 3
     passes = int(round(kern.get("k_radix_scatter", (0, 0))[1]))
-    models = kernel_models(n, n_out, pairs, L, k3, passes)
+    models = kernel_models(n, n_out, pairs, L, k3, passes, fused=gather == B.GATHER_FUSED)
     if dominant == "k_gemm":
         # with materialised buffers the GEMM's intensity is below the MFMA ridge: price it on HBM
         flops = models["k_gemm_flops"][1]
@@ -269,6 +288,11 @@ def main():
         "gemm_frac_mfma": round(gemm_tflops / MFMA_PEAK_TFLOPS[L.dtype], 5),
         "padding_overhead": (plan.rows_padded - plan.rows_real) / max(plan.rows_real, 1),
         "gemm_launches": plan.n_gemm_launches,
+        "gather": args.gather,
+        # the same layer with the other gather form (breakdown pass, phase events)
+        "gmas_ms_other_gather": {"gather": "buffer" if args.gather == "fused" else "fused",
+                                 **{p: round(v, 5) for p, v in alt_gmas.items()},
+                                 "total": round(sum(alt_gmas.values()), 5)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -65,6 +65,14 @@ typedef enum {
   SPCONV_GROUP_MAPORDER = 2 /* prior-art grouping in Map (offset) order, for comparison */
 } spconv_grouping;
 
+/* How the GEMMs get their A rows (Section 2.2, Step 2). */
+typedef enum {
+  SPCONV_GATHER_BUFFER = 1, /* Algorithm 1: a gather kernel copies each input row to the
+                               per-pair buffer rows listed in the input metadata table */
+  SPCONV_GATHER_FUSED = 2   /* the GEMM kernels load pair r's input row straight from the
+                               features (its row index is the pair list's input index) */
+} spconv_gather;
+
 /* Tunables; any field left 0 takes its default.  The Map-step fields are the
  * hyperparameters of Section 5.1.4 (B = source-block size, C = query-block
  * limit); the GMaS fields are the Gather / Scatter tile sizes of Algorithm 1
@@ -86,7 +94,11 @@ typedef struct {
                         the input coordinates probed once per (output, offset), the prior-art
                         Map of Section 2.2 Step 1, kept as an ablation.  Same pairs (as sets),
                         listed in caller-row order within each offset */
-  int reserved[7];
+  int gather;        /* spconv_forward: SPCONV_GATHER_BUFFER = Algorithm 1, input rows copied into a
+                        per-pair buffer that the GEMMs read; SPCONV_GATHER_FUSED = the GEMMs load
+                        each pair's input row directly (no buffer); 0 = default (fused).  Results
+                        are bit-identical */
+  int reserved[6];
 } spconv_options;
 
 typedef struct spconv_map spconv_map; /* opaque host-side object */
@@ -177,7 +189,7 @@ int spconv_concat_rows(const void* d_a, int c_a, const void* d_b, int c_b, void*
 
 /* What spconv_forward will launch for this map (host-only): padded and real
  * buffer rows (padding overhead = (padded - real) / real, Section 3 figure on
- * GEMM reordering), number of GEMM launches, and the tiles used. */
+ * GEMM reordering), number of GEMM launches, the tiles used and the gather form. */
 typedef struct {
   int64_t rows_real;
   int64_t rows_padded;
@@ -185,6 +197,7 @@ typedef struct {
   int t_gather;
   int t_scatter;
   int grouping;
+  int gather; /* spconv_gather */
 } spconv_plan_info;
 int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype,
                         const spconv_options* opt, spconv_plan_info* info);

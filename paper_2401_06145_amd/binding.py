@@ -19,6 +19,7 @@ SPCONV_OK, SPCONV_EINVAL, SPCONV_ERANGE, SPCONV_EDUP, SPCONV_ENOSPC, SPCONV_EHIP
 SPCONV_SUBM, SPCONV_DOWN, SPCONV_UP = 0, 1, 2
 SPCONV_F32, SPCONV_F16, SPCONV_BF16 = 0, 1, 2
 GROUP_RAGGED, GROUP_SORTED, GROUP_MAPORDER = 0, 1, 2
+GATHER_BUFFER, GATHER_FUSED = 1, 2
 MODES = {"subm": SPCONV_SUBM, "down": SPCONV_DOWN, "up": SPCONV_UP}
 DTYPES = {torch.float32: SPCONV_F32, torch.float16: SPCONV_F16, torch.bfloat16: SPCONV_BF16}
 TORCH_DTYPES = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
@@ -43,7 +44,7 @@ class Options(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int), ("Cq", ctypes.c_int), ("t_gather", ctypes.c_int),
                 ("t_scatter", ctypes.c_int), ("grouping", ctypes.c_int), ("partial_dtype", ctypes.c_int),
                 ("launch_cost_rows", ctypes.c_int), ("presorted", ctypes.c_int), ("search", ctypes.c_int),
-                ("reserved", ctypes.c_int * 7)]
+                ("gather", ctypes.c_int), ("reserved", ctypes.c_int * 6)]
 
     @classmethod
     def make(cls, **kw) -> "Options":
@@ -58,7 +59,7 @@ class Options(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("rows_real", ctypes.c_int64), ("rows_padded", ctypes.c_int64),
                 ("n_gemm_launches", ctypes.c_int), ("t_gather", ctypes.c_int), ("t_scatter", ctypes.c_int),
-                ("grouping", ctypes.c_int)]
+                ("grouping", ctypes.c_int), ("gather", ctypes.c_int)]
 
 
 _lib = None

@@ -328,6 +328,7 @@ struct GmasPlan {
   int dtype = 0, elem = 4, pelem = 4, part_dtype = 0;
   int t_gather = 0, t_scatter = 0;
   int grouping = SPCONV_GROUP_RAGGED;
+  int gather = 2;  // 1: Algorithm 1 into a buffer; 2: fused into the GEMM's operand loads
   int64_t rows_real = 0, rows_padded = 0;
   int n_launches = 0;
   std::vector<std::vector<GemmSeg>> launches;  // one entry per GEMM launch (group)
@@ -389,6 +390,9 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
     return fail(SPCONV_EINVAL, "t_scatter must be 4..64 (power of two), divide c_out and span whole 16-byte partial vectors");
   p->grouping = (opt && opt->grouping) ? opt->grouping - 1 : SPCONV_GROUP_RAGGED;
   if (p->grouping < 0 || p->grouping > 2) return fail(SPCONV_EINVAL, "grouping");
+  p->gather = (opt && opt->gather) ? opt->gather : SPCONV_GATHER_FUSED;
+  if (p->gather != SPCONV_GATHER_BUFFER && p->gather != SPCONV_GATHER_FUSED)
+    return fail(SPCONV_EINVAL, "gather must be 0, SPCONV_GATHER_BUFFER or SPCONV_GATHER_FUSED");
 
   const int K3 = m->K3;
   p->rows_real = m->ptr[K3];
@@ -442,7 +446,8 @@ size_t plan_forward_ws(void* base, const spconv_map* m, int c_in, int c_out, con
   b->wt = (gemm_wide(c_in, c_out, p.dtype, p.part_dtype) && gemm_wide_transposed(c_in, c_out))
               ? a.take_bytes((size_t)m->K3 * c_in * c_out * p.elem)
               : nullptr;
-  b->buf_in = a.take_bytes((size_t)p.rows_real * c_in * p.elem);
+  // the fused gather reads the input rows directly: no gathered buffer
+  b->buf_in = (p.gather == SPCONV_GATHER_BUFFER) ? a.take_bytes((size_t)p.rows_real * c_in * p.elem) : nullptr;
   // one spare row past the partials: the full-width GEMM's stores of rows without data
   b->buf_out = a.take_bytes((size_t)(p.rows_real + 1) * c_out * p.pelem);
   return align_up(a.off, 256);
@@ -739,6 +744,7 @@ int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype, con
   info->t_gather = p.t_gather;
   info->t_scatter = p.t_scatter;
   info->grouping = p.grouping;
+  info->gather = p.gather;
   return SPCONV_OK;
 }
 
@@ -777,7 +783,8 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
   // a map without tables has no pairs: the scatter then writes zeros (plus the epilogue)
   const int K3 = m->omt ? m->K3 : 0;
   if (p.rows_real > 0) {
-    {
+    const bool fused = p.gather == SPCONV_GATHER_FUSED;
+    if (!fused) {
       PhaseScope ph(PH_GATHER, s);
       SPC_TRY(launch_gather(d_x, m->n_in, c_in, p.elem, m->imt, m->imt_stride, m->in_perm, K3, b.buf_in, p.t_gather,
                             s),
@@ -786,8 +793,11 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
     {
       PhaseScope ph(PH_GEMM, s);
       if (b.wt) SPC_TRY(launch_transpose_w(d_w, b.wt, m->K3, c_in, c_out, s), "weight transpose");
+      // fused: the A rows are the input rows of the pairs (pair r reads x[pin[r]])
+      const void* a_src = fused ? d_x : b.buf_in;
+      const int32_t* a_rows = fused ? m->pin : nullptr;
       for (const auto& segs : p.launches)
-        SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), b.buf_in, d_w, b.wt, b.buf_out,
+        SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), a_src, a_rows, d_w, b.wt, b.buf_out,
                             static_cast<char*>(b.buf_out) + (size_t)p.rows_real * c_out * p.pelem, c_in, c_out,
                             dtype, p.part_dtype, s),
                 "grouped GEMM");

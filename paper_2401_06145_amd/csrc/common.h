@@ -205,10 +205,13 @@ bool gemm_wide_transposed(int c_in, int c_out);
 // wt[k][n][c] = w[k][c][n] for 16-bit weights.
 hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_out, hipStream_t s);
 // Launches the segments (any number; split into launches of at most 64 segments).
+// a_rows NULL: buffer row r of the A operand is buf_in row r (the gathered buffer).
+// a_rows set: the gather is fused into the operand loads, row r is buf_in row
+// a_rows[r] (buf_in is then the layer's input features, a_rows the pairs' input rows).
 // wt: transposed weights (launch_transpose_w) or NULL;
 // dump_row: one spare row of c_out partials the full-width kernel may overwrite.
-hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, const void* wt,
-                       void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
+hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
+                       const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
                        hipStream_t s);
 
 }  // namespace spc

@@ -16,6 +16,11 @@
 // Group padding rows (segment height > rows) are fed as zeros: they cost MFMA
 // cycles, like the zero-padded batched GEMMs of the paper, but no memory traffic.
 //
+// The A operand is either the gathered buffer (row r of the launch is buffer row
+// r, Algorithm 1's layout) or, with the gather fused into the operand loads, the
+// layer's input features themselves: row r is then input row a_rows[r], the input
+// index of pair r.  The fused form never writes or reads the gathered buffer.
+//
 // Two kernels.  k_gemm_wide (f16 / bf16, c_in <= 512) gives a workgroup the full
 // output width whenever W_k^T fits the 160 KiB of LDS, so every buf_in row is
 // read from HBM once; it stages W_k^T from a transposed copy of the weights
@@ -42,6 +47,7 @@ struct GemmLaunchArgs {
 };
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
@@ -98,7 +104,8 @@ __device__ __forceinline__ void store4(__hip_bfloat16* p, f32x4 v) {
 
 // T: operand type; TO: partial (output buffer) type; NT: 16-column tiles per workgroup.
 template <typename T, typename TO, int NT>
-__global__ __launch_bounds__(kThreads) void k_gemm(GemmLaunchArgs g, const T* __restrict__ A, const T* __restrict__ W,
+__global__ __launch_bounds__(kThreads) void k_gemm(GemmLaunchArgs g, const T* __restrict__ A,
+                                                   const int32_t* __restrict__ arows, const T* __restrict__ W,
                                                    TO* __restrict__ C, int c_in, int c_out, int kp, int ldk,
                                                    int rows_per_tile) {
   using M = Mfma<T>;
@@ -133,7 +140,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmLaunchArgs g, const T* __
   for (int m0 = r_begin + wave * 16; m0 < r_end; m0 += 64) {
     const int row = m0 + col;
     const bool real = row < rows;
-    const T* arow = A + (row0 + row) * (int64_t)c_in;
+    const int64_t src = !real ? 0 : (arows ? (int64_t)arows[row0 + row] : row0 + row);
+    const T* arow = A + src * (int64_t)c_in;
     f32x4 acc[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -172,10 +180,12 @@ constexpr int wide_mb(int, int) { return 1; }
 // (then W_k^T is staged from it with 16-byte copies); dump is one spare
 // row of c_out partials that absorbs the stores of rows without data.  Loads
 // never branch: lanes without data (rows past the segment, k past c_in) read a
-// valid dummy address and select zero, so the compiler keeps the next blocks'
+// valid dummy address; k past c_in is then zeroed, rows past the segment compute
+// values that only reach the dump row.  So the compiler keeps the next blocks'
 // loads in flight across the current blocks' MFMAs.
-template <typename T, typename TO, int NT, int KSTEPS>
+template <typename T, typename TO, int NT, int KSTEPS, bool GATHER>
 __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, const T* __restrict__ A,
+                                                            const int32_t* __restrict__ arows,
                                                             const T* __restrict__ w, const T* __restrict__ wt,
                                                             TO* __restrict__ C,
                                                             TO* __restrict__ dump, int c_in, int c_out, int ldk,
@@ -240,11 +250,24 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   const int row_lim = min(rows, r_end);  // rows of this tile that hold data
   // raw: the next blocks as loaded (dummy data where masked); cur: the blocks in use
   F raw[MB][KSTEPS], cur[MB][KSTEPS];
+  // GATHER: source rows of the blocks issued next, fetched one round ahead so the
+  // operand loads never wait for their index (masked lanes read the segment's first)
+  int32_t src[MB];
+  auto fetch_rows = [&](int mb) {
+    if constexpr (GATHER) {
+#pragma unroll
+      for (int b = 0; b < MB; ++b) {
+        const int row = mb + 16 * b + col;
+        src[b] = arows[row0 + (row < row_lim ? row : 0)];
+      }
+    }
+  };
   auto issue = [&](int mb) {
 #pragma unroll
     for (int b = 0; b < MB; ++b) {
       const int row = mb + 16 * b + col;
-      const T* arow = A + (row0 + row) * (int64_t)c_in;
+      const int64_t r = GATHER ? (int64_t)src[b] : row0 + row;
+      const T* arow = A + r * (int64_t)c_in;
 #pragma unroll
       for (int q = 0; q < KSTEPS; ++q) {
         const int kk = 32 * q + 8 * sub;
@@ -252,20 +275,34 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
       }
     }
   };
-  auto take = [&](int mb) {
+  // Lanes past c_in must feed zeros (a non-finite dummy value times the zero
+  // weights would still poison the sums); rows past the tile may feed anything,
+  // their results go to the dump row.  The zeroing is an AND with a per-k-step mask
+  // the compiler cannot see through: a select on the loaded value lets it sink the
+  // loads into the select's branch, after the MFMAs, and the prefetch is lost.
+  u32x4 kmask[KSTEPS];
 #pragma unroll
-    for (int b = 0; b < MB; ++b) {
-      const bool row_ok = mb + 16 * b + col < row_lim;
+  for (int q = 0; q < KSTEPS; ++q) {
+    uint32_t m = (32 * q + 8 * sub < c_in) ? 0xFFFFFFFFu : 0u;
+    asm("" : "+v"(m));
+    kmask[q] = u32x4{m, m, m, m};
+  }
+  auto take = [&](int) {
 #pragma unroll
-      for (int q = 0; q < KSTEPS; ++q) cur[b][q] = (row_ok && 32 * q + 8 * sub < c_in) ? raw[b][q] : M::zero();
-    }
+    for (int b = 0; b < MB; ++b)
+#pragma unroll
+      for (int q = 0; q < KSTEPS; ++q)
+        cur[b][q] = __builtin_bit_cast(F, __builtin_bit_cast(u32x4, raw[b][q]) & kmask[q]);
   };
   int m0 = r_begin + rg * MB * 16;
+  fetch_rows(m0);
   issue(m0);
+  fetch_rows(m0 + STEP);
   take(m0);
   for (; m0 < r_end; m0 += STEP) {
     const int m1 = m0 + STEP;
     issue(m1);  // masked to the dummy address past the tile; lands during the MFMAs below
+    fetch_rows(m1 + STEP);
     // keeps the W^T fragment reads inside the loop: hoisted, they would need
     // 4 * NTW * KSTEPS registers and spill
     asm volatile("" ::: "memory");
@@ -294,6 +331,12 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
       for (int t = 0; t < NTW; ++t) store4(crow + 16 * t, acc[b][t]);
     }
     take(m1);
+    // the masked operands are complete here, not at the top of the next round:
+    // there the compiler's wait would also cover the stores just issued
+#pragma unroll
+    for (int b = 0; b < MB; ++b)
+#pragma unroll
+      for (int q = 0; q < KSTEPS; ++q) asm volatile("" ::"v"(cur[b][q]));
   }
 }
 
@@ -327,11 +370,11 @@ int wide_round_rows(int nt, int ks) {
   return kWideWaves / cg * wide_mb(nt / cg, ks) * 16;
 }
 
-template <typename T, typename TO>
+template <typename T, typename TO, bool GATHER>
 const void* wide_kernel(int nt, int ks) {
-#define SPC_W(N, KS_)                                                                   \
-  if constexpr (wide_fits(N, KS_)) {                                                     \
-    if (nt == N && ks == KS_) return reinterpret_cast<const void*>(&k_gemm_wide<T, TO, N, KS_>); \
+#define SPC_W(N, KS_)                                                                                     \
+  if constexpr (wide_fits(N, KS_)) {                                                                       \
+    if (nt == N && ks == KS_) return reinterpret_cast<const void*>(&k_gemm_wide<T, TO, N, KS_, GATHER>); \
   }
 #define SPC_WK(N) \
   SPC_W(N, 1) SPC_W(N, 2) SPC_W(N, 3) SPC_W(N, 4) SPC_W(N, 6) SPC_W(N, 8) SPC_W(N, 12) SPC_W(N, 16)
@@ -341,10 +384,14 @@ const void* wide_kernel(int nt, int ks) {
   return nullptr;
 }
 
-const void* wide_kernel_for(int dtype, int part_dtype, int nt, int ks) {
-  if (dtype == 1 && part_dtype == 0) return wide_kernel<__half, float>(nt, ks);
-  if (dtype == 1 && part_dtype == 1) return wide_kernel<__half, __half>(nt, ks);
-  if (dtype == 2 && part_dtype == 2) return wide_kernel<__hip_bfloat16, __hip_bfloat16>(nt, ks);
+const void* wide_kernel_for(int dtype, int part_dtype, bool gather, int nt, int ks) {
+  if (dtype == 1 && part_dtype == 0)
+    return gather ? wide_kernel<__half, float, true>(nt, ks) : wide_kernel<__half, float, false>(nt, ks);
+  if (dtype == 1 && part_dtype == 1)
+    return gather ? wide_kernel<__half, __half, true>(nt, ks) : wide_kernel<__half, __half, false>(nt, ks);
+  if (dtype == 2 && part_dtype == 2)
+    return gather ? wide_kernel<__hip_bfloat16, __hip_bfloat16, true>(nt, ks)
+                  : wide_kernel<__hip_bfloat16, __hip_bfloat16, false>(nt, ks);
   return nullptr;
 }
 
@@ -369,8 +416,8 @@ __global__ __launch_bounds__(256) void k_transpose_w(const uint16_t* __restrict_
 }
 
 template <typename T, typename TO>
-hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const void* W, void* C, int c_in,
-                  int c_out, int rows_per_tile, hipStream_t s) {
+hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const int32_t* arows, const void* W,
+                  void* C, int c_in, int c_out, int rows_per_tile, hipStream_t s) {
   const int KS = Mfma<T>::KS;
   const int kp = (c_in + KS - 1) / KS * KS;
   const int ldk = kp + 16 / (int)sizeof(T);
@@ -393,8 +440,8 @@ hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const
   switch (nt) {
 #define SPC_G(N)                                                                                     \
   case N:                                                                                            \
-    hipLaunchKernelGGL((k_gemm<T, TO, N>), grid, dim3(kThreads), lds, s, g, a, w, c, c_in, c_out, kp, ldk, \
-                       rows_per_tile);                                                               \
+    hipLaunchKernelGGL((k_gemm<T, TO, N>), grid, dim3(kThreads), lds, s, g, a, arows, w, c, c_in, c_out, kp, \
+                       ldk, rows_per_tile);                                                          \
     break;
     SPC_G(1)
     SPC_G(2)
@@ -426,8 +473,9 @@ hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_o
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const void* w, const void* wt,
-                       void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype, hipStream_t s) {
+hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
+                       const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
+                       hipStream_t s) {
   if (c_out % 16 != 0) return hipErrorInvalidValue;
   const bool wide = dump_row && gemm_wide(c_in, c_out, dtype, part_dtype);
   int64_t rows_all = 0;
@@ -443,7 +491,7 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
     ks = wide_ksteps(c_in);
     ldk = 32 * ks + 8;
     lds = (size_t)16 * nt * ldk * 2;
-    wfn = wide_kernel_for(dtype, part_dtype, nt, ks);
+    wfn = wide_kernel_for(dtype, part_dtype, a_rows != nullptr, nt, ks);
     if (!wfn) return hipErrorInvalidValue;
     int per_cu = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wfn, kWideThreads, lds);
@@ -485,18 +533,19 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
       void* c = buf_out;
       void* d = dump_row;
       const void* wp = w;
-      void* args[] = {&g, &a, &wp, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile};
+      const int32_t* ar = a_rows;
+      void* args[] = {&g, &a, &ar, &wp, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile};
       e = hipLaunchKernel(wfn, grid, dim3(kWideThreads), args, lds, s);
     } else if (dtype == 0 && part_dtype == 0)
-      e = gemm_t<float, float>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);
+      e = gemm_t<float, float>(g, tiles, buf_in, a_rows, w, buf_out, c_in, c_out, rows_per_tile, s);
     else if (dtype == 1 && part_dtype == 0)
-      e = gemm_t<__half, float>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);
+      e = gemm_t<__half, float>(g, tiles, buf_in, a_rows, w, buf_out, c_in, c_out, rows_per_tile, s);
     else if (dtype == 1 && part_dtype == 1)
-      e = gemm_t<__half, __half>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);
+      e = gemm_t<__half, __half>(g, tiles, buf_in, a_rows, w, buf_out, c_in, c_out, rows_per_tile, s);
     else if (dtype == 2 && part_dtype == 0)
-      e = gemm_t<__hip_bfloat16, float>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);
+      e = gemm_t<__hip_bfloat16, float>(g, tiles, buf_in, a_rows, w, buf_out, c_in, c_out, rows_per_tile, s);
     else if (dtype == 2 && part_dtype == 2)
-      e = gemm_t<__hip_bfloat16, __hip_bfloat16>(g, tiles, buf_in, w, buf_out, c_in, c_out, rows_per_tile, s);
+      e = gemm_t<__hip_bfloat16, __hip_bfloat16>(g, tiles, buf_in, a_rows, w, buf_out, c_in, c_out, rows_per_tile, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -214,7 +214,7 @@ def test_grouping_tiles_partials_are_result_neutral():
     infos = []
     for g in (B.GROUP_RAGGED, B.GROUP_SORTED, B.GROUP_MAPORDER):
         for tg, ts in ((8, 8), (16, 16), (64, 32), (32, 64)):
-            opt = B.Options.make(grouping=g, t_gather=tg, t_scatter=ts)
+            opt = B.Options.make(grouping=g, t_gather=tg, t_scatter=ts, gather=B.GATHER_BUFFER)
             y = B.Forward(km, 64, 64, torch.float16, opt)(xd, wd)
             assert torch.equal(y, base), f"grouping {g} tiles {tg}/{ts} changed the result"
         infos.append(km.plan(64, 64, torch.float16, B.Options.make(grouping=g)))
@@ -228,6 +228,68 @@ def test_grouping_tiles_partials_are_result_neutral():
     e32, e16 = rel_err(to_f64(y32), ref), rel_err(to_f64(base), ref)
     print(f"normwise error: float32 partials {e32:.2e}, float16 partials {e16:.2e}", flush=True)
     assert e32 <= TOL["f16"] and e16 <= TOL["f16"] / 3
+
+
+@pytest.mark.parametrize("dtype,c_in,c_out,pd", [
+    ("f32", 16, 32, 0),     # fallback kernel
+    ("f16", 16, 16, 0),     # half of one 32-deep k-step is padding
+    ("f16", 48, 64, 0),     # padding inside the second k-step
+    ("f16", 64, 64, 1),     # float32 partials
+    ("bf16", 64, 32, 1),    # fallback kernel, bf16
+    ("bf16", 96, 32, 0),
+    ("f16", 256, 128, 0),   # W^T staged from the transposed copy
+])
+def test_gather_forms_bit_identical(dtype, c_in, c_out, pd):
+    """GEMMs that load each pair's input row directly (the fused gather) see the
+    same operands in the same order as GEMMs reading Algorithm 1's gathered
+    buffer, so the two forms agree bit for bit, with and without group padding."""
+    say(f"gather forms {dtype} {c_in}->{c_out} partials {pd}")
+    c = _cloud(77, 6000, -12, 12)
+    x = scenes.features(len(c), c_in, dtype, 21)
+    w = scenes.weights(3, c_in, c_out, dtype, 22)
+    km = B.KernelMap.build(to_dev(c), 3)
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    td = B.TORCH_DTYPES[dtype]
+    ys = {}
+    for g in (B.GATHER_BUFFER, B.GATHER_FUSED):
+        for grp in (B.GROUP_RAGGED, B.GROUP_SORTED):
+            opt = B.Options.make(gather=g, grouping=grp, partial_dtype=pd)
+            assert km.plan(c_in, c_out, td, opt).gather == g
+            ys[g, grp] = B.Forward(km, c_in, c_out, td, opt)(xd, wd)
+    assert km.plan(c_in, c_out, td).gather == B.GATHER_FUSED  # the default
+    base = ys[B.GATHER_BUFFER, B.GROUP_RAGGED]
+    for key, y in ys.items():
+        assert torch.equal(y, base), f"gather form / grouping {key} changed the result"
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    ref = oracle.features(scenes.to_f64(x, dtype), scenes.to_f64(w, dtype), okm)
+    assert rel_err(to_f64(base), ref) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("c_in", [16, 48])
+def test_padding_lanes_feed_exact_zeros(c_in):
+    """When c_in does not fill the 32-deep MFMA k-steps, the padding lanes read a
+    dummy row (input row 0) and must still feed zeros: with an infinity in row 0,
+    only the outputs that row 0 really reaches may be non-finite."""
+    say(f"k padding with a non-finite dummy row, c_in={c_in}")
+    c = _cloud(78, 3000, -9, 9)
+    x = scenes.features(len(c), c_in, "f16", 23)
+    x[0, :] = np.inf
+    w = scenes.weights(3, c_in, 32, "f16", 24)
+    km = B.KernelMap.build(to_dev(c), 3)
+    xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    reached = np.zeros(len(c), dtype=bool)
+    reached[okm.pout[okm.pin == 0]] = True
+    assert 0 < reached.sum() < len(c)
+    keep = ~reached
+    xf = scenes.to_f64(x, "f16")
+    xf[0, :] = 0.0  # row 0 does not reach the kept rows
+    ref = oracle.features(xf, scenes.to_f64(w, "f16"), okm)[keep]
+    for g in (B.GATHER_BUFFER, B.GATHER_FUSED):
+        y = B.Forward(km, c_in, 32, torch.float16, B.Options.make(gather=g))(xd, wd)
+        got = to_f64(y)[keep]
+        assert np.isfinite(got).all(), f"gather form {g}: padding lanes leaked the dummy row"
+        assert rel_err(got, ref) <= TOL["f16"]
 
 
 def test_large_cloud_one_kernel_sort_passes():

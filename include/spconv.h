@@ -168,7 +168,8 @@ size_t spconv_forward_workspace_bytes(const spconv_map* m, int c_in, int c_out, 
  *   d_y [n_out][c_out], all row-major in `dtype`; d_y is fully overwritten (rows
  *   without pairs get zeros).  Products accumulate in float32.
  * Requirements: c_in, c_out in [1, 1024]; 16-byte rows (c * element size % 16 == 0)
- * and c_out % 16 == 0.  Asynchronous on `stream`; no host synchronisation. */
+ * and c_out % 16 == 0; d_x, d_w, d_y (and d_residual) 16-byte aligned, else
+ * SPCONV_EINVAL.  Asynchronous on `stream`; no host synchronisation. */
 int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in,
                    int c_out, int dtype, const spconv_options* opt, void* d_workspace,
                    size_t ws_bytes, void* stream);

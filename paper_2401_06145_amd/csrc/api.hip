@@ -184,6 +184,7 @@ struct MapBufs {
   int32_t* ts;    // T_s, the source-side table
   uint32_t* item_cnt;
   uint32_t* item_off;
+  uint2* item_desc;  // per work item: query range and offset (count pass -> write pass)
   uint64_t* hkeys;  // hash-table search only
   uint32_t* hvals;
   int log2cap;
@@ -249,6 +250,7 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   b->ts = m.take<int32_t>((int64_t)K3 * n_src);
   b->item_cnt = m.take<uint32_t>(b->max_items);
   b->item_off = m.take<uint32_t>(b->max_items);
+  b->item_desc = m.take<uint2>(b->max_items);
   b->mm_partial = static_cast<int32_t*>(m.take_bytes(minmax_temp_bytes()));
   b->scan_tmp = m.take_bytes(scan_temp_bytes(std::max(std::max(nkb, n_src), b->max_items)));
   b->log2cap = 0;
@@ -377,11 +379,9 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
   p->pelem = elem_bytes(p->part_dtype);
   // tiles: default one 16-byte vector per thread for gather and for the partial reads of scatter
   p->t_gather = (opt && opt->t_gather) ? opt->t_gather : 16 / p->elem;
-  // Algorithm 2 on gfx950 picked 16 channels (two 16-byte vectors) for 2-byte partials and
-  // 4 channels for float32 ones on every tuned layer; fall back to one vector if 16 does not divide
-  int ts_default = (p->pelem == 2) ? 16 : 4;
-  if (c_out % ts_default != 0) ts_default = 16 / p->pelem;
-  p->t_scatter = (opt && opt->t_scatter) ? opt->t_scatter : ts_default;
+  // scatter: one 16-byte partial vector per thread (the row-group scatter, which reads
+  // each output's table entries once)
+  p->t_scatter = (opt && opt->t_scatter) ? opt->t_scatter : 16 / p->pelem;
   if (p->t_gather <= 0 || c_in % p->t_gather != 0 || (p->t_gather * p->elem) % 16 != 0 ||
       (p->t_gather * p->elem / 16) > 16 || ((p->t_gather * p->elem / 16) & (p->t_gather * p->elem / 16 - 1)))
     return fail(SPCONV_EINVAL, "t_gather must divide c_in and span 1, 2, 4, 8 or 16 16-byte vectors");
@@ -585,6 +585,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   a.ts = b.ts;
   a.ts_stride = n_src;
   a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
+  a.item_desc = b.item_desc;
   // the hash-table search treats all queries of an offset as one block
   const int64_t nb = tu.hash ? 1 : b.nb;
   {
@@ -773,6 +774,9 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
   if (st != SPCONV_OK) return st;
   if (m->n_out > 0 && !d_y) return fail(SPCONV_EINVAL, "d_y is NULL");
   if (p.rows_real > 0 && (!d_x || !d_w)) return fail(SPCONV_EINVAL, "d_x / d_w is NULL");
+  auto misaligned = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) != 0; };
+  if (misaligned(d_x) || misaligned(d_w) || misaligned(d_y) || misaligned(d_residual))
+    return fail(SPCONV_EINVAL, "d_x, d_w, d_y and d_residual must be 16-byte aligned");
   FwdBufs b;
   const size_t need = plan_forward_ws(nullptr, m, c_in, c_out, p, &b);
   if (need > 0 && (!d_workspace || ws_bytes < need)) return fail(SPCONV_ENOSPC, "forward workspace too small");

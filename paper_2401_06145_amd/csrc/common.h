@@ -143,6 +143,9 @@ struct SearchArgs {
   // entries come from a fill before it, or (sym != 0) from the write pass itself.
   int32_t* ts;
   int64_t ts_stride;
+  // Per work item, written by the count pass and read by the write pass:
+  // x = first sorted query position, y = query count | (offset << 16).
+  uint2* item_desc;
   // Submanifold map with odd K: query q misses offset k exactly when source q
   // has no partner at the mirrored offset K^3 - 1 - k, so the write pass marks
   // that T_s entry instead of a separate fill.

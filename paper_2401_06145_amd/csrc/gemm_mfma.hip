@@ -217,30 +217,6 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   const int tile = (int)blockIdx.x - g.tile_start[s];
   const int n0 = blockIdx.y * BN;
 
-  if (wt) {
-    // W_k^T rows n0 .. n0 + BN from the transposed copy, 8 elements (16 bytes) per
-    // copy; columns past c_in are zero
-    const T* wk = wt + ((int64_t)k * c_out + n0) * c_in;
-    constexpr int CH = KP / 8;  // 16-byte chunks per LDS row
-    for (int idx = tid; idx < BN * CH; idx += kWideThreads) {
-      const int n = idx / CH;
-      const int c = (idx - n * CH) * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (c < c_in) v = *reinterpret_cast<const uint4*>(wk + (int64_t)n * c_in + c);
-      *reinterpret_cast<uint4*>(lw + n * ldk + c) = v;
-    }
-  } else {
-    // small W_k: transpose while staging, one element per thread and step (reads
-    // coalesced along n; the LDS row pitch keeps the 2-byte writes conflict-free)
-    const T* wk = w + (int64_t)k * c_in * c_out + n0;
-    for (int idx = tid; idx < BN * KP; idx += kWideThreads) {
-      const int c = idx / BN;
-      const int n = idx - c * BN;
-      lw[n * ldk + c] = (c < c_in) ? wk[(int64_t)c * c_out + n] : zero_elem<T>();
-    }
-  }
-  __syncthreads();
-
   const int r_begin = tile * rows_per_tile;
   const int r_end = min(r_begin + rows_per_tile, height);
   const int sub = lane >> 4;
@@ -275,6 +251,63 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
       }
     }
   };
+
+  // Prologue, ordered so that its round trips overlap: the first blocks' source
+  // rows, then the first kWStage 16-byte chunks of the W_k^T slice per thread, then
+  // the first blocks' operands (they wait only for their rows), then the chunks go
+  // to LDS.  A chunk is 8 consecutive k of one column n when read from the
+  // transposed copy, or 8 consecutive n of one k when read from W itself (and
+  // transposed on the way into LDS).  k past c_in is zero.
+  const int m_first = r_begin + rg * MB * 16;
+  fetch_rows(m_first);
+  constexpr int CH_T = KP / 8;  // chunks per W^T row (transposed copy)
+  constexpr int CH_N = BN / 8;  // chunks per W row slice (plain copy)
+  constexpr int NCHUNK = BN * KP / 8;
+  const T* wk_t = wt ? wt + ((int64_t)k * c_out + n0) * c_in : nullptr;
+  const T* wk_p = w + (int64_t)k * c_in * c_out + n0;
+  auto chunk_nc = [&](int idx, int* n, int* c) {
+    if (wt) {
+      *n = idx / CH_T;
+      *c = (idx - *n * CH_T) * 8;
+    } else {
+      *c = idx / CH_N;
+      *n = (idx - *c * CH_N) * 8;
+    }
+  };
+  auto load_chunk = [&](int idx) -> uint4 {
+    int n, c;
+    chunk_nc(idx, &n, &c);
+    if (idx >= NCHUNK || c >= c_in) return make_uint4(0, 0, 0, 0);
+    return wt ? *reinterpret_cast<const uint4*>(wk_t + (int64_t)n * c_in + c)
+              : *reinterpret_cast<const uint4*>(wk_p + (int64_t)c * c_out + n);
+  };
+  auto store_chunk = [&](int idx, const uint4& v) {
+    if (idx >= NCHUNK) return;
+    int n, c;
+    chunk_nc(idx, &n, &c);
+    if (wt) {
+      *reinterpret_cast<uint4*>(lw + n * ldk + c) = v;
+    } else {
+      const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) lw[(n + j) * ldk + c] = e[j];
+    }
+  };
+  constexpr int kWStage = 8;  // chunks per thread in flight at a time
+  uint4 wv[kWStage];
+#pragma unroll
+  for (int u = 0; u < kWStage; ++u) wv[u] = load_chunk(u * kWideThreads + tid);
+  issue(m_first);
+#pragma unroll
+  for (int u = 0; u < kWStage; ++u) store_chunk(u * kWideThreads + tid, wv[u]);
+  for (int cb = kWStage * kWideThreads; cb < NCHUNK; cb += kWStage * kWideThreads) {
+#pragma unroll
+    for (int u = 0; u < kWStage; ++u) wv[u] = load_chunk(cb + u * kWideThreads + tid);
+#pragma unroll
+    for (int u = 0; u < kWStage; ++u) store_chunk(cb + u * kWideThreads + tid, wv[u]);
+  }
+  __syncthreads();
+
   // Lanes past c_in must feed zeros (a non-finite dummy value times the zero
   // weights would still poison the sums); rows past the tile may feed anything,
   // their results go to the dump row.  The zeroing is an AND with a per-k-step mask
@@ -294,9 +327,7 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
       for (int q = 0; q < KSTEPS; ++q)
         cur[b][q] = __builtin_bit_cast(F, __builtin_bit_cast(u32x4, raw[b][q]) & kmask[q]);
   };
-  int m0 = r_begin + rg * MB * 16;
-  fetch_rows(m0);
-  issue(m0);
+  int m0 = m_first;
   fetch_rows(m0 + STEP);
   take(m0);
   for (; m0 < r_end; m0 += STEP) {

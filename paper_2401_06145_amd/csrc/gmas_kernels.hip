@@ -22,7 +22,7 @@ namespace spc {
 namespace {
 
 constexpr int kThreads = 256;
-// metadata entries loaded ahead per thread (independent loads in flight)
+// metadata entries loaded ahead per gather thread (independent loads in flight)
 constexpr int kMtBatch = 8;
 
 // V = 16-byte vectors per thread (tile T = V * 16 / element bytes channels).
@@ -137,17 +137,155 @@ __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf
   }
 }
 
+// Row-group scatter (the default tile: one 16-byte partial vector per thread).  A
+// group of LP = c_out / W lanes of one wave owns an output row, lane `sub` holding
+// channels [sub W, sub W + W) for W = 16 / sizeof(TP) (CH such vectors per lane when
+// the row is wider than a wave).  So:
+//  * the output's table entries are read once per output, not once per tile: lane
+//    sub reads offsets sub, sub + LP, ...; a wave ballot then ranks the listed ones
+//    in offset order, and their rows go to a per-group list in LDS;
+//  * every partial row is read by the group as whole contiguous 16-byte vectors, and
+//    the output row is written the same way;
+//  * the rows of a batch of listed entries are all requested before the first is
+//    added.
+// Offsets are summed in ascending order, as in the tiled scatter, so both give the
+// same result bit for bit.
+constexpr int kRowList = 32;       // table entries per group and batch (at least LP)
+constexpr int kRowListWave = 1024;  // list entries per wave
+
+template <typename TP, typename TO, int CH>
+__global__ __launch_bounds__(kThreads) void k_scatter_rows(const TP* __restrict__ buf, int64_t n_out, int c_out,
+                                                           const int32_t* __restrict__ omt, int64_t stride,
+                                                           const uint32_t* __restrict__ perm, int K3, TO* y,
+                                                           const TO* residual, int relu, int LP) {
+  constexpr int W = 16 / (int)sizeof(TP);  // channels per 16-byte partial vector
+  constexpr int WPB = kThreads / kWave;
+  __shared__ int32_t s_list[WPB][kRowListWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int gpw = kWave / LP;  // groups per wave (lanes past gpw * LP idle)
+  const int group = lane / LP;
+  const int sub = lane - group * LP;
+  const int64_t p = ((int64_t)blockIdx.x * WPB + wave) * gpw + group;
+  const bool active = group < gpw && p < n_out;
+  const int64_t i = active ? (perm ? (int64_t)perm[p] : p) : 0;
+  // the group's slice of the wave's 64 lanes
+  const uint64_t gmask = (LP >= kWave ? ~0ull : ((1ull << LP) - 1ull)) << (group < gpw ? group * LP : 0);
+  const int per_batch = max(1, kRowList / LP);  // table entries per lane and batch
+  // the group's list holds one batch: per_batch * LP entries (gpw of them fit a wave's
+  // kRowListWave: at most 32 groups of 32 entries)
+  int32_t* list = &s_list[wave][(group < gpw ? group : 0) * per_batch * LP];
+  float acc[CH][W];
+#pragma unroll
+  for (int c = 0; c < CH; ++c)
+#pragma unroll
+    for (int e = 0; e < W; ++e) acc[c][e] = 0.f;
+  float rsd[CH][W];
+  if (residual && active) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const TO* rp = residual + i * (int64_t)c_out + (int64_t)(c * LP + sub) * W;
+#pragma unroll
+      for (int e = 0; e < W; ++e) rsd[c][e] = to_f32<TO>(rp[e]);
+    }
+  }
+  for (int kb = 0; kb < K3; kb += per_batch * LP) {
+    // this batch's offsets kb + sub + LP m, m < per_batch
+    int nv = 0;
+    for (int m = 0; m < per_batch; ++m) {
+      const int k = kb + sub + LP * m;
+      const int32_t r = (active && k < K3) ? omt[(int64_t)k * stride + p] : -1;
+      const uint64_t bal = __ballot(r >= 0) & gmask;
+      if (r >= 0) list[nv + popc64(bal & lanemask_lt())] = r;
+      nv += popc64(bal);
+    }
+    // listed rows, in offset order (the list is the group's own: no barrier)
+    for (int j0 = 0; j0 < nv; j0 += 4) {
+      int32_t row[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) row[j] = (j0 + j < nv) ? list[j0 + j] : -1;
+      uint4 v[4][CH];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+          v[j][c] = (row[j] >= 0) ? *reinterpret_cast<const uint4*>(buf + (int64_t)row[j] * c_out +
+                                                                     (int64_t)(c * LP + sub) * W)
+                                  : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (row[j] >= 0) {
+#pragma unroll
+          for (int c = 0; c < CH; ++c) {
+            const TP* pv = reinterpret_cast<const TP*>(&v[j][c]);
+#pragma unroll
+            for (int e = 0; e < W; ++e) acc[c][e] += to_f32<TP>(pv[e]);
+          }
+        }
+      }
+    }
+  }
+  if (!active) return;
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    TO out[W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) {
+      float a = acc[c][e];
+      if (residual) a += rsd[c][e];
+      if (relu) a = fmaxf(a, 0.f);
+      out[e] = from_f32<TO>(a);
+    }
+    TO* dst = y + i * (int64_t)c_out + (int64_t)(c * LP + sub) * W;
+    constexpr int BYTES = W * sizeof(TO);
+    if constexpr (BYTES == 16) {
+      *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(out);
+    } else if constexpr (BYTES == 8) {
+      *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(out);
+    } else {
+#pragma unroll
+      for (int e = 0; e < W; ++e) dst[e] = out[e];
+    }
+  }
+}
+
 unsigned blocks_for(int64_t threads) { return (unsigned)((threads + kThreads - 1) / kThreads); }
+
+// Lanes per output row of the row-group scatter, or 0 where it does not apply: it
+// serves the tile of one 16-byte partial vector per thread when a row is at most a
+// wave of such vectors, or 2 or 4 per lane of a full wave.
+int scatter_row_lanes(int c_out, int pelem, int tile) {
+  if (tile * pelem != 16 || (c_out * pelem) % 16 != 0) return 0;
+  const int vec = c_out * pelem / 16;
+  if (vec <= kWave) return vec;
+  if (vec == 2 * kWave || vec == 4 * kWave) return kWave;
+  return 0;
+}
 
 template <typename TP, typename TO>
 hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* omt, int64_t stride,
                      const uint32_t* perm, int K3, void* y, int tile, const void* residual, int relu, hipStream_t s) {
   ProfScope ps(KN_SCATTER, s);
-  const int64_t threads = n_out * (c_out / tile);
-  const dim3 g(blocks_for(threads)), b(kThreads);
   const TP* p = static_cast<const TP*>(buf);
   TO* o = static_cast<TO*>(y);
   const TO* r = static_cast<const TO*>(residual);
+  const int lp = scatter_row_lanes(c_out, (int)sizeof(TP), tile);
+  if (lp > 0) {
+    // row-group scatter: one 16-byte partial vector per lane and row slice
+    const int vec = c_out * (int)sizeof(TP) / 16;
+    const int ch = vec / lp;
+    const int64_t per_block = (int64_t)(kThreads / kWave) * (kWave / lp);
+    const dim3 g((unsigned)((n_out + per_block - 1) / per_block)), b(kThreads);
+    switch (ch) {
+      case 1: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 1>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp); break;
+      case 2: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 2>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp); break;
+      case 4: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 4>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  const int64_t threads = n_out * (c_out / tile);
+  const dim3 g(blocks_for(threads)), b(kThreads);
   switch (tile) {
 #define SPC_SC(T)                                                                                    \
   case T:                                                                                            \

@@ -33,6 +33,7 @@ unsigned grid_for(int64_t n, int per_block = kThreads, int64_t cap = 1 << 20) {
 // Coordinate bounds: per-block partial min / max, then one block reduces them.
 // ----------------------------------------------------------------------------
 constexpr int kMinmaxBlocks = 256;
+constexpr int kMinmaxBatch = 8;  // rows in flight per thread
 
 // Per-block bounds of the coordinates; the host reduces the partials (it has to
 // wait for them anyway, to lay out the keys).  Block 0 also resets the control
@@ -48,13 +49,24 @@ __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int6
   int32_t mn[4] = {INT_MAX, INT_MAX, INT_MAX, INT_MAX};
   int32_t mx[4] = {INT_MIN, INT_MIN, INT_MIN, INT_MIN};
   const int64_t n = na + nb;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const int4 v = (i < na) ? a[i] : b[i - na];
-    const int32_t c[4] = {v.x, v.y, v.z, v.w};
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  // batches of kMinmaxBatch rows per thread, all requested before the first is used
+  // (rows past n re-read row n - 1, which leaves the bounds unchanged)
+  for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += kMinmaxBatch * stride) {
+    int4 v[kMinmaxBatch];
 #pragma unroll
-    for (int f = 0; f < 4; ++f) {
-      mn[f] = min(mn[f], c[f]);
-      mx[f] = max(mx[f], c[f]);
+    for (int u = 0; u < kMinmaxBatch; ++u) {
+      const int64_t i = min(i0 + u * stride, n - 1);
+      v[u] = *((i < na) ? a + i : b + (i - na));
+    }
+#pragma unroll
+    for (int u = 0; u < kMinmaxBatch; ++u) {
+      const int32_t c[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+      for (int f = 0; f < 4; ++f) {
+        mn[f] = min(mn[f], c[f]);
+        mx[f] = max(mx[f], c[f]);
+      }
     }
   }
 #pragma unroll
@@ -428,14 +440,17 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
   h[threadIdx.x] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * (kThreads * ITEMS);
+  // all of the thread's keys are requested before the first is used (lanes past n
+  // re-read the last key and are masked out of the counts)
+  uint64_t key[ITEMS];
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) key[r] = load_key<FROM_COORDS>(keys, coords, L, min(base + r * kThreads + threadIdx.x, n - 1));
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
-    const int64_t i = base + r * kThreads + threadIdx.x;
-    if (i < n) {
-      const uint32_t d = (uint32_t)(load_key<FROM_COORDS>(keys, coords, L, i) >> shift) & 255u;
-      const uint64_t peers = match_digit(d);
-      if ((peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)popc64(peers));
-    }
+    const bool valid = base + r * kThreads + threadIdx.x < n;
+    const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
+    const uint64_t peers = match_digit(d, valid);
+    if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)popc64(peers));
   }
   __syncthreads();
   if (TILE_MAJOR)
@@ -663,49 +678,50 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
 // order, and o, the pair's GEMM buffer row, is also stored in both metadata
 // tables (T_q in place of the source position, T_s at the source position).
 // ----------------------------------------------------------------------------
-struct ItemRange {
-  int k;
-  int64_t b, q0, q1;
-};
-
-__device__ __forceinline__ ItemRange locate_item(const SearchArgs& a, int64_t w, int64_t nb, const uint32_t* bounds,
-                                                 const uint32_t* istart, int64_t* s_kb) {
-  if (threadIdx.x < kWave) {
-    // last (k, b) whose first item index is <= w
-    const int64_t kb = wave_upper_bound<uint32_t, int64_t>(istart, (int64_t)a.K3 * nb, w) - 1;
-    if (threadIdx.x == 0) *s_kb = kb;
+// Sorted position of ROUNDS independent keys at once in the LDS block, by binary
+// lifting: the block holds 2^LOG2B + 1 keys, padded past its nB real keys with
+// the largest key (never smaller than a query), so no step needs a bounds check.
+// Positions are kept as byte offsets and every step's distance is a constant, so
+// a step is one LDS read, one 64-bit compare and one select per key, and the
+// ROUNDS reads of a step are issued together.  pos = number of keys < key (at
+// most 2^LOG2B - 1; then the final probe tells a hit from a key past the block),
+// hit = whether the key is present.
+template <int ROUNDS, int LOG2B>
+__device__ __forceinline__ void lds_search(const uint64_t* lkey, const uint64_t (&key)[ROUNDS], int (&pos)[ROUNDS],
+                                           bool (&hit)[ROUNDS]) {
+  const char* base = reinterpret_cast<const char*>(lkey);
+  uint32_t off[ROUNDS];
+#pragma unroll
+  for (int r = 0; r < ROUNDS; ++r) off[r] = 0;
+#pragma unroll
+  for (int step = 1 << (LOG2B - 1); step > 0; step >>= 1) {
+    uint64_t v[ROUNDS];
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) v[r] = *reinterpret_cast<const uint64_t*>(base + off[r] + 8 * (step - 1));
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) off[r] += (v[r] < key[r]) ? 8u * step : 0u;
   }
-  __syncthreads();
-  const int64_t kb = *s_kb;
-  ItemRange r;
-  r.k = (int)(kb / nb);
-  r.b = kb - (int64_t)r.k * nb;
-  const int64_t blo = (r.b == 0) ? 0 : (int64_t)bounds[kb - 1];
-  const int64_t bhi = bounds[kb];
-  r.q0 = blo + (w - (int64_t)istart[kb]) * a.Cq;
-  r.q1 = min(r.q0 + (int64_t)a.Cq, bhi);
-  return r;
-}
-
-__device__ __forceinline__ int lds_lower(const uint64_t* lkey, int nB, int log2B, uint64_t key) {
-  // number of LDS keys < key, by binary lifting over a power-of-two range
-  int pos = 0;
-  for (int step = 1 << (log2B - 1); step > 0; step >>= 1)
-    if (pos + step <= nB && lkey[pos + step - 1] < key) pos += step;
-  if (pos < nB && lkey[pos] < key) ++pos;
-  return pos;
+  uint64_t v[ROUNDS];
+#pragma unroll
+  for (int r = 0; r < ROUNDS; ++r) v[r] = *reinterpret_cast<const uint64_t*>(base + off[r]);
+#pragma unroll
+  for (int r = 0; r < ROUNDS; ++r) {
+    hit[r] = v[r] == key[r];
+    pos[r] = (int)(off[r] >> 3);
+  }
 }
 
 // Forward search, write pass: one workgroup per work item.  The count pass left
-// each query's result in T_q (matching sorted source position, or -1); matches
-// are ranked with wave ballots from the item's scanned match offset, so every
-// offset's pairs come out in sorted-query order, and pair index o (the pair's
-// GEMM buffer row) replaces the source position in T_q and is stored in T_s.
+// each query's result in T_q (matching sorted source position, or -1) and the
+// item's query range in item_desc; matches are ranked with wave ballots from the
+// item's scanned match offset, so every offset's pairs come out in sorted-query
+// order, and pair index o (the pair's GEMM buffer row) replaces the source
+// position in T_q and is stored in T_s.  The loads of all rounds are issued
+// together: results first, then the rows of the matches.
 template <int ROUNDS>
-__global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const uint32_t* bounds, int64_t nb,
-                                                            const uint32_t* istart, const uint32_t* item_off,
-                                                            int32_t* pin, int32_t* pout, ControlBlock* cb) {
-  __shared__ int64_t s_kb;
+__global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const uint32_t* istart, int64_t nb,
+                                                            const uint32_t* item_off, int32_t* pin, int32_t* pout,
+                                                            ControlBlock* cb) {
   __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -722,34 +738,40 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
   }
   if (w >= n_items) return;  // workgroup-uniform: the grid is sized for the worst case
 
-  const ItemRange it = locate_item(a, w, nb, bounds, istart, &s_kb);
-  int32_t* res = a.res + (int64_t)it.k * a.res_stride;
-  int32_t r_in[ROUNDS], r_out[ROUNDS], r_sp[ROUNDS];
-  uint64_t bal[ROUNDS];
-  // mirrored offset's T_s row, for the misses of a symmetric map
-  int32_t* ts_mirror = a.ts + (int64_t)(a.K3 - 1 - it.k) * a.ts_stride;
+  const uint2 d = a.item_desc[w];
+  const uint64_t base = item_off[w];
+  const int64_t q0 = d.x;
+  const int64_t q1 = q0 + (d.y & 0xFFFFu);
+  const int k = (int)(d.y >> 16);
+  int32_t* res = a.res + (int64_t)k * a.res_stride;
+  int32_t sp[ROUNDS];
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
-    const int64_t qp = it.q0 + (int64_t)r * kThreads + tid;
-    bool hit = false;
-    r_in[r] = 0;
-    r_out[r] = 0;
-    r_sp[r] = -1;
-    if (qp < it.q1) {
-      const int32_t sp = res[qp];
-      if (sp >= 0) {
-        hit = true;
-        r_sp[r] = sp;
-        const int32_t src = (int32_t)a.sidx[sp];
-        const int32_t qry = (int32_t)a.qrow[qp];
-        r_in[r] = a.swap_roles ? qry : src;
-        r_out[r] = a.swap_roles ? src : qry;
-      } else if (a.sym) {
-        ts_mirror[qp] = -1;
-      }
-    }
+    const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+    sp[r] = (qp < q1) ? res[qp] : -1;
+  }
+  int32_t r_in[ROUNDS], r_out[ROUNDS];
+  uint64_t bal[ROUNDS];
+#pragma unroll
+  for (int r = 0; r < ROUNDS; ++r) {
+    // rows of the match (a valid dummy address for lanes without one)
+    const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+    const bool hit = sp[r] >= 0;
+    const int32_t src = (int32_t)a.sidx[hit ? sp[r] : 0];
+    const int32_t qry = (int32_t)a.qrow[hit ? qp : 0];
+    r_in[r] = a.swap_roles ? qry : src;
+    r_out[r] = a.swap_roles ? src : qry;
     bal[r] = __ballot(hit);
     if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal[r]);
+  }
+  if (a.sym) {
+    // mirrored offset's T_s row, for the misses of a symmetric map
+    int32_t* ts_mirror = a.ts + (int64_t)(a.K3 - 1 - k) * a.ts_stride;
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+      const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+      if (qp < q1 && sp[r] < 0) ts_mirror[qp] = -1;
+    }
   }
   __syncthreads();
   uint32_t total = 0;
@@ -762,17 +784,16 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
       total += s_cnt[r][v];
     }
   }
-  const uint64_t base = item_off[w];
-  int32_t* ts = a.ts + (int64_t)it.k * a.ts_stride;
+  int32_t* ts = a.ts + (int64_t)k * a.ts_stride;
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
     if ((bal[r] >> lane) & 1ull) {
       const uint64_t o = base + before[r] + (uint64_t)popc64(bal[r] & lanemask_lt());
-      const int64_t qp = it.q0 + (int64_t)r * kThreads + tid;
+      const int64_t qp = q0 + (int64_t)r * kThreads + tid;
       pin[o] = r_in[r];
       pout[o] = r_out[r];
       res[qp] = (int32_t)o;
-      ts[r_sp[r]] = (int32_t)o;
+      ts[sp[r]] = (int32_t)o;
     }
   }
 }
@@ -781,14 +802,17 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
 // (source block b, group of G offsets) stages block b in LDS once and then runs
 // every work item of (k, b) for the offsets k of its group, chunk by chunk (the
 // items and their order are those of the balance step).  Each chunk stores its
-// queries' results and its match count.  With few source blocks the groups are
-// small, so that the grid still fills the GPU; with many, one workgroup takes
-// all K^3 offsets of its block and reads it from HBM once instead of K^3 times.
-template <int ROUNDS>
+// queries' results, its match count and its query range (for the write pass).
+// With few source blocks the groups are small, so that the grid still fills the
+// GPU; with many, one workgroup takes all K^3 offsets of its block and reads it
+// from HBM once instead of K^3 times.  The block's keys, the first chunk's query
+// keys and its bounds are all requested before the first wait; each chunk's
+// ROUNDS searches run as independent chains.
+template <int ROUNDS, int LOG2B>
 __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const uint32_t* bounds,
                                                             const uint32_t* chunks, int64_t nb,
                                                             const uint32_t* istart, uint32_t* item_cnt,
-                                                            int64_t max_items, int G, ControlBlock* cb, int log2B) {
+                                                            int64_t max_items, int G, ControlBlock* cb) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
   uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
@@ -804,14 +828,47 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
 
   const int64_t s0 = b * (int64_t)a.B;
   const int nB = (int)min((int64_t)a.B, a.n_src - s0);
-  for (int e = tid; e < nB; e += kThreads) lkey[e] = a.skeys[s0 + e];
+  // Requested together before the first wait: the block's first 4 * kThreads keys,
+  // the key before the block (repeat check), the first offset's bounds and the
+  // keys of its first chunk.
+  uint64_t sv[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) sv[u] = a.skeys[s0 + min(u * kThreads + tid, nB - 1)];
+  const uint64_t key_before = a.skeys[s0 > 0 ? s0 - 1 : 0];
+  const int k_first = g * G;
+  const int k_end = min(a.K3, k_first + G);
+  int64_t q_lo = 0, q_hi = 0, first = 0;
+  uint32_t nch = 0;
+  auto load_bounds = [&](int k) {
+    const int64_t kb = (int64_t)k * nb + b;
+    q_lo = (b == 0) ? 0 : (int64_t)bounds[kb - 1];
+    q_hi = bounds[kb];
+    nch = chunks[kb];
+    first = istart[kb];
+  };
+  uint64_t key[ROUNDS];
+  // keys of the chunk [q0, q1) (q0 < q1; lanes past q1 re-read q0)
+  auto load_keys = [&](int64_t q0, int64_t q1, uint64_t dk) {
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+      const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+      key[r] = a.qkeys[qp < q1 ? qp : q0] + dk;
+    }
+  };
+  load_bounds(k_first);
+  if (nch > 0) load_keys(q_lo, min(q_lo + (int64_t)a.Cq, q_hi), (uint64_t)a.dk[k_first]);
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    if (u * kThreads + tid < nB) lkey[u * kThreads + tid] = sv[u];
+  for (int e = 4 * kThreads + tid; e < nB; e += kThreads) lkey[e] = a.skeys[s0 + e];  // B > 4 * kThreads
+  for (int e = nB + tid; e <= (1 << LOG2B); e += kThreads) lkey[e] = ~0ull;   // padding
   __syncthreads();
   if (g == 0) {
     // the sorted source keys must be strictly increasing: equal neighbours are
     // repeated coordinates, decreasing ones an unsorted input declared sorted
     bool dup = false, unsorted = false;
     for (int e = tid; e < nB; e += kThreads) {
-      const uint64_t prev = (e > 0) ? lkey[e - 1] : (s0 > 0 ? a.skeys[s0 - 1] : 0ull);
+      const uint64_t prev = (e > 0) ? lkey[e - 1] : key_before;
       if (e > 0 || s0 > 0) {
         dup |= lkey[e] == prev;
         unsorted |= lkey[e] < prev;
@@ -821,29 +878,23 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
     if (__ballot(unsorted) != 0 && lane == 0) atomicOr(&cb->err, kErrUnsorted);
   }
 
-  const int k_end = min(a.K3, (g + 1) * G);
-  for (int k = g * G; k < k_end; ++k) {
-    const int64_t kb = (int64_t)k * nb + b;
-    const int64_t q_lo = (b == 0) ? 0 : (int64_t)bounds[kb - 1];
-    const int64_t q_hi = bounds[kb];
-    const uint32_t nch = chunks[kb];
-    const int64_t first = istart[kb];
+  for (int k = k_first; k < k_end; ++k) {
+    if (k != k_first) load_bounds(k);
     int32_t* res = a.res + (int64_t)k * a.res_stride;
     const uint64_t dk = (uint64_t)a.dk[k];
     for (uint32_t c = 0; c < nch; ++c) {
       const int64_t q0 = q_lo + (int64_t)c * a.Cq;
       const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
+      if (k != k_first || c != 0) load_keys(q0, q1, dk);
+      int pos[ROUNDS];
+      bool hit[ROUNDS];
+      lds_search<ROUNDS, LOG2B>(lkey, key, pos, hit);
 #pragma unroll
       for (int r = 0; r < ROUNDS; ++r) {
         const int64_t qp = q0 + (int64_t)r * kThreads + tid;
-        bool hit = false;
-        if (qp < q1) {
-          const uint64_t key = a.qkeys[qp] + dk;
-          const int pos = lds_lower(lkey, nB, log2B, key);
-          hit = pos < nB && lkey[pos] == key;
-          res[qp] = hit ? (int32_t)(s0 + pos) : -1;
-        }
-        const uint64_t bal = __ballot(hit);
+        const bool valid = qp < q1;
+        if (valid) res[qp] = hit[r] ? (int32_t)(s0 + pos[r]) : -1;
+        const uint64_t bal = __ballot(valid && hit[r]);
         if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal);
       }
       __syncthreads();
@@ -854,6 +905,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
 #pragma unroll
           for (int v = 0; v < kWavesPerBlock; ++v) total += s_cnt[r][v];
         item_cnt[first + c] = total;
+        a.item_desc[first + c] = make_uint2((uint32_t)q0, (uint32_t)(q1 - q0) | ((uint32_t)k << 16));
       }
       __syncthreads();  // s_cnt is rewritten by the next chunk
     }
@@ -861,20 +913,30 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
 }
 
 template <int ROUNDS>
-hipError_t forward_count_t(unsigned grid, size_t lds, hipStream_t s, const SearchArgs& a, const uint32_t* bounds,
+hipError_t forward_count_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds,
                            const uint32_t* chunks, int64_t nb, const uint32_t* istart, uint32_t* item_cnt,
                            int64_t max_items, int G, ControlBlock* cb, int log2B) {
-  hipLaunchKernelGGL((k_forward_count<ROUNDS>), dim3(grid), dim3(kThreads), lds, s, a, bounds, chunks, nb, istart,
-                     item_cnt, max_items, G, cb, log2B);
+  // the block plus its padding: 2^log2B + 1 keys
+  const size_t lds = (((size_t)1 << log2B) + 1) * sizeof(uint64_t);
+  switch (log2B) {
+#define SPC_FC(L2)                                                                                                 \
+  case L2:                                                                                                         \
+    hipLaunchKernelGGL((k_forward_count<ROUNDS, L2>), dim3(grid), dim3(kThreads), lds, s, a, bounds, chunks, nb,  \
+                       istart, item_cnt, max_items, G, cb);                                                       \
+    break;
+    SPC_FC(6) SPC_FC(7) SPC_FC(8) SPC_FC(9) SPC_FC(10) SPC_FC(11) SPC_FC(12)
+#undef SPC_FC
+    default:
+      return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 template <int ROUNDS>
-hipError_t forward_write_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds, int64_t nb,
-                           const uint32_t* istart, const uint32_t* item_off, int32_t* pin, int32_t* pout,
-                           ControlBlock* cb) {
-  hipLaunchKernelGGL((k_forward_write<ROUNDS>), dim3(grid), dim3(kThreads), 0, s, a, bounds, nb, istart, item_off,
-                     pin, pout, cb);
+hipError_t forward_write_t(unsigned grid, hipStream_t s, const SearchArgs& a, int64_t nb, const uint32_t* istart,
+                           const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb) {
+  hipLaunchKernelGGL((k_forward_write<ROUNDS>), dim3(grid), dim3(kThreads), 0, s, a, istart, nb, item_off, pin, pout,
+                     cb);
   return hipGetLastError();
 }
 
@@ -978,6 +1040,7 @@ __global__ __launch_bounds__(kThreads) void k_hash_count(SearchArgs a, const uin
 #pragma unroll
       for (int v = 0; v < kWavesPerBlock; ++v) total += s_cnt[r][v];
     item_cnt[w] = total;
+    a.item_desc[w] = make_uint2((uint32_t)q0, (uint32_t)(q1 - q0) | ((uint32_t)k << 16));
   }
 }
 
@@ -1219,10 +1282,10 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
     const unsigned grid = (unsigned)(max_items > 0 ? max_items : 1);
     ProfScope ps(KN_FORWARD_WRITE, s);
     switch (rounds) {
-      case 1: return forward_write_t<1>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
-      case 2: return forward_write_t<2>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
-      case 4: return forward_write_t<4>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
-      case 8: return forward_write_t<8>(grid, s, a, bounds, nb, istart, item_off, pin, pout, cb);
+      case 1: return forward_write_t<1>(grid, s, a, nb, istart, item_off, pin, pout, cb);
+      case 2: return forward_write_t<2>(grid, s, a, nb, istart, item_off, pin, pout, cb);
+      case 4: return forward_write_t<4>(grid, s, a, nb, istart, item_off, pin, pout, cb);
+      case 8: return forward_write_t<8>(grid, s, a, nb, istart, item_off, pin, pout, cb);
       default: return hipErrorInvalidValue;
     }
   }
@@ -1231,13 +1294,12 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
   const int G = (int)((a.K3 + ngroups0 - 1) / ngroups0);
   const int64_t ngroups = (a.K3 + G - 1) / G;
   const unsigned grid = (unsigned)(nb * ngroups);
-  const size_t lds = (size_t)a.B * sizeof(uint64_t);
   ProfScope ps(KN_FORWARD_COUNT, s);
   switch (rounds) {
-    case 1: return forward_count_t<1>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
-    case 2: return forward_count_t<2>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
-    case 4: return forward_count_t<4>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
-    case 8: return forward_count_t<8>(grid, lds, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 1: return forward_count_t<1>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 2: return forward_count_t<2>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 4: return forward_count_t<4>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 8: return forward_count_t<8>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
     default: return hipErrorInvalidValue;
   }
 }

@@ -230,6 +230,42 @@ def test_grouping_tiles_partials_are_result_neutral():
     assert e32 <= TOL["f16"] and e16 <= TOL["f16"] / 3
 
 
+@pytest.mark.parametrize("K,c_out,pd", [
+    (3, 16, 0),     # two lanes per output row, 32 groups per wave
+    (3, 96, 0),     # 12 lanes per row: five groups per wave, four idle lanes
+    (5, 64, 0),     # 125 offsets: several table batches per lane
+    (3, 512, 0),    # one wave per row
+    (3, 1024, 0),   # two vectors per lane
+    (3, 256, 1),    # float32 partials: four channels per lane
+    (5, 16, 1),
+])
+def test_row_scatter_matches_tiled_and_oracle(K, c_out, pd):
+    """The row-group scatter (default tile) and the tiled scatter sum the same
+    partials in the same offset order: identical outputs, also with the fused
+    residual + ReLU epilogue; both within tolerance of the oracle."""
+    say(f"row scatter K={K} c_out={c_out} partials={'f32' if pd else 'f16'}")
+    c = _cloud(70 + K, 3000, -6, 6)
+    x = scenes.features(len(c), 32, "f16", 71)
+    w = scenes.weights(K, 32, c_out, "f16", 72)
+    km = B.KernelMap.build(to_dev(c), K)
+    xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
+    res = to_dev(scenes.features(len(c), c_out, "f16", 73), "f16")
+    row = B.Options.make(partial_dtype=pd)
+    tiled = B.Options.make(partial_dtype=pd, t_scatter=16)
+    assert km.plan(32, c_out, torch.float16, row).t_scatter == (4 if pd else 8)
+    y_row = B.Forward(km, 32, c_out, torch.float16, row)(xd, wd)
+    y_tiled = B.Forward(km, 32, c_out, torch.float16, tiled)(xd, wd)
+    assert torch.equal(y_row, y_tiled)
+    e_row = B.Forward(km, 32, c_out, torch.float16, row)(xd, wd, residual=res, relu=True)
+    e_tiled = B.Forward(km, 32, c_out, torch.float16, tiled)(xd, wd, residual=res, relu=True)
+    assert torch.equal(e_row, e_tiled)
+    okm = oracle.kernel_map(c, None, K, 1, "subm")
+    ref = oracle.features(scenes.to_f64(x, "f16"), scenes.to_f64(w, "f16"), okm)
+    assert rel_err(to_f64(y_row), ref) <= TOL["f16"]
+    ref_e = np.maximum(ref + to_f64(res), 0.0)
+    assert rel_err(to_f64(e_row), ref_e) <= TOL["f16"]
+
+
 @pytest.mark.parametrize("dtype,c_in,c_out,pd", [
     ("f32", 16, 32, 0),     # fallback kernel
     ("f16", 16, 16, 0),     # half of one 32-deep k-step is padding

@@ -12,7 +12,8 @@ Measurement:
   1. an untimed pass with HIP events around every phase and kernel launch gives
      the per-phase split (Map ms, GMaS ms) and picks the dominant kernel (most
      GPU time per step);
-  2. the timed steps record HIP events only around that kernel's launches, on the
+  2. the timed steps record HIP events only around that kernel's launches (in one of
+     every five steps, so that the event records do not load every step), on the
      stream it runs on; its algorithmic bytes (or flops) per launch over the mean
      launch duration give the roofline figure.
 """
@@ -32,6 +33,7 @@ HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}
 MAP_PHASES = ("bounds", "sort", "hash", "outcoords", "backward", "balance", "metadata", "forward", "readback")
 GMAS_PHASES = ("gather", "gemm", "scatter")
+EVENT_EVERY = 5  # timed steps per step with events around the dominant kernel
 
 
 def parse():
@@ -214,19 +216,27 @@ def main():
                 kern[name] = (ms / R, cnt / R)
     dominant = max(kern, key=lambda k: kern[k][0])
 
-    # 2. timed steps; events only around the dominant kernel's launches
-    B.spconv_profile_enable(1 << ids[dominant])
+    # 2. timed steps; events only around the dominant kernel's launches, in every
+    #    EVENT_EVERY-th step (each event record costs the host a few microseconds,
+    #    which would otherwise be charged to every step)
+    mask = 1 << ids[dominant]
+    sampled = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        on = i % EVENT_EVERY == 0
+        if on:
+            B.spconv_profile_enable(mask)
+            sampled += 1
         step()
+        if on:
+            B.spconv_profile_enable(False)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    B.spconv_profile_enable(False)
     live = B.spconv_profile_read(reset=True)[dominant]
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     mean_launch_ms = live[0] / live[1]
-    launches_per_step = live[1] / args.steps
+    launches_per_step = live[1] / sampled
 
     k3 = L.K ** 3
     passes = int(round(kern.get("k_radix_scatter", (0, 0))[1]))
@@ -250,7 +260,8 @@ def main():
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 5), "traffic": None, "kernel": dominant,
                 "algorithmic_flops_per_launch": work}
-    roof.update({"mean_launch_ms": round(mean_launch_ms, 6), "launches_per_step": launches_per_step})
+    roof.update({"mean_launch_ms": round(mean_launch_ms, 6), "launches_per_step": launches_per_step,
+                 "timed_launches": int(live[1]), "event_steps": f"1 in {EVENT_EVERY} timed steps"})
     tb = measured_traffic(dominant, wl.name)
     roof["traffic"] = round(tb) if tb is not None else None
 

@@ -133,8 +133,10 @@ def _ptr(t: torch.Tensor | None):
 
 
 def _stream(stream=None):
-    s = torch.cuda.current_stream() if stream is None else stream
-    return ctypes.c_void_p(s.cuda_stream)
+    if stream is None:
+        # the current stream's raw handle, without building a Stream object
+        return ctypes.c_void_p(torch._C._cuda_getCurrentRawStream(torch.cuda.current_device()))
+    return ctypes.c_void_p(stream.cuda_stream)
 
 
 def _opt(opt: Options | None):

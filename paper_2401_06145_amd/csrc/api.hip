@@ -6,6 +6,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "common.h"
@@ -267,48 +268,6 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   return align_up(m.off, 256);
 }
 
-int bit_length(uint64_t v) {
-  int b = 0;
-  while (v) {
-    ++b;
-    v >>= 1;
-  }
-  return b;
-}
-
-// Key layout from coordinate bounds; pad = kernel reach plus the Eq. 1 cell.
-int make_layout(const int32_t mn[4], const int32_t mx[4], int K, int stride, int t, KeyLayout* L) {
-  const int64_t pad = (int64_t)t * (K - 1) + (int64_t)t * stride;
-  int width[4];
-  for (int f = 0; f < 4; ++f) {
-    const int64_t p = (f == 0) ? 0 : pad;
-    const int64_t lo = (int64_t)mn[f] - p;
-    const int64_t hi = (int64_t)mx[f] + p;
-    L->lo[f] = lo;
-    width[f] = bit_length((uint64_t)(hi - lo));
-    L->width[f] = width[f];
-  }
-  L->shift[3] = 0;
-  L->shift[2] = width[3];
-  L->shift[1] = width[3] + width[2];
-  L->shift[0] = width[3] + width[2] + width[1];
-  L->total_bits = width[0] + width[1] + width[2] + width[3];
-  if (L->total_bits > 62) return fail(SPCONV_ERANGE, "coordinate extent (plus kernel reach) needs more than 62 key bits");
-  return SPCONV_OK;
-}
-
-// Delta(K, t): offset k = ix K^2 + iy K + iz is t * (ix - c, iy - c, iz - c).
-void offset_deltas(int K, int t, const KeyLayout& L, int64_t* dk) {
-  const int c = (K % 2 == 1) ? (K - 1) / 2 : 0;
-  int k = 0;
-  for (int ix = 0; ix < K; ++ix)
-    for (int iy = 0; iy < K; ++iy)
-      for (int iz = 0; iz < K; ++iz, ++k) {
-        const int64_t dx = (int64_t)t * (ix - c), dy = (int64_t)t * (iy - c), dz = (int64_t)t * (iz - c);
-        dk[k] = dx * ((int64_t)1 << L.shift[1]) + dy * ((int64_t)1 << L.shift[2]) + dz * ((int64_t)1 << L.shift[3]);
-      }
-}
-
 int check_map_args(int64_t n_in, int64_t n_out, int K, int stride, int t, int mode) {
   if (K < 1 || K > 5) return fail(SPCONV_EUNSUPPORTED, "K must be in [1, 5]");
   if (t < 1) return fail(SPCONV_EINVAL, "tensor_stride must be >= 1");
@@ -472,9 +431,32 @@ size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode, 
   return plan_map(nullptr, n_src, nq_max, K * K * K, tu, mode, &b);
 }
 
-int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords, int64_t n_out, int K,
-                     int stride, int tensor_stride, int mode, const spconv_options* opt, void* d_workspace,
-                     size_t ws_bytes, void* stream, spconv_map** out_map) {
+}  // extern "C"
+
+namespace {
+
+// Sort passes to plan for a build before its key layout is known (the layout is
+// computed on the device, so the host never waits for the bounds): the count the
+// same inputs needed last time, else the last count needed on this thread (start:
+// 4 passes, a 32-bit key).  A build whose key turns out wider is redone with the
+// passes it needs.
+struct PassHint {
+  std::unordered_map<std::string, int> by_input;
+  int last = 4;
+};
+thread_local PassHint g_pass_hint;
+
+std::string pass_key(const int32_t* a, int64_t na, const int32_t* b, int64_t nb, int K, int stride, int t, int mode) {
+  char buf[160];
+  snprintf(buf, sizeof(buf), "%p/%lld/%p/%lld/%d/%d/%d/%d", (const void*)a, (long long)na, (const void*)b,
+           (long long)nb, K, stride, t, mode);
+  return buf;
+}
+
+int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords, int64_t n_out, int K,
+                   int stride, int tensor_stride, int mode, const spconv_options* opt, void* d_workspace,
+                   size_t ws_bytes, void* stream, spconv_map** out_map, int passes, int* passes_needed) {
+  *passes_needed = 0;
   if (!out_map) return fail(SPCONV_EINVAL, "out_map is NULL");
   *out_map = nullptr;
   int st = check_map_args(n_in, mode == SPCONV_UP ? n_out : 0, K, stride, tensor_stride, mode);
@@ -520,22 +502,17 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     delete m;
     return code;
   };
-  KeyLayout L;
+  // key layout on the device (no host wait): bounds partials, then one workgroup
+  const KeyLayout* L = &b.cb->layout;
   {
     PhaseScope ph(PH_BOUNDS, s);
     int np = 0;
     hipError_t e = launch_minmax(d_in_coords, n_in, d_out_coords, mode == SPCONV_UP ? n_out : 0, b.mm_partial,
                                  b.cb, &np, s);
-    int32_t* h = static_cast<int32_t*>(staging(65536));
-    if (!h) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
-    if (e == hipSuccess) e = hipMemcpyAsync(h, b.mm_partial, (size_t)np * 8 * sizeof(int32_t), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    // builds that do not sort the keys take any key width (up to 62 bits)
+    const int plan = (tu.hash || (tu.presorted && mode != SPCONV_DOWN)) ? 8 : passes;
+    if (e == hipSuccess) e = launch_layout(b.mm_partial, np, K, stride, tensor_stride, K3, plan, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "coordinate bounds"));
-    int32_t mm[8];
-    for (int f = 0; f < 8; ++f) mm[f] = h[f];
-    for (int i = 1; i < np; ++i)
-      for (int f = 0; f < 8; ++f) mm[f] = (f < 4) ? std::min(mm[f], h[i * 8 + f]) : std::max(mm[f], h[i * 8 + f]);
-    if ((st = make_layout(mm, mm + 4, K, stride, tensor_stride, &L)) != SPCONV_OK) return bail(st);
   }
   if (tu.hash) {
     PhaseScope ph(PH_HASH, s);
@@ -545,11 +522,11 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     PhaseScope ph(PH_SORT, s);
     // sorted inputs (a previous layer's outputs) only need their keys packed (Section 5.1.1)
     hipError_t e = tu.presorted ? launch_pack(src_coords, n_src, L, b.skeys, b.sidx, s)
-                                : radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, L.total_bits,
+                                : radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, passes,
                                                 b.sort_tmp, &b.cb->err, s);
     if (e == hipSuccess && mode == SPCONV_UP)
       e = tu.presorted ? launch_pack(d_in_coords, n_in, L, b.qkeys, b.qrow, s)
-                       : radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, L.total_bits,
+                       : radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, passes,
                                        b.sort_tmp, &b.cb->err, s);
     if (e != hipSuccess) return bail(hip_fail(e, "sort"));
   }
@@ -558,7 +535,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     const int64_t cell = (int64_t)tensor_stride * stride;
     hipError_t e = launch_down_keys(b.skeys, n_src, L, cell, b.dkeys, b.dvals, s);
     if (e == hipSuccess)
-      e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, L.total_bits, b.sort_tmp,
+      e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, passes, b.sort_tmp,
                         &b.cb->err, s);
     if (e == hipSuccess)
       e = unique_keys(b.dkeys, n_src, L, b.flags, b.pos, b.scan_tmp, b.qkeys, b.qrow, b.qcoords, b.cb, s);
@@ -575,7 +552,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   a.n_q = nq_max;
   a.n_q_dev = (mode == SPCONV_DOWN) ? &b.cb->n_q : nullptr;
   a.K3 = K3;
-  offset_deltas(K, tensor_stride, L, a.dk);
+  a.dk = b.cb->dk;
   a.B = tu.B;
   a.Cq = tu.Cq;
   a.swap_roles = (mode == SPCONV_UP) ? 1 : 0;
@@ -586,6 +563,7 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   a.ts_stride = n_src;
   a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
   a.item_desc = b.item_desc;
+  a.pair_cap = (int64_t)K3 * nq_max;
   // the hash-table search treats all queries of an offset as one block
   const int64_t nb = tu.hash ? 1 : b.nb;
   {
@@ -620,9 +598,17 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
     PhaseScope ph(PH_READBACK, s);
     ControlBlock* hc = static_cast<ControlBlock*>(staging(65536));
     if (!hc) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
-    hipError_t e = hipMemcpyAsync(hc, b.cb, sizeof(ControlBlock), hipMemcpyDeviceToHost, s);
+    hipError_t e = hipMemcpyAsync(hc, b.cb, kControlHeadBytes, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return bail(hip_fail(e, "count read-back"));
+    if (hc->err & kErrRange)
+      return bail(fail(SPCONV_ERANGE, "coordinate extent (plus kernel reach) needs more than 62 key bits"));
+    if (hc->err & kErrWide) {
+      // the key is wider than the sort planned for: the caller redoes the build
+      *passes_needed = (hc->layout.total_bits + 7) / 8;
+      return bail(SPCONV_OK);
+    }
+    *passes_needed = (hc->layout.total_bits + 7) / 8;
     if (hc->err & kErrDup) return bail(fail(SPCONV_EDUP, "duplicate coordinates"));
     if (hc->err & kErrOverflow) return bail(fail(SPCONV_EHIP, "overflow of the work items or of the hash table"));
     if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "a look-back exceeded its wait bound"));
@@ -660,6 +646,35 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   }
   *out_map = m;
   return SPCONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords, int64_t n_out, int K,
+                     int stride, int tensor_stride, int mode, const spconv_options* opt, void* d_workspace,
+                     size_t ws_bytes, void* stream, spconv_map** out_map) {
+  PassHint& hint = g_pass_hint;
+  const std::string key = pass_key(d_in_coords, n_in, d_out_coords, n_out, K, stride, tensor_stride, mode);
+  const auto it = hint.by_input.find(key);
+  int passes = (it != hint.by_input.end()) ? it->second : hint.last;
+  int needed = 0;
+  int st = build_map_impl(d_in_coords, n_in, d_out_coords, n_out, K, stride, tensor_stride, mode, opt, d_workspace,
+                          ws_bytes, stream, out_map, passes, &needed);
+  if (st == SPCONV_OK && !*out_map && needed > passes) {
+    // the key needs more passes than planned: redo with the count it needs
+    passes = needed;
+    st = build_map_impl(d_in_coords, n_in, d_out_coords, n_out, K, stride, tensor_stride, mode, opt, d_workspace,
+                        ws_bytes, stream, out_map, passes, &needed);
+    if (st == SPCONV_OK && !*out_map) return fail(SPCONV_EHIP, "key layout changed between two builds");
+  }
+  if (needed > 0) {
+    if (hint.by_input.size() >= 256) hint.by_input.clear();
+    hint.by_input[key] = needed;
+    hint.last = needed;
+  }
+  return st;
 }
 
 int spconv_map_transpose(const spconv_map* down, spconv_map** out_map) {

@@ -55,6 +55,8 @@ enum : uint32_t {
   kErrSpin = 2u,         // a look-back wait exceeded its bound
   kErrOverflow = 4u,     // more work items than the launch was sized for
   kErrUnsorted = 8u,     // rows declared sorted are not in (b, x, y, z) order
+  kErrRange = 16u,       // the coordinate extent plus kernel reach needs more than 62 key bits
+  kErrWide = 32u,        // the key needs more bits than the sort passes planned by the host
 };
 
 // Small control block in device memory, read back once at the end of a map build.
@@ -65,7 +67,12 @@ struct ControlBlock {
   uint32_t n_items;       // forward-search work items of the balance step
   uint32_t n_pairs;       // total matches
   uint32_t seg_pair_start[kMaxOffsets + 3];  // first pair of offset k; [K3] = n_pairs
+  KeyLayout layout;       // key layout, computed on the device from the coordinate bounds
+  int64_t dk[kMaxOffsets];  // packed key delta of each offset under that layout
 };
+// The part of the control block the host reads back after a build (counts, flags,
+// the layout's width); the offset deltas stay on the device.
+constexpr size_t kControlHeadBytes = offsetof(ControlBlock, dk);
 
 // ---------------------------------------------------------------------------
 // Measurement: HIP events around phases and around individual kernel launches,
@@ -103,19 +110,25 @@ size_t minmax_temp_bytes();
 // int32 (min b,x,y,z then max b,x,y,z) in `partial`; also resets cb's counters.
 hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t nb, int32_t* partial,
                          ControlBlock* cb, int* n_partial, hipStream_t s);
-hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals,
+hipError_t launch_pack(const int32_t* coords, int64_t n, const KeyLayout* L, uint64_t* keys, uint32_t* vals,
                        hipStream_t s);
 size_t radix_temp_bytes(int64_t n);
-// Sorts by the low `bits` key bits; the result ends in (keys, vals).  If `coords` is
-// non-null the input is those coordinates (keys packed with L, values = row index).
-// Look-back waits that exceed their bound set kErrSpin in *err (nothing hangs).
-hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals,
-                         uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, int bits, void* d_temp,
+// Device-side key layout from the bounds partials, into cb->layout and cb->dk (see
+// k_layout); flags kErrRange / kErrWide (more than 8 * passes key bits).
+hipError_t launch_layout(const int32_t* partial, int np, int K, int stride, int t, int K3, int passes,
+                         ControlBlock* cb, hipStream_t s);
+// Sorts by the low 8 * passes key bits (passes whose digit lies above the layout's
+// key bits are plain copies); the result ends in (keys, vals).  If `coords` is
+// non-null the input is those coordinates (keys packed with the device layout *L,
+// values = row index).  Look-back waits that exceed their bound set kErrSpin in *err
+// (nothing hangs).
+hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals,
+                         uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, int passes, void* d_temp,
                          uint32_t* err, hipStream_t s);
-hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell,
+hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, const KeyLayout* L, int64_t cell,
                             uint64_t* dkeys, uint32_t* vals, hipStream_t s);
 // Distinct consecutive keys of sorted `keys` -> qkeys, qrow = position, coords; n_q into cb.
-hipError_t unique_keys(const uint64_t* keys, int64_t n, KeyLayout L, uint32_t* flags,
+hipError_t unique_keys(const uint64_t* keys, int64_t n, const KeyLayout* L, uint32_t* flags,
                        uint32_t* pos, void* d_temp, uint64_t* qkeys, uint32_t* qrow,
                        int32_t* out_coords, ControlBlock* cb, hipStream_t s);
 
@@ -128,7 +141,7 @@ struct SearchArgs {
   int64_t n_q;
   const uint32_t* n_q_dev;
   int K3;
-  int64_t dk[kMaxOffsets];  // key delta of each offset
+  const int64_t* dk;      // key delta of each offset (device, from the layout kernel)
   int B;                  // source block size
   int Cq;                 // query block limit
   int swap_roles;         // UP: pairs are (query row, source row)
@@ -146,6 +159,7 @@ struct SearchArgs {
   // Per work item, written by the count pass and read by the write pass:
   // x = first sorted query position, y = query count | (offset << 16).
   uint2* item_desc;
+  int64_t pair_cap;       // capacity of the pair lists (K3 * queries)
   // Submanifold map with odd K: query q misses offset k exactly when source q
   // has no partner at the mirrored offset K^3 - 1 - k, so the write pass marks
   // that T_s entry instead of a separate fill.
@@ -167,7 +181,7 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
 constexpr uint64_t kHashEmpty = ~0ull;
 // Clears the table, packs every input row (caller order) into keys[i] with
 // idx[i] = i, and inserts (key, i); repeated keys set kErrDup in *err.
-hipError_t launch_hash_build(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* hkeys, uint32_t* hvals,
+hipError_t launch_hash_build(const int32_t* coords, int64_t n, const KeyLayout* L, uint64_t* hkeys, uint32_t* hvals,
                              int log2cap, uint64_t* keys, uint32_t* idx, uint32_t* err, hipStream_t s);
 // Work items of the probe: one query block of all n_q queries per offset
 // (bounds[k] = n_q, chunks[k] = its number of Cq chunks), i.e. one source block.

@@ -28,6 +28,8 @@
 // it multiplies the current one.  k_gemm is the general fallback (any c_in,
 // float32) with a narrower column slice per workgroup.
 #include <algorithm>
+#include <mutex>
+#include <vector>
 
 #include "common.h"
 
@@ -504,6 +506,40 @@ hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_o
   return hipGetLastError();
 }
 
+// Workgroups per CU of a wide-GEMM instance and the device's CU count, queried once
+// per (device, kernel, LDS size) and kept (the queries cost the host microseconds
+// on every forward otherwise).
+hipError_t wide_occupancy(const void* fn, size_t lds, int* per_cu, int* cus) {
+  struct Entry {
+    int dev;
+    const void* fn;
+    size_t lds;
+    int per_cu, cus;
+  };
+  static std::mutex mu;
+  static std::vector<Entry> cache;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  {
+    std::lock_guard<std::mutex> lk(mu);
+    for (const Entry& x : cache)
+      if (x.dev == dev && x.fn == fn && x.lds == lds) {
+        *per_cu = x.per_cu;
+        *cus = x.cus;
+        return hipSuccess;
+      }
+  }
+  Entry x{dev, fn, lds, 0, 0};
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&x.per_cu, fn, kWideThreads, lds)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&x.cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  cache.push_back(x);
+  *per_cu = x.per_cu;
+  *cus = x.cus;
+  return hipSuccess;
+}
+
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
                        const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
                        hipStream_t s) {
@@ -524,12 +560,9 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
     lds = (size_t)16 * nt * ldk * 2;
     wfn = wide_kernel_for(dtype, part_dtype, a_rows != nullptr, nt, ks);
     if (!wfn) return hipErrorInvalidValue;
-    int per_cu = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wfn, kWideThreads, lds);
+    int per_cu = 0, cus = 0;
+    hipError_t e = wide_occupancy(wfn, lds, &per_cu, &cus);
     if (e != hipSuccess) return e;
-    int dev = 0, cus = 0;
-    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
     const int64_t slots = (int64_t)std::max(per_cu, 1) * std::max(cus, 1);
     const int round = wide_round_rows(nt, ks);
     const int64_t want = (rows_all + 2 * slots - 1) / (2 * slots);

@@ -34,6 +34,7 @@ unsigned grid_for(int64_t n, int per_block = kThreads, int64_t cap = 1 << 20) {
 // ----------------------------------------------------------------------------
 constexpr int kMinmaxBlocks = 256;
 constexpr int kMinmaxBatch = 8;  // rows in flight per thread
+constexpr int kMaxPartials = kMinmaxBlocks;  // bounds partials reduced by the layout kernel
 
 // Per-block bounds of the coordinates; the host reduces the partials (it has to
 // wait for them anyway, to lay out the keys).  Block 0 also resets the control
@@ -96,11 +97,85 @@ __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int6
 }
 
 
+// Key layout on the device, from the bounds partials: one workgroup reduces them,
+// biases each field by its minimum minus the kernel reach and the Eq. 1 cell (b is
+// never offset), gives it the bit width of its extent, packs the fields b, x, y, z
+// from the most significant end, and writes the layout and the packed key delta
+// of every offset into the control block.  Flags: kErrRange if the key needs more
+// than 62 bits, kErrWide if it needs more than the 8 * passes bits the host
+// planned its sort for.  Nothing waits for the host, so the map build needs no
+// read-back before the sort.
+__device__ __forceinline__ int bit_length_u64(uint64_t v) { return v ? 64 - __clzll((long long)v) : 0; }
+
+__global__ __launch_bounds__(kThreads) void k_layout(const int32_t* partial, int np, int K, int stride, int t,
+                                                     int K3, int passes, ControlBlock* cb) {
+  __shared__ int32_t red[kThreads];
+  __shared__ int32_t mm[8];
+  __shared__ int shift_s[4];
+  const int tid = threadIdx.x;
+  // thread tid reduces field f = tid % 8 over partials tid / 8, tid / 8 + 32, ...
+  // (all of its loads in flight together), then 32 values per field in LDS
+  {
+    const int f = tid & 7;
+    const bool is_min = f < 4;
+    int32_t r = is_min ? INT_MAX : INT_MIN;
+    int32_t v[kMaxPartials / 32];
+#pragma unroll
+    for (int u = 0; u < kMaxPartials / 32; ++u) {
+      const int i = tid / 8 + 32 * u;
+      v[u] = (i < np) ? partial[i * 8 + f] : r;
+    }
+#pragma unroll
+    for (int u = 0; u < kMaxPartials / 32; ++u) r = is_min ? min(r, v[u]) : max(r, v[u]);
+    red[tid] = r;
+  }
+  __syncthreads();
+  if (tid < 8) {
+    int32_t r = red[tid];
+    for (int i = 1; i < 32; ++i) r = (tid < 4) ? min(r, red[i * 8 + tid]) : max(r, red[i * 8 + tid]);
+    mm[tid] = r;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const int64_t pad = (int64_t)t * (K - 1) + (int64_t)t * stride;
+    KeyLayout L;
+    int w[4];
+    for (int f = 0; f < 4; ++f) {
+      const int64_t p = (f == 0) ? 0 : pad;
+      L.lo[f] = (int64_t)mm[f] - p;
+      w[f] = bit_length_u64((uint64_t)((int64_t)mm[4 + f] + p - L.lo[f]));
+      L.width[f] = w[f];
+    }
+    L.total_bits = w[0] + w[1] + w[2] + w[3];
+    uint32_t err = 0;
+    if (L.total_bits > 62) err |= kErrRange;
+    if (L.total_bits > 8 * passes) err |= kErrWide;
+    // shifts stay below 64 even when the extent does not fit (the build then fails)
+    L.shift[3] = 0;
+    L.shift[2] = min(w[3], 63);
+    L.shift[1] = min(w[3] + w[2], 63);
+    L.shift[0] = min(w[3] + w[2] + w[1], 63);
+    cb->layout = L;
+    for (int f = 0; f < 4; ++f) shift_s[f] = L.shift[f];
+    if (err) atomicOr(&cb->err, err);
+  }
+  __syncthreads();
+  // Delta(K, t): offset k = ix K^2 + iy K + iz is t (ix - c, iy - c, iz - c)
+  const int c = (K % 2 == 1) ? (K - 1) / 2 : 0;
+  for (int k = tid; k < K3; k += kThreads) {
+    const int ix = k / (K * K), iy = (k / K) % K, iz = k % K;
+    const int64_t dx = (int64_t)t * (ix - c), dy = (int64_t)t * (iy - c), dz = (int64_t)t * (iz - c);
+    cb->dk[k] = (int64_t)((uint64_t)dx << shift_s[1]) + (int64_t)((uint64_t)dy << shift_s[2]) +
+                (int64_t)((uint64_t)dz << shift_s[3]);
+  }
+}
+
 // ----------------------------------------------------------------------------
 // Key packing helpers
 // ----------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, KeyLayout L, uint64_t* keys,
+__global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, const KeyLayout* __restrict__ Lp, uint64_t* keys,
                                                    uint32_t* vals) {
+  const KeyLayout L = *Lp;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int4 v = c[i];
@@ -298,9 +373,10 @@ __device__ __forceinline__ void tile_place(TileLds<ITEMS>& t, const uint64_t key
 }
 
 template <bool FROM_COORDS>
-__global__ __launch_bounds__(kThreads) void k_radix_upsweep(const uint64_t* keys, const int4* coords, KeyLayout L,
+__global__ __launch_bounds__(kThreads) void k_radix_upsweep(const uint64_t* keys, const int4* coords, const KeyLayout* __restrict__ Lp,
                                                             int64_t n, int passes, uint32_t* gpart, uint32_t* status,
                                                             int64_t status_words, uint32_t* tickets) {
+  const KeyLayout L = *Lp;
   __shared__ uint32_t h[kRsMaxPasses][256];
   for (int p = 0; p < passes; ++p) h[p][threadIdx.x] = 0;
   __syncthreads();
@@ -355,9 +431,10 @@ __global__ __launch_bounds__(1024) void k_radix_totals(const uint32_t* gpart, in
 
 template <bool FROM_COORDS>
 __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, const uint32_t* vin, const int4* coords,
-                                                         KeyLayout L, uint64_t* kout, uint32_t* vout, int64_t n,
+                                                         const KeyLayout* __restrict__ Lp, uint64_t* kout, uint32_t* vout, int64_t n,
                                                          int pass, const uint32_t* gofs, uint32_t* status,
                                                          uint32_t* tickets, uint32_t* err) {
+  const KeyLayout L = *Lp;
   __shared__ TileLds<kRsItems> t;
   __shared__ uint32_t s_tile;
   const int tid = threadIdx.x;
@@ -434,8 +511,12 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
 constexpr int64_t kFusedScanTiles = 256;
 
 template <bool FROM_COORDS, bool TILE_MAJOR, int ITEMS>
-__global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, KeyLayout L,
+__global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, const KeyLayout* __restrict__ Lp,
                                                          int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
+  const KeyLayout L = *Lp;
+  // a digit above the key's bits is zero for every key: the scatter copies the
+  // tile and needs no histogram
+  if (!FROM_COORDS && shift >= L.total_bits) return;
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
   __syncthreads();
@@ -464,13 +545,26 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
 // Otherwise `offs` is the scanned digit-major histogram.
 template <bool FROM_COORDS, bool FUSED, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t* kin, const uint32_t* vin,
-                                                            const int4* coords, KeyLayout L, uint64_t* kout,
+                                                            const int4* coords, const KeyLayout* __restrict__ Lp, uint64_t* kout,
                                                             uint32_t* vout, int64_t n, int shift,
                                                             const uint32_t* offs, int64_t ntiles) {
+  const KeyLayout L = *Lp;
   __shared__ TileLds<ITEMS> t;
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   const int64_t base = (int64_t)blockIdx.x * (kThreads * ITEMS);
+  if (!FROM_COORDS && shift >= L.total_bits) {
+    // identity pass (the planned pass count exceeds the key's bits): stable copy
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r) {
+      const int64_t i = base + (int64_t)r * kThreads + tid;
+      if (i < n) {
+        kout[i] = kin[i];
+        vout[i] = vin[i];
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
   // the tile's keys are loaded first, so that their latency overlaps the offset sums
@@ -535,8 +629,9 @@ __device__ __forceinline__ int64_t floor_to_cell(int64_t v, int64_t cell) {
   return q * cell;
 }
 
-__global__ __launch_bounds__(kThreads) void k_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell,
+__global__ __launch_bounds__(kThreads) void k_down_keys(const uint64_t* skeys, int64_t n, const KeyLayout* __restrict__ Lp, int64_t cell,
                                                         uint64_t* dkeys, uint32_t* vals) {
+  const KeyLayout L = *Lp;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const uint64_t k = skeys[i];
@@ -554,9 +649,10 @@ __global__ __launch_bounds__(kThreads) void k_unique_flags(const uint64_t* keys,
   flags[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1u : 0u;
 }
 
-__global__ __launch_bounds__(kThreads) void k_unique_write(const uint64_t* keys, int64_t n, KeyLayout L,
+__global__ __launch_bounds__(kThreads) void k_unique_write(const uint64_t* keys, int64_t n, const KeyLayout* __restrict__ Lp,
                                                            const uint32_t* flags, const uint32_t* pos,
                                                            uint64_t* qkeys, uint32_t* qrow, int4* coords) {
+  const KeyLayout L = *Lp;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n || flags[i] == 0) return;
   const uint32_t p = pos[i];
@@ -651,7 +747,10 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
   wave_upper_bound2<uint64_t, int64_t>(a.qkeys, nq, thr_hi, thr_lo, &hi, &lo);
   if (lane == 0) {
     bounds[wid] = (uint32_t)hi;
-    chunks[wid] = (uint32_t)((hi - lo + a.Cq - 1) / a.Cq);
+    // keys that are not in order (a build whose sort was planned too short, or rows
+    // wrongly declared presorted; both are reported) can invert a block's bounds:
+    // such a block gets no work, so no pass reads past the query keys
+    chunks[wid] = (hi > lo) ? (uint32_t)((hi - lo + a.Cq - 1) / a.Cq) : 0u;
   }
   if (k == 0 && a.check_q) {
     // the query keys of a transposed map (the coarse inputs) must be strictly
@@ -790,6 +889,10 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
     if ((bal[r] >> lane) & 1ull) {
       const uint64_t o = base + before[r] + (uint64_t)popc64(bal[r] & lanemask_lt());
       const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+      if (o >= (uint64_t)a.pair_cap) {  // only when keys were out of order (reported)
+        atomicOr(&cb->err, kErrOverflow);
+        continue;
+      }
       pin[o] = r_in[r];
       pout[o] = r_out[r];
       res[qp] = (int32_t)o;
@@ -841,18 +944,19 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
   uint32_t nch = 0;
   auto load_bounds = [&](int k) {
     const int64_t kb = (int64_t)k * nb + b;
-    q_lo = (b == 0) ? 0 : (int64_t)bounds[kb - 1];
     q_hi = bounds[kb];
+    // min(): keys out of order can invert the bounds (the chunks are then empty)
+    q_lo = (b == 0) ? 0 : min((int64_t)bounds[kb - 1], q_hi);
     nch = chunks[kb];
     first = istart[kb];
   };
   uint64_t key[ROUNDS];
-  // keys of the chunk [q0, q1) (q0 < q1; lanes past q1 re-read q0)
+  // keys of the chunk [q0, q1) (lanes past q1 re-read the first key)
   auto load_keys = [&](int64_t q0, int64_t q1, uint64_t dk) {
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) {
       const int64_t qp = q0 + (int64_t)r * kThreads + tid;
-      key[r] = a.qkeys[qp < q1 ? qp : q0] + dk;
+      key[r] = a.qkeys[qp < q1 ? qp : 0] + dk;
     }
   };
   load_bounds(k_first);
@@ -883,7 +987,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
     int32_t* res = a.res + (int64_t)k * a.res_stride;
     const uint64_t dk = (uint64_t)a.dk[k];
     for (uint32_t c = 0; c < nch; ++c) {
-      const int64_t q0 = q_lo + (int64_t)c * a.Cq;
+      const int64_t q0 = min(q_lo + (int64_t)c * a.Cq, q_hi);
       const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
       if (k != k_first || c != 0) load_keys(q0, q1, dk);
       int pos[ROUNDS];
@@ -951,9 +1055,10 @@ __device__ __forceinline__ uint64_t hash_slot(uint64_t key, int log2cap) {
   return (key * 0x9E3779B97F4A7C15ull) >> (64 - log2cap);
 }
 
-__global__ __launch_bounds__(kThreads) void k_hash_insert(const int4* c, int64_t n, KeyLayout L, uint64_t* hkeys,
+__global__ __launch_bounds__(kThreads) void k_hash_insert(const int4* c, int64_t n, const KeyLayout* __restrict__ Lp, uint64_t* hkeys,
                                                           uint32_t* hvals, int log2cap, uint64_t* keys, uint32_t* idx,
                                                           uint32_t* err) {
+  const KeyLayout L = *Lp;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int4 v = c[i];
@@ -1068,7 +1173,14 @@ hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t
   return hipGetLastError();
 }
 
-hipError_t launch_pack(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* keys, uint32_t* vals, hipStream_t s) {
+hipError_t launch_layout(const int32_t* partial, int np, int K, int stride, int t, int K3, int passes,
+                         ControlBlock* cb, hipStream_t s) {
+  ProfScope ps(KN_MINMAX, s);
+  hipLaunchKernelGGL(k_layout, dim3(1), dim3(kThreads), 0, s, partial, np, K, stride, t, K3, passes, cb);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const int32_t* coords, int64_t n, const KeyLayout* L, uint64_t* keys, uint32_t* vals, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   ProfScope ps(KN_PACK, s);
   hipLaunchKernelGGL(k_pack, dim3(grid_for(n)), dim3(kThreads), 0, s, reinterpret_cast<const int4*>(coords), n, L,
@@ -1101,7 +1213,7 @@ namespace {
 // thread: smaller tiles shorten each workgroup's chain while the launch is
 // latency-bound.
 template <int ITEMS>
-hipError_t radix_sort_tiled_t(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+hipError_t radix_sort_tiled_t(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
                               uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
   const int64_t ntiles = (n + kThreads * ITEMS - 1) / (kThreads * ITEMS);
   uint32_t* hist = static_cast<uint32_t*>(d_temp);
@@ -1160,7 +1272,7 @@ hipError_t radix_sort_tiled_t(const int32_t* coords, KeyLayout L, uint64_t* keys
   return hipSuccess;
 }
 
-hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+hipError_t radix_sort_tiled(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
                             uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
   if ((n + kRsTileSmall - 1) / kRsTileSmall <= kFusedScanTiles)
     return radix_sort_tiled_t<kRsItemsSmall>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
@@ -1169,10 +1281,9 @@ hipError_t radix_sort_tiled(const int32_t* coords, KeyLayout L, uint64_t* keys, 
 
 }  // namespace
 
-hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
-                         uint32_t* vals_alt, int64_t n, int bits, void* d_temp, uint32_t* err, hipStream_t s) {
+hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
+                         uint32_t* vals_alt, int64_t n, int passes, void* d_temp, uint32_t* err, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int passes = (bits + 7) / 8;
   if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
   if (n <= 1 || passes == 0) return hipSuccess;
   if (passes > kRsMaxPasses || n >= ((int64_t)1 << 30)) return hipErrorInvalidValue;
@@ -1237,7 +1348,7 @@ hipError_t radix_sort_kv(const int32_t* coords, KeyLayout L, uint64_t* keys, uin
   return hipSuccess;
 }
 
-hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64_t cell, uint64_t* dkeys,
+hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, const KeyLayout* L, int64_t cell, uint64_t* dkeys,
                             uint32_t* vals, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   ProfScope ps(KN_DOWN_KEYS, s);
@@ -1245,7 +1356,7 @@ hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, KeyLayout L, int64
   return hipGetLastError();
 }
 
-hipError_t unique_keys(const uint64_t* keys, int64_t n, KeyLayout L, uint32_t* flags, uint32_t* pos, void* d_temp,
+hipError_t unique_keys(const uint64_t* keys, int64_t n, const KeyLayout* L, uint32_t* flags, uint32_t* pos, void* d_temp,
                        uint64_t* qkeys, uint32_t* qrow, int32_t* out_coords, ControlBlock* cb, hipStream_t s) {
   if (n <= 0) return launch_fill_u32(&cb->n_q, 0u, 1, s);
   ProfScope ps(KN_UNIQUE, s);
@@ -1304,7 +1415,7 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
   }
 }
 
-hipError_t launch_hash_build(const int32_t* coords, int64_t n, KeyLayout L, uint64_t* hkeys, uint32_t* hvals,
+hipError_t launch_hash_build(const int32_t* coords, int64_t n, const KeyLayout* L, uint64_t* hkeys, uint32_t* hvals,
                              int log2cap, uint64_t* keys, uint32_t* idx, uint32_t* err, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(hkeys), 0xFFFFFFFFu, (int64_t)2 << log2cap, s);

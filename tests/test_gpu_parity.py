@@ -104,6 +104,31 @@ def test_negative_and_wide_coordinates():
     _ = rng
 
 
+def test_sort_pass_planning_wide_then_narrow():
+    """The host plans the sort's passes before the device has laid out the keys:
+    a key wider than planned is detected and the build redone with enough passes;
+    a narrower one runs the extra passes as copies.  Wide (41-bit), narrow and
+    wide-again clouds in turn, each checked against the oracle's map; DOWN maps
+    sort their output keys with the same plan."""
+    say("sort pass planning")
+    narrow = _cloud(40, 3000, -8, 8)                       # ~14 key bits
+    wide = _cloud(41, 3000, -8, 8)
+    wide[:, 1] *= 400                                      # x, y, z over ~2^12 each
+    wide[:, 2] *= 300
+    wide[:, 3] *= 500
+    wide[:, 0] += 2                                        # b up to 3
+    assert len(np.unique(wide, axis=0)) == len(wide)
+    for c, mode, K, s_ in ((wide, "subm", 3, 1), (narrow, "subm", 3, 1), (wide, "down", 2, 2),
+                           (narrow, "down", 3, 2), (wide, "subm", 3, 1)):
+        dc = to_dev(c)
+        km = B.KernelMap.build(dc, K, s_, 1, mode)
+        q = oracle.out_coords(c, s_, 1) if mode == "down" else None
+        okm = oracle.kernel_map(c, q, K, 1, mode)
+        assert_map_equal(km, okm)
+        if mode == "down":
+            assert np.array_equal(km.out_coords().cpu().numpy(), q)
+
+
 # ----------------------------------------------------------------------------
 # Hand example and the paper's segment example
 # ----------------------------------------------------------------------------

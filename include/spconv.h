@@ -125,7 +125,11 @@ size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode,
  * output rows in the caller's order for SUBM / UP and in sorted (b,x,y,z) order for
  * DOWN.  The map also holds the metadata tables of the GMaS step.  K^3 * max(n_in,
  * n_out) must stay below 2^31 (int32 pair indices; SPCONV_EUNSUPPORTED otherwise).
- * Synchronises `stream` twice (coordinate bounds, then per-offset counts).
+ * The key layout is computed on the device, so the build synchronises `stream`
+ * once, at its end (per-offset counts and error flags).  The host plans the radix
+ * sort's passes before the layout is known (from the previous build of the same
+ * inputs); a key wider than planned is detected and the build redone, so a first
+ * build of unusually wide coordinates costs two passes over the Map.
  * On success *out_map owns a host object to release with spconv_free_map(). */
 int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords,
                      int64_t n_out, int K, int stride, int tensor_stride, int mode,

@@ -43,7 +43,8 @@ FOLD = [
     (r"k_forward_write\b", "k_forward_write"),
     (r"k_gemm(_wide)?\b", "k_gemm"),
     (r"k_tile_(scan|reduce)\b", "k_scan"),
-    (r"k_minmax_(partial|final)\b", "k_minmax"),
+    (r"k_minmax_(partial|final)\b|k_layout\b", "k_minmax"),
+    (r"k_scatter(_rows)?\b", "k_scatter"),
     (r"k_unique_(flags|write)\b", "k_unique"),
     (r"k_fill_u32\b", "k_fill"),
 ]

@@ -5,7 +5,10 @@
   point clouds, profiles Gather (and Scatter) for R rounds with every admissible
   tile T (a divisor of the channel count that covers whole 16-byte vectors), and
   keeps the fastest.  The sampled clouds are seeded synthetic scenes of the same
-  recipe (the paper samples its dataset).
+  recipe (the paper samples its dataset).  Gather tiles are timed on Algorithm 1's
+  gather kernel (the buffer form).  For Scatter, the tile of one 16-byte partial
+  vector per thread is the row-group kernel (a lane group per output row); the
+  wider tiles are the one-thread-per-output-tile kernel.
 * ``map``: the source-block size B and query-block limit C of the double-traversed
   binary search (Section 5.1.4), swept over powers of two.
 
@@ -76,7 +79,8 @@ def tune_tiles(workloads, rounds: int, samples: int, channels):
                 x = torch.from_numpy(scenes.features(len(coords_np), L.c_in, L.dtype, 7)).to(dev)
                 w = torch.from_numpy(scenes.weights(L.K, L.c_in, L.c_out, L.dtype, 8)).to(dev)
                 for t in tile_candidates(L.c_in, e):
-                    f = B.Forward(km, L.c_in, L.c_out, tdt, B.Options.make(t_gather=t))
+                    # Algorithm 1's gather kernel (the default fuses the gather into the GEMM)
+                    f = B.Forward(km, L.c_in, L.c_out, tdt, B.Options.make(t_gather=t, gather=B.GATHER_BUFFER))
                     ms = _timed(lambda: f(x, w), "k_gather", rounds)
                     res["gather"].setdefault(t, []).append(ms)
                 for t in [t for t in tile_candidates(L.c_out, e) if t <= 64 and (t & (t - 1)) == 0 and t >= 4]:

@@ -125,8 +125,12 @@ size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode,
  * output rows in the caller's order for SUBM / UP and in sorted (b,x,y,z) order for
  * DOWN.  The map also holds the metadata tables of the GMaS step.  K^3 * max(n_in,
  * n_out) must stay below 2^31 (int32 pair indices; SPCONV_EUNSUPPORTED otherwise).
- * The key layout is computed on the device, so the build synchronises `stream`
- * once, at its end (per-offset counts and error flags).  The host plans the radix
+ * The key layout is computed on the device, so the host waits once, at the end
+ * of the build, for the per-offset counts and error flags: the search's last
+ * kernel publishes them into mapped host memory as it starts, and the build
+ * returns while that kernel still writes the pair lists and tables.  Work on
+ * `stream` (or after synchronising it) sees the complete map; other streams must
+ * wait for `stream` first.  The host plans the radix
  * sort's passes before the layout is known (from the previous build of the same
  * inputs); a key wider than planned is detected and the build redone, so a first
  * build of unusually wide coordinates costs two passes over the Map.

@@ -1,6 +1,7 @@
 // Host side of the C-ABI (include/spconv.h): argument checks, workspace plans,
 // the Map-step orchestration (Section 5.1) and the GMaS plan (Section 5.2).
 #include <algorithm>
+#include <chrono>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
@@ -140,22 +141,51 @@ ProfScope::~ProfScope() {
 namespace {
 using PhaseScope = spc::ProfScope;
 
-// Pinned host staging for the two read-backs of a map build (one per thread).
-struct Staging {
-  void* p = nullptr;
-  size_t n = 0;
+// Mapped, coherent host buffer into which a map build's write pass publishes the
+// control block's head (one per thread: a build returns only once it has read
+// it).  Allocated on a thread's first build and kept; the device address of
+// mapped memory is the same on every device.
+struct PubBuffer {
+  uint32_t* host = nullptr;
+  uint32_t* dev = nullptr;
+  uint32_t seq = 0;
 };
-thread_local Staging g_stage;
+thread_local PubBuffer g_pub;
 
-void* staging(size_t bytes) {
-  if (g_stage.n < bytes) {
-    if (g_stage.p) (void)hipHostFree(g_stage.p);
-    g_stage.p = nullptr;
-    g_stage.n = 0;
-    if (hipHostMalloc(&g_stage.p, bytes, hipHostMallocDefault) != hipSuccess) return nullptr;
-    g_stage.n = bytes;
+PubBuffer* pub_buffer() {
+  if (!g_pub.host) {
+    void* p = nullptr;
+    if (hipHostMalloc(&p, kPubBytes, hipHostMallocMapped | hipHostMallocPortable | hipHostMallocCoherent) != hipSuccess)
+      return nullptr;
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, p, 0) != hipSuccess) {
+      (void)hipHostFree(p);
+      return nullptr;
+    }
+    std::memset(p, 0, kPubBytes);
+    g_pub.host = static_cast<uint32_t*>(p);
+    g_pub.dev = static_cast<uint32_t*>(d);
   }
-  return g_stage.p;
+  return &g_pub;
+}
+
+// Waits until the write pass has published sequence number `seq`: spins on the
+// flag for up to 2 ms (the head is published at the start of the pass), then
+// blocks on the stream, after which the flag must be set.
+hipError_t pub_wait(const PubBuffer* pb, uint32_t seq, hipStream_t s, bool* ok) {
+  const uint32_t* flag = pb->host + kPubFlagOffset / 4;
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint32_t spin = 0;; ++spin) {
+    if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) == seq) {
+      *ok = true;
+      return hipSuccess;
+    }
+    if ((spin & 1023u) == 1023u && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(2)) break;
+    __builtin_ia32_pause();
+  }
+  const hipError_t e = hipStreamSynchronize(s);
+  *ok = __atomic_load_n(flag, __ATOMIC_ACQUIRE) == seq;
+  return e;
 }
 
 // ---------------------------------------------------------------------------
@@ -564,6 +594,11 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
   a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
   a.item_desc = b.item_desc;
   a.pair_cap = (int64_t)K3 * nq_max;
+  PubBuffer* pb = pub_buffer();
+  if (!pb) return bail(fail(SPCONV_EHIP, "mapped host buffer allocation failed"));
+  if (++pb->seq == 0) pb->seq = 1;
+  a.pub = pb->dev;
+  a.pub_seq = pb->seq;
   // the hash-table search treats all queries of an offset as one block
   const int64_t nb = tu.hash ? 1 : b.nb;
   {
@@ -595,12 +630,15 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     if (e != hipSuccess) return bail(hip_fail(e, "forward search"));
   }
   {
+    // the head as the write pass published it (the pass may still be running)
     PhaseScope ph(PH_READBACK, s);
-    ControlBlock* hc = static_cast<ControlBlock*>(staging(65536));
-    if (!hc) return bail(fail(SPCONV_EHIP, "pinned staging allocation failed"));
-    hipError_t e = hipMemcpyAsync(hc, b.cb, kControlHeadBytes, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    bool ok = false;
+    hipError_t e = pub_wait(pb, a.pub_seq, s, &ok);
     if (e != hipSuccess) return bail(hip_fail(e, "count read-back"));
+    if (!ok) return bail(fail(SPCONV_EHIP, "the write pass did not publish its counts"));
+    ControlBlock head;
+    std::memcpy(&head, pb->host, kControlHeadBytes);
+    const ControlBlock* hc = &head;
     if (hc->err & kErrRange)
       return bail(fail(SPCONV_ERANGE, "coordinate extent (plus kernel reach) needs more than 62 key bits"));
     if (hc->err & kErrWide) {

@@ -164,7 +164,16 @@ struct SearchArgs {
   // has no partner at the mirrored offset K^3 - 1 - k, so the write pass marks
   // that T_s entry instead of a separate fill.
   int sym;
+  // Mapped, coherent host buffer (or NULL).  The write pass's first workgroup
+  // copies the control block's head (kControlHeadBytes) into it, then stores
+  // pub_seq at byte kPubFlagOffset: the host reads the counts while the rest of
+  // the pass still runs, instead of waiting for the stream.
+  uint32_t* pub;
+  uint32_t pub_seq;
 };
+constexpr size_t kPubFlagOffset = 1024;
+constexpr size_t kPubBytes = 4096;
+static_assert(kControlHeadBytes % 4 == 0 && kControlHeadBytes <= kPubFlagOffset, "head fits before the flag");
 // Section 5.1.2, backward search fused with the per-(k, b) chunk counts of the
 // balancing step (and the duplicate-key check).
 hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, uint32_t* chunks,

@@ -828,12 +828,30 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
   const int64_t w = blockIdx.x;
   const int64_t n_items = cb->n_items;
 
-  if (w == 0 && tid <= a.K3) {
+  if (w == 0 && wave == 0) {
     // per-offset pair counts: the items of offset k are [istart[k nb], istart[(k+1) nb])
-    const int k = tid;
-    const int64_t first = (k < a.K3) ? (int64_t)istart[(int64_t)k * nb] : n_items;
-    const uint64_t off = (first < n_items) ? (uint64_t)item_off[first] : (uint64_t)cb->n_pairs;
-    cb->seg_pair_start[k] = (uint32_t)off;
+    for (int k = lane; k <= a.K3; k += kWave) {
+      const int64_t first = (k < a.K3) ? (int64_t)istart[(int64_t)k * nb] : n_items;
+      const uint32_t off = (first < n_items) ? item_off[first] : cb->n_pairs;
+      cb->seg_pair_start[k] = off;
+      if (a.pub)
+        __hip_atomic_store(&a.pub[offsetof(ControlBlock, seg_pair_start) / 4 + k], off, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+    if (a.pub) {
+      // The rest of the head: every flag that the map can raise is final here but
+      // kErrOverflow of this pass, which only follows keys out of order (flagged
+      // by the count pass).  One wave publishes, so its fence orders all the
+      // stores before the flag.
+      constexpr int kSeg0 = offsetof(ControlBlock, seg_pair_start) / 4;
+      constexpr int kSeg1 = kSeg0 + kMaxOffsets + 3;
+      const uint32_t* head = reinterpret_cast<const uint32_t*>(cb);
+      for (int i = lane; i < (int)(kControlHeadBytes / 4); i += kWave)
+        if (i < kSeg0 || i >= kSeg1) __hip_atomic_store(&a.pub[i], head[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __threadfence_system();
+      if (lane == 0)
+        __hip_atomic_store(&a.pub[kPubFlagOffset / 4], a.pub_seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
   }
   if (w >= n_items) return;  // workgroup-uniform: the grid is sized for the worst case
 

@@ -329,9 +329,21 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
       for (int q = 0; q < KSTEPS; ++q)
         cur[b][q] = __builtin_bit_cast(F, __builtin_bit_cast(u32x4, raw[b][q]) & kmask[q]);
   };
+  // The next round's source rows must be in registers wherever a round starts.
+  // Waited for here and at the end of each round (they were requested before that
+  // round's stores), so the loop head needs no wait: on this chip loads and stores
+  // share one counter, and a wait there would also drain the previous round's
+  // stores before the next operands are requested.
+  auto rows_ready = [&]() {
+    if constexpr (GATHER) {
+#pragma unroll
+      for (int b = 0; b < MB; ++b) asm volatile("" ::"v"(src[b]));
+    }
+  };
   int m0 = m_first;
   fetch_rows(m0 + STEP);
   take(m0);
+  rows_ready();
   for (; m0 < r_end; m0 += STEP) {
     const int m1 = m0 + STEP;
     issue(m1);  // masked to the dummy address past the tile; lands during the MFMAs below
@@ -370,6 +382,7 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
     for (int b = 0; b < MB; ++b)
 #pragma unroll
       for (int q = 0; q < KSTEPS; ++q) asm volatile("" ::"v"(cur[b][q]));
+    rows_ready();
   }
 }
 

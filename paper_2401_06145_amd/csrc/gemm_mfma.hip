@@ -170,12 +170,24 @@ constexpr size_t kLdsMax = 160 * 1024;
 
 // Register blocking of the full-width kernel.  A wave computes MB 16-row blocks
 // times NTW 16-column tiles, so every W^T fragment it reads from LDS feeds MB
-// MFMAs; CG waves split the workgroup's NT = CG * NTW column tiles, the others
-// take further rows.  Measured on gfx950, blocking (MB > 1 or CG > 1) lowers the
-// occupancy more than it saves LDS traffic for these HBM-bound products, so
-// both are 1; the structure stays for other shapes.
+// MFMAs (the W fragment reads, 1 KiB per wave per MFMA at MB = 1, otherwise
+// bound the kernel from 128 columns up); CG waves split the workgroup's NT =
+// CG * NTW column tiles, the others take further rows.  Two row blocks per wave
+// while their operands (and the next blocks' in flight) take at most 128
+// registers: up to 128 input channels (from 160 channels the two blocks and
+// their successors in flight need 160 registers and the kernel spills).  The
+// columns of a two-block wave are produced in NCH chunks of at most 8 tiles, so
+// that operands, accumulators and fragments stay within the 256 registers a
+// wave has at two waves per SIMD.  Measured on gfx950: C = 128 GEMM 0.142 ->
+// 0.132 ms; one block per wave stays faster in one chunk; CG > 1 cost more
+// occupancy than it saved.
 constexpr int wide_cg(int) { return 1; }
-constexpr int wide_mb(int, int) { return 1; }
+constexpr int wide_mb(int, int ksteps) { return ksteps <= 4 ? 2 : 1; }
+constexpr int wide_nch(int ntw, int mb) {
+  int nch = 1;
+  while (mb > 1 && ntw / nch > 8 && ntw % (2 * nch) == 0) nch *= 2;
+  return nch;
+}
 
 // NT = 16-column tiles per workgroup; KSTEPS >= c_in / 32 k-steps of 32 (k past
 // c_in is zero).  w is W, [K^3][c_in][c_out]; wt is NULL or W^T, [K^3][c_out][c_in]
@@ -198,6 +210,9 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   constexpr int CG = wide_cg(NT);
   constexpr int NTW = NT / CG;
   constexpr int MB = wide_mb(NTW, KSTEPS);
+  constexpr int NCH = wide_nch(NTW, MB);
+  constexpr int NTC = NTW / NCH;  // column tiles per chunk
+  static_assert(NTW % NCH == 0, "chunks must split the tiles");
   constexpr int RG = kWideWaves / CG;   // row groups
   constexpr int STEP = RG * MB * 16;    // rows per round of the workgroup
   static_assert(NT % CG == 0, "column groups must split the tiles");
@@ -315,12 +330,12 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   // their results go to the dump row.  The zeroing is an AND with a per-k-step mask
   // the compiler cannot see through: a select on the loaded value lets it sink the
   // loads into the select's branch, after the MFMAs, and the prefetch is lost.
-  u32x4 kmask[KSTEPS];
+  uint32_t kmask[KSTEPS];
 #pragma unroll
   for (int q = 0; q < KSTEPS; ++q) {
     uint32_t m = (32 * q + 8 * sub < c_in) ? 0xFFFFFFFFu : 0u;
     asm("" : "+v"(m));
-    kmask[q] = u32x4{m, m, m, m};
+    kmask[q] = m;
   }
   auto take = [&](int) {
 #pragma unroll
@@ -351,29 +366,35 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
     // keeps the W^T fragment reads inside the loop: hoisted, they would need
     // 4 * NTW * KSTEPS registers and spill
     asm volatile("" ::: "memory");
-    f32x4 acc[MB][NTW];
 #pragma unroll
-    for (int b = 0; b < MB; ++b)
+    for (int ch = 0; ch < NCH; ++ch) {
+      f32x4 acc[MB][NTC];
 #pragma unroll
-      for (int t = 0; t < NTW; ++t) acc[b][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int b = 0; b < MB; ++b)
 #pragma unroll
-    for (int q = 0; q < KSTEPS; ++q) {
-      F wf[NTW];
+        for (int t = 0; t < NTC; ++t) acc[b][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int t = 0; t < NTW; ++t) wf[t] = M::load(lwp + 16 * t * ldk + 32 * q);
+      for (int q = 0; q < KSTEPS; ++q) {
+        // with two row blocks, one k-step's fragments at a time (the scheduler
+        // would otherwise fetch a whole chunk's ahead and spill)
+        if constexpr (MB > 1) asm volatile("" ::: "memory");
+        F wf[NTC];
 #pragma unroll
-      for (int t = 0; t < NTW; ++t)
+        for (int t = 0; t < NTC; ++t) wf[t] = M::load(lwp + 16 * (ch * NTC + t) * ldk + 32 * q);
 #pragma unroll
-        for (int b = 0; b < MB; ++b) acc[b][t] = M::mma(wf[t], cur[b][q], acc[b][t]);
-    }
-    // lanes without a row store into the dump row instead of branching, so the
-    // store count is fixed and the wait for the next blocks below skips the stores
+        for (int t = 0; t < NTC; ++t)
 #pragma unroll
-    for (int b = 0; b < MB; ++b) {
-      const int row = m0 + 16 * b + col;
-      TO* crow = (row < row_lim ? C + (row0 + row) * (int64_t)c_out : dump) + n0 + nw + 4 * sub;
+          for (int b = 0; b < MB; ++b) acc[b][t] = M::mma(wf[t], cur[b][q], acc[b][t]);
+      }
+      // lanes without a row store into the dump row instead of branching, so the
+      // store count is fixed and the wait for the next blocks below skips the stores
 #pragma unroll
-      for (int t = 0; t < NTW; ++t) store4(crow + 16 * t, acc[b][t]);
+      for (int b = 0; b < MB; ++b) {
+        const int row = m0 + 16 * b + col;
+        TO* crow = (row < row_lim ? C + (row0 + row) * (int64_t)c_out : dump) + n0 + nw + 4 * sub;
+#pragma unroll
+        for (int t = 0; t < NTC; ++t) store4(crow + 16 * (ch * NTC + t), acc[b][t]);
+      }
     }
     take(m1);
     // the masked operands are complete here, not at the top of the next round:

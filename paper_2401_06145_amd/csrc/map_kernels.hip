@@ -297,6 +297,38 @@ __device__ __forceinline__ void tile_load(const uint64_t* kin, const uint32_t* v
   }
 }
 
+// The same tile in two steps, so that the loads need not wait for the key
+// layout (device memory written by an earlier kernel): tile_fetch requests the
+// keys, or the coordinates, and the values (lanes past n re-read the last
+// element; later steps mask them out); tile_pack packs fetched coordinates.
+template <bool FROM_COORDS, int ITEMS>
+__device__ __forceinline__ void tile_fetch(const uint64_t* kin, const uint32_t* vin, const int4* coords, int64_t base,
+                                           int64_t n, uint64_t key[ITEMS], int4 crd[ITEMS], uint32_t val[ITEMS]) {
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) {
+    const int64_t i = tile_index<ITEMS>(base, r);
+    const int64_t ic = min(i, n - 1);
+    if constexpr (FROM_COORDS) {
+      crd[r] = coords[ic];
+      val[r] = (uint32_t)i;
+    } else {
+      key[r] = kin[ic];
+      val[r] = vin[ic];
+    }
+  }
+}
+
+template <bool FROM_COORDS, int ITEMS>
+__device__ __forceinline__ void tile_pack(const KeyLayout& L, const int4 crd[ITEMS], uint64_t key[ITEMS]) {
+  if constexpr (FROM_COORDS) {
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r) {
+      const int32_t a[4] = {crd[r].x, crd[r].y, crd[r].z, crd[r].w};
+      key[r] = pack_key(L, a);
+    }
+  }
+}
+
 // Stable ranks within the wave's run: rank[r] = number of earlier keys of the
 // wave with the same digit.  Leaves the wave's digit counts in t.wc[wave] (which
 // must be zero).  No workgroup barrier: a wave's LDS accesses complete in order,
@@ -513,22 +545,39 @@ constexpr int64_t kFusedScanTiles = 256;
 template <bool FROM_COORDS, bool TILE_MAJOR, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, const KeyLayout* __restrict__ Lp,
                                                          int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
-  const KeyLayout L = *Lp;
-  // a digit above the key's bits is zero for every key: the scatter copies the
-  // tile and needs no histogram
-  if (!FROM_COORDS && shift >= L.total_bits) return;
   __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0;
-  __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * (kThreads * ITEMS);
-  // all of the thread's keys are requested before the first is used (lanes past n
-  // re-read the last key and are masked out of the counts)
+  // all of the thread's keys (or coordinates) are requested first, before the key
+  // layout is read (lanes past n re-read the last key and are masked out of the
+  // counts)
   uint64_t key[ITEMS];
-#pragma unroll
-  for (int r = 0; r < ITEMS; ++r) key[r] = load_key<FROM_COORDS>(keys, coords, L, min(base + r * kThreads + threadIdx.x, n - 1));
+  int4 crd[FROM_COORDS ? ITEMS : 1];
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
-    const bool valid = base + r * kThreads + threadIdx.x < n;
+    const int64_t i = min(base + r * kThreads + threadIdx.x, n - 1);
+    if constexpr (FROM_COORDS)
+      crd[r] = coords[i];
+    else
+      key[r] = keys[i];
+  }
+  h[threadIdx.x] = 0;
+  const KeyLayout L = *Lp;
+  // a digit above the key's bits is zero for every key: the scatter copies the
+  // tile and needs no histogram (the tile is counted as empty rather than left by
+  // an early return, which would let the compiler move the key loads after the
+  // layout read)
+  const bool active = FROM_COORDS || shift < L.total_bits;
+  __syncthreads();
+  if constexpr (FROM_COORDS) {
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r) {
+      const int32_t a[4] = {crd[r].x, crd[r].y, crd[r].z, crd[r].w};
+      key[r] = pack_key(L, a);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) {
+    const bool valid = active && base + r * kThreads + threadIdx.x < n;
     const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
     const uint64_t peers = match_digit(d, valid);
     if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)popc64(peers));
@@ -548,30 +597,20 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
                                                             const int4* coords, const KeyLayout* __restrict__ Lp, uint64_t* kout,
                                                             uint32_t* vout, int64_t n, int shift,
                                                             const uint32_t* offs, int64_t ntiles) {
-  const KeyLayout L = *Lp;
   __shared__ TileLds<ITEMS> t;
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   const int64_t base = (int64_t)blockIdx.x * (kThreads * ITEMS);
-  if (!FROM_COORDS && shift >= L.total_bits) {
-    // identity pass (the planned pass count exceeds the key's bits): stable copy
-#pragma unroll
-    for (int r = 0; r < ITEMS; ++r) {
-      const int64_t i = base + (int64_t)r * kThreads + tid;
-      if (i < n) {
-        kout[i] = kin[i];
-        vout[i] = vin[i];
-      }
-    }
-    return;
-  }
-#pragma unroll
-  for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
-  // the tile's keys are loaded first, so that their latency overlaps the offset sums
+  // The tile's keys and the offset sums' loads go out first; the key layout
+  // (needed to pack coordinates, and to tell an identity pass) is read while they
+  // are in flight.
   uint64_t key[ITEMS];
   uint32_t val[ITEMS];
   uint32_t rank[ITEMS];
-  tile_load<FROM_COORDS, ITEMS>(kin, vin, coords, L, base, n, key, val);
+  int4 crd[FROM_COORDS ? ITEMS : 1];
+  tile_fetch<FROM_COORDS, ITEMS>(kin, vin, coords, base, n, key, crd, val);
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
   if (FUSED) {
     // wave v sums tiles v, v + 4, ...; lane l covers digits 4l..4l+3 with 16-byte loads,
     // so all of a wave's loads are independent and in flight together
@@ -613,6 +652,20 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
   } else {
     t.gbase[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
   }
+  const KeyLayout L = *Lp;
+  if (!FROM_COORDS && shift >= L.total_bits) {
+    // identity pass (the planned pass count exceeds the key's bits): stable copy
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r) {
+      const int64_t i = tile_index<ITEMS>(base, r);
+      if (i < n) {
+        kout[i] = key[r];
+        vout[i] = val[r];
+      }
+    }
+    return;
+  }
+  tile_pack<FROM_COORDS, ITEMS>(L, crd, key);
   __syncthreads();  // wc cleared
   tile_rank<ITEMS>(t, key, base, n, shift, rank);
   __syncthreads();
@@ -826,6 +879,10 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
   const int64_t w = blockIdx.x;
+  // requested before the item count is known (the grid covers max_items items,
+  // so w indexes both arrays)
+  const uint2 d = a.item_desc[w];
+  const uint64_t base = item_off[w];
   const int64_t n_items = cb->n_items;
 
   if (w == 0 && wave == 0) {
@@ -855,8 +912,6 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
   }
   if (w >= n_items) return;  // workgroup-uniform: the grid is sized for the worst case
 
-  const uint2 d = a.item_desc[w];
-  const uint64_t base = item_off[w];
   const int64_t q0 = d.x;
   const int64_t q1 = q0 + (d.y & 0xFFFFu);
   const int k = (int)(d.y >> 16);
@@ -940,12 +995,9 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
-  const int64_t b = (int64_t)blockIdx.x % nb;
-  const int g = (int)((int64_t)blockIdx.x / nb);
-  const int64_t n_items = cb->n_items;
-  // items past the last one count zero: the match-count scan runs over max_items
-  for (int64_t i = n_items + (int64_t)blockIdx.x * kThreads + tid; i < max_items; i += (int64_t)gridDim.x * kThreads)
-    item_cnt[i] = 0;
+  // (nb < 2^31: 32-bit division, not the 64-bit software sequence)
+  const int64_t b = (int)blockIdx.x % (int)nb;
+  const int g = (int)blockIdx.x / (int)nb;
 
   const int64_t s0 = b * (int64_t)a.B;
   const int nB = (int)min((int64_t)a.B, a.n_src - s0);
@@ -1032,6 +1084,11 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
       __syncthreads();  // s_cnt is rewritten by the next chunk
     }
   }
+  // items past the last one count zero: the match-count scan runs over max_items
+  // (last, so that the search's loads need not wait for the item count)
+  const int64_t n_items = cb->n_items;
+  for (int64_t i = n_items + (int64_t)blockIdx.x * kThreads + tid; i < max_items; i += (int64_t)gridDim.x * kThreads)
+    item_cnt[i] = 0;
 }
 
 template <int ROUNDS>

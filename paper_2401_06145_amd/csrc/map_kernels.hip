@@ -583,15 +583,17 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
     if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)popc64(peers));
   }
   __syncthreads();
-  if (TILE_MAJOR)
-    hist[(int64_t)blockIdx.x * 256 + threadIdx.x] = h[threadIdx.x];
+  if (TILE_MAJOR)  // 16-bit counts (a tile holds at most kThreads * ITEMS <= 2048 keys)
+    reinterpret_cast<uint16_t*>(hist)[(int64_t)blockIdx.x * 256 + threadIdx.x] = (uint16_t)h[threadIdx.x];
   else
     hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
-// FUSED: `offs` holds tile-major histograms; the first position of digit d in
-// this tile is (keys of smaller digits) + (keys of digit d in earlier tiles).
-// Otherwise `offs` is the scanned digit-major histogram.
+// FUSED: `offs` holds tile-major histograms of 16-bit counts; the first position
+// of digit d in this tile is (keys of smaller digits) + (keys of digit d in
+// earlier tiles).  Every workgroup reads all of them, so their size, not their
+// latency, sets this step's time (measured: 4 of the pass's 8.6 us at 118 tiles
+// of 32-bit counts).  Otherwise `offs` is the scanned digit-major histogram.
 template <bool FROM_COORDS, bool FUSED, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t* kin, const uint32_t* vin,
                                                             const int4* coords, const KeyLayout* __restrict__ Lp, uint64_t* kout,
@@ -612,42 +614,61 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
 #pragma unroll
   for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
   if (FUSED) {
-    // wave v sums tiles v, v + 4, ...; lane l covers digits 4l..4l+3 with 16-byte loads,
-    // so all of a wave's loads are independent and in flight together
+    // A 16-byte load holds 8 counts, so a wave's load covers two tiles: lane l
+    // reads digits 8 (l % 32) .. + 7 of tile 2 p + l / 32 for tile pairs
+    // p = wave, wave + 4, ...; all of a wave's loads are independent and in flight
+    // together.
     const int lane = tid & (kWave - 1);
     const int64_t tile = blockIdx.x;
+    const int half = lane >> 5;
     const uint4* h4 = reinterpret_cast<const uint4*>(offs);
-    uint4 bef = make_uint4(0, 0, 0, 0), tot4 = make_uint4(0, 0, 0, 0);
-    for (int64_t t0 = wave; t0 < ntiles; t0 += 16 * kWavesPerBlock) {
+    uint32_t tot8[8], bef8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tot8[e] = bef8[e] = 0;
+    const int64_t npairs = (ntiles + 1) / 2;
+    for (int64_t p0 = wave; p0 < npairs; p0 += 16 * kWavesPerBlock) {
       uint4 v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
-        const int64_t tt = t0 + (int64_t)u * kWavesPerBlock;
-        v[u] = (tt < ntiles) ? h4[tt * 64 + lane] : make_uint4(0, 0, 0, 0);
+        const int64_t tt = 2 * (p0 + (int64_t)u * kWavesPerBlock) + half;
+        v[u] = (tt < ntiles) ? h4[tt * 32 + (lane & 31)] : make_uint4(0, 0, 0, 0);
       }
+      // the batch is summed on the packed pairs: a 16-bit half gathers at most 16
+      // tiles of at most 2048 keys, so no carry crosses into its neighbour
+      uint32_t tp[4] = {0, 0, 0, 0}, bp[4] = {0, 0, 0, 0};
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
-        const int64_t tt = t0 + (int64_t)u * kWavesPerBlock;
-        tot4.x += v[u].x; tot4.y += v[u].y; tot4.z += v[u].z; tot4.w += v[u].w;
-        if (tt < tile) {
-          bef.x += v[u].x; bef.y += v[u].y; bef.z += v[u].z; bef.w += v[u].w;
-        }
+        const int64_t tt = 2 * (p0 + (int64_t)u * kWavesPerBlock) + half;
+        const bool early = tt < tile;
+        tp[0] += v[u].x; tp[1] += v[u].y; tp[2] += v[u].z; tp[3] += v[u].w;
+        bp[0] += early ? v[u].x : 0u; bp[1] += early ? v[u].y : 0u;
+        bp[2] += early ? v[u].z : 0u; bp[3] += early ? v[u].w : 0u;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        tot8[e] += (tp[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+        bef8[e] += (bp[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
       }
     }
-    // per-wave partial sums -> per-digit sums (thread d); the key stage serves as
-    // scratch (this kernel writes keys straight to their global positions)
+    // per-(wave, half) partial sums -> per-digit sums (thread d); the key stage
+    // serves as scratch (this kernel writes keys straight to their global
+    // positions): 8 rows of 256 counts
     uint32_t* s_part = reinterpret_cast<uint32_t*>(t.key);
-    reinterpret_cast<uint4*>(s_part)[wave * 64 + lane] = tot4;
+    static_assert(sizeof(t.key) >= 2 * kWavesPerBlock * 256 * sizeof(uint32_t), "scratch rows fit the key stage");
+    uint32_t* row = s_part + (2 * wave + half) * 256 + 8 * (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) row[e] = tot8[e];
     __syncthreads();
     uint32_t tot = 0;
 #pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) tot += s_part[w * 256 + tid];
+    for (int w = 0; w < 2 * kWavesPerBlock; ++w) tot += s_part[w * 256 + tid];
     __syncthreads();
-    reinterpret_cast<uint4*>(s_part)[wave * 64 + lane] = bef;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) row[e] = bef8[e];
     __syncthreads();
     uint32_t before = 0;
 #pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) before += s_part[w * 256 + tid];
+    for (int w = 0; w < 2 * kWavesPerBlock; ++w) before += s_part[w * 256 + tid];
     t.gbase[tid] = block_excl256(tot, t.s_wave) + before;
   } else {
     t.gbase[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];

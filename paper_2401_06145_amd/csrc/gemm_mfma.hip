@@ -174,15 +174,17 @@ constexpr size_t kLdsMax = 160 * 1024;
 // bound the kernel from 128 columns up); CG waves split the workgroup's NT =
 // CG * NTW column tiles, the others take further rows.  Two row blocks per wave
 // while their operands (and the next blocks' in flight) take at most 128
-// registers: up to 128 input channels (from 160 channels the two blocks and
-// their successors in flight need 160 registers and the kernel spills).  The
-// columns of a two-block wave are produced in NCH chunks of at most 8 tiles, so
-// that operands, accumulators and fragments stay within the 256 registers a
-// wave has at two waves per SIMD.  Measured on gfx950: C = 128 GEMM 0.142 ->
-// 0.132 ms; one block per wave stays faster in one chunk; CG > 1 cost more
-// occupancy than it saved.
+// registers and the layer is wide enough for the LDS reads to matter: 65 to 128
+// input channels (from 160 channels the two blocks and their successors in
+// flight need 160 registers and the kernel spills).  The columns of a two-block
+// wave are produced in NCH chunks of at most 8 tiles, so that operands,
+// accumulators and fragments stay within the 256 registers a wave has at two
+// waves per SIMD.  Measured on gfx950: C = 128 GEMM 0.142 -> 0.132 ms; at C = 64
+// one block per wave is faster (26.5 vs 28.5 us on the 120k LiDAR layer), at
+// C = 32 the two are equal; one block per wave stays faster in one chunk; CG > 1
+// cost more occupancy than it saved.
 constexpr int wide_cg(int) { return 1; }
-constexpr int wide_mb(int, int ksteps) { return ksteps <= 4 ? 2 : 1; }
+constexpr int wide_mb(int, int ksteps) { return (ksteps == 3 || ksteps == 4) ? 2 : 1; }
 constexpr int wide_nch(int ntw, int mb) {
   int nch = 1;
   while (mb > 1 && ntw / nch > 8 && ntw % (2 * nch) == 0) nch *= 2;

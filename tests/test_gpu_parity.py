@@ -382,6 +382,27 @@ def test_mid_cloud_scanned_sort_offsets():
     assert rel_err(to_f64(y)[rows], ref) <= TOL["f16"]
 
 
+@pytest.mark.parametrize("side", [123, 194])
+def test_sort_with_one_shared_low_digit(side):
+    """Every key shares its lowest radix digit: z takes multiples of 256, so the
+    first pass puts each whole tile in one bin (the largest 16-bit tile and group
+    counts the fused small sorts can meet), and the next pass splits on z's high
+    bits.  side 123: ~121k voxels, 1024-key tiles; side 194: ~301k voxels,
+    2048-key tiles."""
+    say(f"shared low digit, {side}x{side}x8 lattice")
+    g = np.stack(np.meshgrid(np.arange(side), np.arange(side), np.arange(8) * 256, indexing="ij"), -1).reshape(-1, 3)
+    c = np.concatenate([np.zeros((len(g), 1), np.int64), g], 1).astype(np.int32)
+    c = c[np.random.default_rng(side).permutation(len(c))]
+    x = scenes.features(len(c), 16, "f16", side + 1)
+    w = scenes.weights(3, 16, 16, "f16", side + 2)
+    km, y = _conv_gpu(c, x, w, 3, dtype="f16")
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    assert_map_equal(km, okm)
+    rows = np.sort(np.random.default_rng(side + 3).choice(len(c), 2000, replace=False))
+    ref = oracle.features(scenes.to_f64(x, "f16"), scenes.to_f64(w, "f16"), okm, rows=rows)
+    assert rel_err(to_f64(y)[rows], ref) <= TOL["f16"]
+
+
 def test_deterministic_pairs():
     say("deterministic pair order")
     c = scenes.workload(1).coords

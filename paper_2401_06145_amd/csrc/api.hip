@@ -213,6 +213,13 @@ struct MapBufs {
   uint32_t* istart;
   int32_t* res;   // T_q, kept as the map's query-side metadata table
   int32_t* ts;    // T_s, the source-side table
+  // Row strides of the two tables: the point counts rounded up to 32 entries, so
+  // that every row starts on a 128-byte line.  The scatter (and the gather) read
+  // 32 consecutive positions of a row per workgroup; with unpadded rows those
+  // straddled two lines, each shared with a neighbouring workgroup that usually
+  // runs on another die and fetched it again.
+  int64_t res_stride;
+  int64_t ts_stride;
   uint32_t* item_cnt;
   uint32_t* item_off;
   uint2* item_desc;  // per work item: query range and offset (count pass -> write pass)
@@ -277,8 +284,10 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   b->bounds = m.take<uint32_t>(nkb);
   b->chunks = m.take<uint32_t>(nkb);
   b->istart = m.take<uint32_t>(nkb);
-  b->res = m.take<int32_t>((int64_t)K3 * nq_max);
-  b->ts = m.take<int32_t>((int64_t)K3 * n_src);
+  b->res_stride = (int64_t)align_up((size_t)nq_max, 32);
+  b->ts_stride = (int64_t)align_up((size_t)n_src, 32);
+  b->res = m.take<int32_t>((int64_t)K3 * b->res_stride);
+  b->ts = m.take<int32_t>((int64_t)K3 * b->ts_stride);
   b->item_cnt = m.take<uint32_t>(b->max_items);
   b->item_off = m.take<uint32_t>(b->max_items);
   b->item_desc = m.take<uint2>(b->max_items);
@@ -588,9 +597,9 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
   a.swap_roles = (mode == SPCONV_UP) ? 1 : 0;
   a.check_q = (mode == SPCONV_UP) ? 1 : 0;
   a.res = b.res;
-  a.res_stride = nq_max;
+  a.res_stride = b.res_stride;
   a.ts = b.ts;
-  a.ts_stride = n_src;
+  a.ts_stride = b.ts_stride;
   a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
   a.item_desc = b.item_desc;
   a.pair_cap = (int64_t)K3 * nq_max;
@@ -615,7 +624,7 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
   if (!a.sym) {
     // sources without a partner at some offset: no query visits their entry
     PhaseScope ph(PH_METADATA, s);
-    hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(b.ts), 0xFFFFFFFFu, (int64_t)K3 * n_src, s);
+    hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(b.ts), 0xFFFFFFFFu, (int64_t)K3 * b.ts_stride, s);
     if (e != hipSuccess) return bail(hip_fail(e, "metadata fill"));
   }
   {
@@ -669,17 +678,17 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
                            : (mode == SPCONV_DOWN ? nullptr : (tu.presorted ? nullptr : b.qrow));
   if (mode == SPCONV_UP) {
     m->imt = b.res;
-    m->imt_stride = nq_max;
+    m->imt_stride = b.res_stride;
     m->in_perm = q_perm;
     m->omt = b.ts;
-    m->omt_stride = n_src;
+    m->omt_stride = b.ts_stride;
     m->out_perm = src_perm;
   } else {
     m->imt = b.ts;
-    m->imt_stride = n_src;
+    m->imt_stride = b.ts_stride;
     m->in_perm = src_perm;
     m->omt = b.res;
-    m->omt_stride = nq_max;
+    m->omt_stride = b.res_stride;
     m->out_perm = q_perm;
   }
   *out_map = m;

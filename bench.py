@@ -89,6 +89,8 @@ def kernel_models(n, n_out, pairs, L, k3, passes, fused=True):
         # radix passes: the first reads int32 coordinates (16 B/row), later ones key + row (12 B)
         "k_radix_scatter": ("hbm", (16 * n + 12 * n + (P - 1) * 24 * n) / P),
         "k_radix_hist": ("hbm", (16 * n + (P - 1) * 8 * n) / P),
+        # by-bucket small sorts: each bucket's keys and rows read and written once
+        "k_radix_local": ("hbm", 24 * n),
         "k_minmax": ("hbm", 16 * n),
         # forward search, count pass: query keys and source keys once, one result word per
         # (offset, query)

@@ -83,7 +83,7 @@ const char* prof_name(int id) {
       "bounds", "sort", "outcoords", "backward", "balance", "forward", "readback", "metadata", "gather", "gemm",
       "scatter", "hash", "", "", "", "",
       "k_minmax", "k_radix_hist", "k_radix_scatter", "k_scan", "k_copy", "k_down_keys", "k_unique", "k_backward",
-      "k_forward_count", "k_forward_write", "k_fill", "", "k_gather", "k_gemm", "k_scatter", "k_pack",
+      "k_forward_count", "k_forward_write", "k_fill", "k_radix_local", "k_gather", "k_gemm", "k_scatter", "k_pack",
       "k_hash_insert", "k_hash_probe", "", "", "", "", "", ""};
   return (id >= 0 && id < PROF_IDS) ? kNames[id] : "";
 }
@@ -479,8 +479,15 @@ namespace {
 // same inputs needed last time, else the last count needed on this thread (start:
 // 4 passes, a 32-bit key).  A build whose key turns out wider is redone with the
 // passes it needs.
+// Sort plan of a map build, kept per input from the previous build of it: the
+// digit passes of the digit-by-digit sort, and whether the small sorts may go by
+// bucket (no bucket of the previous build was too large for one workgroup).
+struct SortPlan {
+  int passes = 4;
+  bool by_bucket = true;
+};
 struct PassHint {
-  std::unordered_map<std::string, int> by_input;
+  std::unordered_map<std::string, SortPlan> by_input;
   int last = 4;
 };
 thread_local PassHint g_pass_hint;
@@ -494,8 +501,10 @@ std::string pass_key(const int32_t* a, int64_t na, const int32_t* b, int64_t nb,
 
 int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords, int64_t n_out, int K,
                    int stride, int tensor_stride, int mode, const spconv_options* opt, void* d_workspace,
-                   size_t ws_bytes, void* stream, spconv_map** out_map, int passes, int* passes_needed) {
+                   size_t ws_bytes, void* stream, spconv_map** out_map, int passes, bool by_bucket,
+                   int* passes_needed, bool* bucket_failed) {
   *passes_needed = 0;
+  *bucket_failed = false;
   if (!out_map) return fail(SPCONV_EINVAL, "out_map is NULL");
   *out_map = nullptr;
   int st = check_map_args(n_in, mode == SPCONV_UP ? n_out : 0, K, stride, tensor_stride, mode);
@@ -548,8 +557,10 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     int np = 0;
     hipError_t e = launch_minmax(d_in_coords, n_in, d_out_coords, mode == SPCONV_UP ? n_out : 0, b.mm_partial,
                                  b.cb, &np, s);
-    // builds that do not sort the keys take any key width (up to 62 bits)
-    const int plan = (tu.hash || (tu.presorted && mode != SPCONV_DOWN)) ? 8 : passes;
+    // builds that do not sort the keys digit by digit take any key width (up to 62
+    // bits): no sort, or every sort by bucket
+    const bool all_bucket = by_bucket && radix_bucket_applies(n_src) && (mode != SPCONV_UP || radix_bucket_applies(n_in));
+    const int plan = (tu.hash || (tu.presorted && mode != SPCONV_DOWN) || all_bucket) ? 8 : passes;
     if (e == hipSuccess) e = launch_layout(b.mm_partial, np, K, stride, tensor_stride, K3, plan, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "coordinate bounds"));
   }
@@ -561,11 +572,11 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     PhaseScope ph(PH_SORT, s);
     // sorted inputs (a previous layer's outputs) only need their keys packed (Section 5.1.1)
     hipError_t e = tu.presorted ? launch_pack(src_coords, n_src, L, b.skeys, b.sidx, s)
-                                : radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, passes,
+                                : radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, passes, by_bucket,
                                                 b.sort_tmp, &b.cb->err, s);
     if (e == hipSuccess && mode == SPCONV_UP)
       e = tu.presorted ? launch_pack(d_in_coords, n_in, L, b.qkeys, b.qrow, s)
-                       : radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, passes,
+                       : radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, passes, by_bucket,
                                        b.sort_tmp, &b.cb->err, s);
     if (e != hipSuccess) return bail(hip_fail(e, "sort"));
   }
@@ -574,7 +585,7 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     const int64_t cell = (int64_t)tensor_stride * stride;
     hipError_t e = launch_down_keys(b.skeys, n_src, L, cell, b.dkeys, b.dvals, s);
     if (e == hipSuccess)
-      e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, passes, b.sort_tmp,
+      e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, passes, by_bucket, b.sort_tmp,
                         &b.cb->err, s);
     if (e == hipSuccess)
       e = unique_keys(b.dkeys, n_src, L, b.flags, b.pos, b.scan_tmp, b.qkeys, b.qrow, b.qcoords, b.cb, s);
@@ -650,6 +661,12 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     const ControlBlock* hc = &head;
     if (hc->err & kErrRange)
       return bail(fail(SPCONV_ERANGE, "coordinate extent (plus kernel reach) needs more than 62 key bits"));
+    if (hc->err & kErrBucket) {
+      // a bucket too large for one workgroup: the caller redoes the build digit by digit
+      *passes_needed = (hc->layout.total_bits + 7) / 8;
+      *bucket_failed = true;
+      return bail(SPCONV_OK);
+    }
     if (hc->err & kErrWide) {
       // the key is wider than the sort planned for: the caller redoes the build
       *passes_needed = (hc->layout.total_bits + 7) / 8;
@@ -705,20 +722,32 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
   PassHint& hint = g_pass_hint;
   const std::string key = pass_key(d_in_coords, n_in, d_out_coords, n_out, K, stride, tensor_stride, mode);
   const auto it = hint.by_input.find(key);
-  int passes = (it != hint.by_input.end()) ? it->second : hint.last;
-  int needed = 0;
-  int st = build_map_impl(d_in_coords, n_in, d_out_coords, n_out, K, stride, tensor_stride, mode, opt, d_workspace,
-                          ws_bytes, stream, out_map, passes, &needed);
-  if (st == SPCONV_OK && !*out_map && needed > passes) {
-    // the key needs more passes than planned: redo with the count it needs
-    passes = needed;
+  SortPlan plan;
+  if (it != hint.by_input.end())
+    plan = it->second;
+  else
+    plan.passes = hint.last;
+  int needed = 0, st = SPCONV_OK;
+  // at most one redo for a too large bucket and one for a key wider than planned
+  for (int attempt = 0; attempt < 3; ++attempt) {
+    bool bucket_failed = false;
     st = build_map_impl(d_in_coords, n_in, d_out_coords, n_out, K, stride, tensor_stride, mode, opt, d_workspace,
-                        ws_bytes, stream, out_map, passes, &needed);
-    if (st == SPCONV_OK && !*out_map) return fail(SPCONV_EHIP, "key layout changed between two builds");
+                        ws_bytes, stream, out_map, plan.passes, plan.by_bucket, &needed, &bucket_failed);
+    if (st != SPCONV_OK || *out_map) break;
+    if (bucket_failed && plan.by_bucket) {
+      plan.by_bucket = false;
+      if (needed > plan.passes) plan.passes = needed;
+    } else if (needed > plan.passes) {
+      plan.passes = needed;
+    } else {
+      return fail(SPCONV_EHIP, "key layout changed between two builds");
+    }
   }
+  if (st == SPCONV_OK && !*out_map) return fail(SPCONV_EHIP, "map build did not settle on a sort plan");
   if (needed > 0) {
     if (hint.by_input.size() >= 256) hint.by_input.clear();
-    hint.by_input[key] = needed;
+    plan.passes = needed;
+    hint.by_input[key] = plan;
     hint.last = needed;
   }
   return st;

@@ -57,6 +57,7 @@ enum : uint32_t {
   kErrUnsorted = 8u,     // rows declared sorted are not in (b, x, y, z) order
   kErrRange = 16u,       // the coordinate extent plus kernel reach needs more than 62 key bits
   kErrWide = 32u,        // the key needs more bits than the sort passes planned by the host
+  kErrBucket = 64u,      // a bucket of the by-bucket small sort exceeds what one workgroup sorts
 };
 
 // Small control block in device memory, read back once at the end of a map build.
@@ -84,7 +85,7 @@ enum ProfId : int {
   PH_METADATA, PH_GATHER, PH_GEMM, PH_SCATTER, PH_HASH,
   // kernels
   KN_MINMAX = 16, KN_RADIX_HIST, KN_RADIX_SCATTER, KN_SCAN, KN_COPY, KN_DOWN_KEYS, KN_UNIQUE,
-  KN_BACKWARD, KN_FORWARD_COUNT, KN_FORWARD_WRITE, KN_FILL, KN_UNUSED_27, KN_GATHER, KN_GEMM, KN_SCATTER,
+  KN_BACKWARD, KN_FORWARD_COUNT, KN_FORWARD_WRITE, KN_FILL, KN_RADIX_LOCAL, KN_GATHER, KN_GEMM, KN_SCATTER,
   KN_PACK, KN_HASH_INSERT, KN_HASH_PROBE,
   PROF_IDS = 40
 };
@@ -121,10 +122,13 @@ hipError_t launch_layout(const int32_t* partial, int np, int K, int stride, int 
 // key bits are plain copies); the result ends in (keys, vals).  If `coords` is
 // non-null the input is those coordinates (keys packed with the device layout *L,
 // values = row index).  Look-back waits that exceed their bound set kErrSpin in *err
-// (nothing hangs).
+// (nothing hangs).  by_bucket: where radix_bucket_applies(n), sort by the key's top
+// digit and then each bucket in one workgroup instead (all key bits, whatever
+// `passes`); a bucket too large for that sets kErrBucket and stays unsorted.
+bool radix_bucket_applies(int64_t n);
 hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals,
-                         uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, int passes, void* d_temp,
-                         uint32_t* err, hipStream_t s);
+                         uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, int passes, bool by_bucket,
+                         void* d_temp, uint32_t* err, hipStream_t s);
 hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, const KeyLayout* L, int64_t cell,
                             uint64_t* dkeys, uint32_t* vals, hipStream_t s);
 // Distinct consecutive keys of sorted `keys` -> qkeys, qrow = position, coords; n_q into cb.

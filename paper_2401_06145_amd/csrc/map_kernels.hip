@@ -542,6 +542,9 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
 // histograms gives the offsets (three launches).
 constexpr int64_t kFusedScanTiles = 256;
 
+// Bit position of the key's top 8-bit digit (0 for keys of at most 8 bits).
+__device__ __forceinline__ int top_digit_shift(const KeyLayout& L) { return max(L.total_bits - 8, 0); }
+
 template <bool FROM_COORDS, bool TILE_MAJOR, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, const KeyLayout* __restrict__ Lp,
                                                          int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
@@ -567,6 +570,8 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
   // an early return, which would let the compiler move the key loads after the
   // layout read)
   const bool active = FROM_COORDS || shift < L.total_bits;
+  // shift < 0: the key's top digit (the bucket pass of the small sorts)
+  const int sh = (shift >= 0) ? shift : top_digit_shift(L);
   __syncthreads();
   if constexpr (FROM_COORDS) {
 #pragma unroll
@@ -578,7 +583,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
     const bool valid = active && base + r * kThreads + threadIdx.x < n;
-    const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
+    const uint32_t d = (uint32_t)(key[r] >> sh) & 255u;
     const uint64_t peers = match_digit(d, valid);
     if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)popc64(peers));
   }
@@ -594,11 +599,14 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
 // earlier tiles).  Every workgroup reads all of them, so their size, not their
 // latency, sets this step's time (measured: 4 of the pass's 8.6 us at 118 tiles
 // of 32-bit counts).  Otherwise `offs` is the scanned digit-major histogram.
+// shift < 0 sorts by the key's top digit; then (FUSED) workgroup 0 also stores
+// the first position of every digit in bucket_start[0..256] (bucket_start[256] = n).
 template <bool FROM_COORDS, bool FUSED, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t* kin, const uint32_t* vin,
                                                             const int4* coords, const KeyLayout* __restrict__ Lp, uint64_t* kout,
                                                             uint32_t* vout, int64_t n, int shift,
-                                                            const uint32_t* offs, int64_t ntiles) {
+                                                            const uint32_t* offs, int64_t ntiles,
+                                                            uint32_t* bucket_start) {
   __shared__ TileLds<ITEMS> t;
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
@@ -670,6 +678,10 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
 #pragma unroll
     for (int w = 0; w < 2 * kWavesPerBlock; ++w) before += s_part[w * 256 + tid];
     t.gbase[tid] = block_excl256(tot, t.s_wave) + before;
+    if (bucket_start && blockIdx.x == 0) {  // workgroup 0: before = 0
+      bucket_start[tid] = t.gbase[tid];
+      if (tid == 0) bucket_start[256] = (uint32_t)n;
+    }
   } else {
     t.gbase[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
   }
@@ -687,10 +699,142 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
     return;
   }
   tile_pack<FROM_COORDS, ITEMS>(L, crd, key);
+  const int sh = (shift >= 0) ? shift : top_digit_shift(L);
   __syncthreads();  // wc cleared
-  tile_rank<ITEMS>(t, key, base, n, shift, rank);
+  tile_rank<ITEMS>(t, key, base, n, sh, rank);
   __syncthreads();
-  tile_place<false, ITEMS>(t, key, val, rank, base, n, shift, kout, vout);
+  tile_place<false, ITEMS>(t, key, val, rank, base, n, sh, kout, vout);
+}
+
+// ----------------------------------------------------------------------------
+// Small sorts by bucket: one stable pass on the key's top digit puts every key
+// in its bucket (k_radix_tile_hist / k_radix_tile_scatter with shift < 0), then
+// one workgroup per bucket sorts the bucket by the remaining low bits in LDS,
+// 8-bit digit by digit: three launches instead of two per digit.  A bucket
+// larger than kBucketCap keys raises kErrBucket and is left unsorted (the map
+// build is then redone with the digit-by-digit sort).
+// ----------------------------------------------------------------------------
+constexpr int kBucketThreads = 1024;
+constexpr int kBucketWaves = kBucketThreads / kWave;
+constexpr int kBucketItems = 8;
+constexpr int kBucketCap = kBucketThreads * kBucketItems;
+constexpr size_t kBucketLds = (size_t)kBucketCap * (sizeof(uint64_t) + sizeof(uint32_t)) +
+                              (size_t)kBucketWaves * 256 * sizeof(uint32_t) + 64 * sizeof(uint32_t);
+
+// Bucket b = [bucket_start[b], bucket_start[b + 1]) of (kin, vin), sorted into the
+// same positions of (kout, vout) (which may be kin, vin: each workgroup reads its
+// whole bucket before it writes).  Slot s of the bucket is item r of lane l of
+// wave w for s = w 64 ITEMS + r 64 + l, so each wave ranks a contiguous run of
+// slots with wave ballots (stable); LDS holds the permuted bucket between digits.
+__global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* kin, const uint32_t* vin,
+                                                                uint64_t* kout, uint32_t* vout,
+                                                                const uint32_t* __restrict__ bucket_start,
+                                                                const KeyLayout* __restrict__ Lp, uint32_t* err) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint64_t* skey = reinterpret_cast<uint64_t*>(smem);
+  uint32_t* sval = reinterpret_cast<uint32_t*>(skey + kBucketCap);
+  uint32_t(*wc)[256] = reinterpret_cast<uint32_t(*)[256]>(sval + kBucketCap);
+  uint32_t* s_part = &wc[kBucketWaves][0];  // 64 words of scan scratch
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const uint32_t b0 = bucket_start[blockIdx.x];
+  const uint32_t b1 = bucket_start[blockIdx.x + 1];
+  const int m = (b1 > b0) ? (int)min(b1 - b0, (uint32_t)(kBucketCap + 1)) : 0;
+  if (m > kBucketCap) {  // workgroup-uniform
+    if (tid == 0) atomicOr(err, kErrBucket);
+    return;
+  }
+  if (m <= 1) {
+    if (m == 1 && tid == 0 && kout != kin) {  // a lone key still moves to the output
+      kout[b0] = kin[b0];
+      vout[b0] = vin[b0];
+    }
+    return;
+  }
+  auto slot = [&](int r) { return wave * (kWave * kBucketItems) + r * kWave + lane; };
+  // Only the first nwv waves hold slots of this bucket (a typical bucket fills one
+  // or two): the others skip every step but the barriers, and item r of a wave is
+  // skipped as a whole once its slots start past the bucket (both wave-uniform).
+  const int nwv = (m + kWave * kBucketItems - 1) / (kWave * kBucketItems);
+  auto item_live = [&](int r) { return wave * (kWave * kBucketItems) + r * kWave < m; };
+  uint64_t key[kBucketItems];
+  uint32_t val[kBucketItems];
+#pragma unroll
+  for (int r = 0; r < kBucketItems; ++r) {
+    const int64_t i = (int64_t)b0 + min(slot(r), m - 1);
+    key[r] = item_live(r) ? kin[i] : 0ull;
+    val[r] = item_live(r) ? vin[i] : 0u;
+  }
+  const KeyLayout L = *Lp;
+  const int bits = top_digit_shift(L);  // the bucket pass sorted the bits above
+  for (int sh = 0; sh < bits; sh += 8) {
+    for (int i = tid; i < nwv * 256; i += kBucketThreads) (&wc[0][0])[i] = 0;
+    __syncthreads();
+    uint32_t rank[kBucketItems];
+#pragma unroll
+    for (int r = 0; r < kBucketItems; ++r) {
+      rank[r] = 0;
+      if (!item_live(r)) continue;
+      const bool valid = slot(r) < m;
+      const uint32_t d = (uint32_t)(key[r] >> sh) & 255u;
+      const uint64_t peers = match_digit(d, valid);
+      if (valid) {
+        const uint32_t before = (uint32_t)popc64(peers & lanemask_lt());
+        rank[r] = wc[wave][d] + before;
+        if (before == 0) wc[wave][d] += (uint32_t)popc64(peers);
+      }
+    }
+    __syncthreads();
+    // digit d's first position: threads 0..255 (waves 0..3) scan the digit totals
+    uint32_t tot = 0, x = 0;
+    if (tid < 256) {
+      for (int w = 0; w < nwv; ++w) tot += wc[w][tid];
+      x = tot;
+#pragma unroll
+      for (int dd = 1; dd < kWave; dd <<= 1) {
+        const uint32_t y = __shfl_up(x, dd, kWave);
+        if (lane >= dd) x += y;
+      }
+      if (lane == kWave - 1) s_part[wave] = x;
+    }
+    __syncthreads();
+    if (tid < 256) {
+      uint32_t start = x - tot;
+      for (int w = 0; w < wave; ++w) start += s_part[w];
+      for (int w = 0; w < nwv; ++w) {
+        const uint32_t c = wc[w][tid];
+        wc[w][tid] = start;
+        start += c;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kBucketItems; ++r) {
+      if (slot(r) < m) {
+        const uint32_t d = (uint32_t)(key[r] >> sh) & 255u;
+        const uint32_t pos = wc[wave][d] + rank[r];
+        skey[pos] = key[r];
+        sval[pos] = val[r];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kBucketItems; ++r) {
+      if (!item_live(r)) continue;
+      const int sl = min(slot(r), m - 1);
+      key[r] = skey[sl];
+      val[r] = sval[sl];
+    }
+    __syncthreads();  // the next digit rewrites wc and the stage
+  }
+#pragma unroll
+  for (int r = 0; r < kBucketItems; ++r) {
+    if (slot(r) < m) {
+      kout[(int64_t)b0 + slot(r)] = key[r];
+      vout[(int64_t)b0 + slot(r)] = val[r];
+    }
+  }
 }
 
 // ----------------------------------------------------------------------------
@@ -1300,7 +1444,9 @@ size_t radix_temp_bytes(int64_t n) {
   const int64_t tiles_small = std::max<int64_t>(1, (n + kRsTileSmall - 1) / kRsTileSmall);
   const int64_t tiles_tiled = std::max(ntiles, tiles_small);
   const size_t tiled = align256((size_t)256 * tiles_tiled * sizeof(uint32_t)) + scan_temp_bytes(256 * tiles_tiled);
-  return std::max(onesweep, tiled);
+  // by-bucket sorts: 16-bit tile histograms, then the 257 bucket starts
+  const size_t bucket = align256((size_t)tiles_small * 256 * sizeof(uint16_t)) + 257 * sizeof(uint32_t);
+  return std::max(std::max(onesweep, tiled), bucket);
 }
 
 namespace {
@@ -1353,7 +1499,7 @@ hipError_t radix_sort_tiled_t(const int32_t* coords, const KeyLayout* L, uint64_
       ProfScope ps(KN_RADIX_SCATTER, s);
 #define SPC_S(FC, FU)                                                                                           \
   hipLaunchKernelGGL((k_radix_tile_scatter<FC, FU, ITEMS>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],   \
-                     FC ? nullptr : vb[src], FC ? c4 : nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles)
+                     FC ? nullptr : vb[src], FC ? c4 : nullptr, L, kb[dst], vb[dst], n, shift, hist, ntiles, nullptr)
       if (first) {
         if (fused) SPC_S(true, true); else SPC_S(true, false);
       } else {
@@ -1375,11 +1521,61 @@ hipError_t radix_sort_tiled(const int32_t* coords, const KeyLayout* L, uint64_t*
   return radix_sort_tiled_t<kRsItems>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
 }
 
+// By-bucket sort (three launches; see radix_bucket_applies for its sizes): tile histograms
+// of the top digit (1024-key tiles, so the scatter sums them itself), the stable
+// bucket pass (into (keys, vals) from coordinates, else into the alternates), and
+// one workgroup per bucket sorting it into (keys, vals).
+hipError_t radix_sort_bucket(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals,
+                             uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, void* d_temp, uint32_t* err,
+                             hipStream_t s) {
+  constexpr int ITEMS = kRsItemsSmall;
+  const int64_t ntiles = (n + kThreads * ITEMS - 1) / (kThreads * ITEMS);
+  uint32_t* hist = static_cast<uint32_t*>(d_temp);
+  uint32_t* bstart =
+      reinterpret_cast<uint32_t*>(static_cast<char*>(d_temp) + align256((size_t)ntiles * 256 * sizeof(uint16_t)));
+  const int4* c4 = reinterpret_cast<const int4*>(coords);
+  uint64_t* mk = coords ? keys : keys_alt;
+  uint32_t* mv = coords ? vals : vals_alt;
+  const unsigned g = (unsigned)ntiles;
+  {
+    ProfScope ps(KN_RADIX_HIST, s);
+    if (coords)
+      hipLaunchKernelGGL((k_radix_tile_hist<true, true, ITEMS>), dim3(g), dim3(kThreads), 0, s, nullptr, c4, L, n, -1,
+                         hist, ntiles);
+    else
+      hipLaunchKernelGGL((k_radix_tile_hist<false, true, ITEMS>), dim3(g), dim3(kThreads), 0, s, keys, nullptr, L, n,
+                         -1, hist, ntiles);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  {
+    ProfScope ps(KN_RADIX_SCATTER, s);
+    if (coords)
+      hipLaunchKernelGGL((k_radix_tile_scatter<true, true, ITEMS>), dim3(g), dim3(kThreads), 0, s, nullptr, nullptr,
+                         c4, L, mk, mv, n, -1, hist, ntiles, bstart);
+    else
+      hipLaunchKernelGGL((k_radix_tile_scatter<false, true, ITEMS>), dim3(g), dim3(kThreads), 0, s, keys, vals,
+                         nullptr, L, mk, mv, n, -1, hist, ntiles, bstart);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  ProfScope ps(KN_RADIX_LOCAL, s);
+  hipLaunchKernelGGL(k_bucket_sort, dim3(256), dim3(kBucketThreads), kBucketLds, s, mk, mv, keys, vals, bstart, L, err);
+  return hipGetLastError();
+}
+
 }  // namespace
 
+// The by-bucket sort serves the sizes whose tile histograms the bucket pass sums
+// itself (at most kFusedScanTiles tiles of 1024 keys).
+bool radix_bucket_applies(int64_t n) { return n > 1 && (n + kRsTileSmall - 1) / kRsTileSmall <= kFusedScanTiles; }
+
 hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
-                         uint32_t* vals_alt, int64_t n, int passes, void* d_temp, uint32_t* err, hipStream_t s) {
+                         uint32_t* vals_alt, int64_t n, int passes, bool by_bucket, void* d_temp, uint32_t* err,
+                         hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  if (by_bucket && radix_bucket_applies(n))
+    return radix_sort_bucket(coords, L, keys, vals, keys_alt, vals_alt, n, d_temp, err, s);
   if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
   if (n <= 1 || passes == 0) return hipSuccess;
   if (passes > kRsMaxPasses || n >= ((int64_t)1 << 30)) return hipErrorInvalidValue;

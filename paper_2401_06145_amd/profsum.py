@@ -29,6 +29,7 @@ CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 # timing-API id -> source file holding the kernel
 SOURCES = {
     "k_minmax": "map_kernels.hip", "k_radix_hist": "map_kernels.hip", "k_radix_scatter": "map_kernels.hip",
+    "k_radix_local": "map_kernels.hip",
     "k_pack": "map_kernels.hip", "k_down_keys": "map_kernels.hip", "k_unique": "map_kernels.hip",
     "k_backward": "map_kernels.hip", "k_forward_count": "map_kernels.hip", "k_forward_write": "map_kernels.hip",
     "k_fill": "map_kernels.hip", "k_scan": "scan.hip", "k_gather": "gmas_kernels.hip",
@@ -39,6 +40,7 @@ SOURCES = {
 FOLD = [
     (r"k_radix_(tile_scatter|pass)\b", "k_radix_scatter"),
     (r"k_radix_(tile_hist|upsweep)\b", "k_radix_hist"),
+    (r"k_bucket_sort\b", "k_radix_local"),
     (r"k_forward_count\b", "k_forward_count"),
     (r"k_forward_write\b", "k_forward_write"),
     (r"k_gemm(_wide)?\b", "k_gemm"),

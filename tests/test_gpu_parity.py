@@ -403,6 +403,23 @@ def test_sort_with_one_shared_low_digit(side):
     assert rel_err(to_f64(y)[rows], ref) <= TOL["f16"]
 
 
+def test_sort_bucket_over_capacity_redone_digit_by_digit():
+    """A dense 128 x 128 plane at x = 0 plus one point at x = 1000: x takes the key's
+    top bits, so all 16384 plane points share the top digit and fall in one bucket,
+    twice what one workgroup sorts.  The first build raises the bucket flag and is
+    redone digit by digit; the second uses the plan kept for this input.  Both maps
+    must equal the oracle's."""
+    say("bucket over capacity, 16385 voxels")
+    g = np.stack(np.meshgrid(np.arange(128), np.arange(128), indexing="ij"), -1).reshape(-1, 2)
+    plane = np.concatenate([np.zeros((len(g), 2), np.int64), g], 1)
+    c = np.concatenate([plane, [[0, 1000, 0, 0]]]).astype(np.int32)
+    c = c[np.random.default_rng(77).permutation(len(c))]
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    dc = to_dev(c)
+    for _ in range(2):
+        assert_map_equal(B.KernelMap.build(dc, 3), okm)
+
+
 def test_deterministic_pairs():
     say("deterministic pair order")
     c = scenes.workload(1).coords

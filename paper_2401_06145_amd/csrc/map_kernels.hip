@@ -723,9 +723,10 @@ constexpr size_t kBucketLds = (size_t)kBucketCap * (sizeof(uint64_t) + sizeof(ui
 
 // Bucket b = [bucket_start[b], bucket_start[b + 1]) of (kin, vin), sorted into the
 // same positions of (kout, vout) (which may be kin, vin: each workgroup reads its
-// whole bucket before it writes).  Slot s of the bucket is item r of lane l of
-// wave w for s = w 64 ITEMS + r 64 + l, so each wave ranks a contiguous run of
-// slots with wave ballots (stable); LDS holds the permuted bucket between digits.
+// whole bucket before it writes).  A bucket of m keys takes ipt = ceil(m / 1024)
+// items per lane, spread over all waves: slot s is item r of lane l of wave w for
+// s = w 64 ipt + r 64 + l, so each wave ranks a contiguous run of slots with wave
+// ballots (stable) in ipt rounds; LDS holds the permuted bucket between digits.
 __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* kin, const uint32_t* vin,
                                                                 uint64_t* kout, uint32_t* vout,
                                                                 const uint32_t* __restrict__ bucket_start,
@@ -752,12 +753,15 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* 
     }
     return;
   }
-  auto slot = [&](int r) { return wave * (kWave * kBucketItems) + r * kWave + lane; };
-  // Only the first nwv waves hold slots of this bucket (a typical bucket fills one
-  // or two): the others skip every step but the barriers, and item r of a wave is
-  // skipped as a whole once its slots start past the bucket (both wave-uniform).
-  const int nwv = (m + kWave * kBucketItems - 1) / (kWave * kBucketItems);
-  auto item_live = [&](int r) { return wave * (kWave * kBucketItems) + r * kWave < m; };
+  // Items per lane: the ranking rounds run serially, so a bucket is spread over
+  // all waves (a typical bucket then takes one round).  Only the first nwv waves
+  // hold slots; the others skip every step but the barriers, and item r of a wave
+  // is skipped as a whole past ipt or once its slots start past the bucket (both
+  // wave-uniform).
+  const int ipt = (m + kBucketThreads - 1) / kBucketThreads;
+  const int nwv = (m + kWave * ipt - 1) / (kWave * ipt);
+  auto slot = [&](int r) { return wave * (kWave * ipt) + r * kWave + lane; };
+  auto item_live = [&](int r) { return r < ipt && wave * (kWave * ipt) + r * kWave < m; };
   uint64_t key[kBucketItems];
   uint32_t val[kBucketItems];
 #pragma unroll
@@ -811,7 +815,7 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* 
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kBucketItems; ++r) {
-      if (slot(r) < m) {
+      if (r < ipt && slot(r) < m) {
         const uint32_t d = (uint32_t)(key[r] >> sh) & 255u;
         const uint32_t pos = wc[wave][d] + rank[r];
         skey[pos] = key[r];
@@ -830,7 +834,7 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* 
   }
 #pragma unroll
   for (int r = 0; r < kBucketItems; ++r) {
-    if (slot(r) < m) {
+    if (r < ipt && slot(r) < m) {
       kout[(int64_t)b0 + slot(r)] = key[r];
       vout[(int64_t)b0 + slot(r)] = val[r];
     }

@@ -77,13 +77,12 @@ def kernel_models(n, n_out, pairs, L, k3, passes, fused=True):
     e = 4 if L.dtype == "f32" else 2
     ep = e  # GEMM partials are stored in the layer dtype
     P = max(passes, 1)
-    # scans per step: the chunk-count scan of the balance step (K^3 x source blocks of
-    # 1024) and the match-count scan (one entry per work item), plus one digit-offset scan
-    # per radix pass when the sort has between 257 and 1023 tiles of 2048 keys
+    # scans per step: the match-count scan (one entry per work item, K^3 x source blocks
+    # of 1024), plus one digit-offset scan per radix pass when the sort has between 257
+    # and 1023 tiles of 2048 keys
     nb = -(-n // 1024)
     ntiles = -(-n // 2048)
-    max_items = k3 * (nb + -(-n_out // 1024)) + 1
-    scan_lens = ([256 * ntiles] * P if 256 < ntiles < 1024 else []) + [k3 * nb, max_items]
+    scan_lens = ([256 * ntiles] * P if 256 < ntiles < 1024 else []) + [k3 * nb]
     m = {
         "k_scan": ("hbm", 8.0 * sum(scan_lens) / len(scan_lens)),
         # radix passes: the first reads int32 coordinates (16 B/row), later ones key + row (12 B)

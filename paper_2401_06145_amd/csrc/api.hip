@@ -208,9 +208,7 @@ struct MapBufs {
   uint32_t* flags;
   uint32_t* pos;
   void* sort_tmp;
-  uint32_t* bounds;
-  uint32_t* chunks;
-  uint32_t* istart;
+  uint32_t* bounds;  // per work item (offset, block): end of its query block
   int32_t* res;   // T_q, kept as the map's query-side metadata table
   int32_t* ts;    // T_s, the source-side table
   // Row strides of the two tables: the point counts rounded up to 32 entries, so
@@ -222,14 +220,15 @@ struct MapBufs {
   int64_t ts_stride;
   uint32_t* item_cnt;
   uint32_t* item_off;
-  uint2* item_desc;  // per work item: query range and offset (count pass -> write pass)
   uint64_t* hkeys;  // hash-table search only
   uint32_t* hvals;
   int log2cap;
   int32_t* mm_partial;
   void* scan_tmp;
-  int64_t max_items;
-  int64_t nb;
+  int64_t max_items;  // work items: K3 * nb_items
+  int64_t nb;         // source blocks of B keys
+  int64_t nb_items;   // blocks per offset of the work items: nb, or for the hash-table
+                      // search blocks of Cq queries
 };
 
 struct Tunables {
@@ -262,7 +261,8 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   Bump m(base);
   const int64_t nmax = std::max(n_src, nq_max);
   b->nb = (n_src + tu.B - 1) / tu.B;
-  b->max_items = (int64_t)K3 * (b->nb + (nq_max + tu.Cq - 1) / tu.Cq) + 1;
+  b->nb_items = tu.hash ? (nq_max + tu.Cq - 1) / tu.Cq : b->nb;
+  b->max_items = (int64_t)K3 * b->nb_items;
   b->skeys = m.take<uint64_t>(n_src);
   b->sidx = m.take<uint32_t>(n_src);
   b->qkeys = (mode == SPCONV_SUBM) ? nullptr : m.take<uint64_t>(nq_max);
@@ -280,19 +280,15 @@ size_t plan_map(void* base, int64_t n_src, int64_t nq_max, int K3, const Tunable
   b->flags = (mode == SPCONV_DOWN) ? m.take<uint32_t>(n_src) : nullptr;
   b->pos = (mode == SPCONV_DOWN) ? m.take<uint32_t>(n_src) : nullptr;
   b->sort_tmp = m.take_bytes(radix_temp_bytes(nmax));
-  const int64_t nkb = (int64_t)K3 * b->nb;
-  b->bounds = m.take<uint32_t>(nkb);
-  b->chunks = m.take<uint32_t>(nkb);
-  b->istart = m.take<uint32_t>(nkb);
+  b->bounds = m.take<uint32_t>(b->max_items);
   b->res_stride = (int64_t)align_up((size_t)nq_max, 32);
   b->ts_stride = (int64_t)align_up((size_t)n_src, 32);
   b->res = m.take<int32_t>((int64_t)K3 * b->res_stride);
   b->ts = m.take<int32_t>((int64_t)K3 * b->ts_stride);
   b->item_cnt = m.take<uint32_t>(b->max_items);
   b->item_off = m.take<uint32_t>(b->max_items);
-  b->item_desc = m.take<uint2>(b->max_items);
   b->mm_partial = static_cast<int32_t*>(m.take_bytes(minmax_temp_bytes()));
-  b->scan_tmp = m.take_bytes(scan_temp_bytes(std::max(std::max(nkb, n_src), b->max_items)));
+  b->scan_tmp = m.take_bytes(scan_temp_bytes(std::max(n_src, b->max_items)));
   b->log2cap = 0;
   b->hkeys = nullptr;
   b->hvals = nullptr;
@@ -612,25 +608,21 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
   a.ts = b.ts;
   a.ts_stride = b.ts_stride;
   a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
-  a.item_desc = b.item_desc;
   a.pair_cap = (int64_t)K3 * nq_max;
   PubBuffer* pb = pub_buffer();
   if (!pb) return bail(fail(SPCONV_EHIP, "mapped host buffer allocation failed"));
   if (++pb->seq == 0) pb->seq = 1;
   a.pub = pb->dev;
   a.pub_seq = pb->seq;
-  // the hash-table search treats all queries of an offset as one block
-  const int64_t nb = tu.hash ? 1 : b.nb;
+  // work items (k, b): the sorted search's source blocks, or the hash-table
+  // search's blocks of Cq queries; the passes split a query block into chunks of
+  // at most Cq themselves, so the balancing step needs no scan of its own
+  const int64_t nb = b.nb_items;
   {
     PhaseScope ph(PH_BACKWARD, s);
-    hipError_t e = tu.hash ? launch_hash_items(K3, nq_max, tu.Cq, b.bounds, b.chunks, s)
-                           : launch_backward(a, b.nb, b.bounds, b.chunks, b.cb, s);
+    hipError_t e = tu.hash ? launch_hash_items(K3, nq_max, tu.Cq, nb, b.bounds, s)
+                           : launch_backward(a, nb, b.bounds, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "backward search"));
-  }
-  {
-    PhaseScope ph(PH_BALANCE, s);
-    hipError_t e = scan_exclusive_u32(b.chunks, b.istart, (int64_t)K3 * nb, &b.cb->n_items, b.scan_tmp, s);
-    if (e != hipSuccess) return bail(hip_fail(e, "balance"));
   }
   if (!a.sym) {
     // sources without a partner at some offset: no query visits their entry
@@ -640,13 +632,11 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
   }
   {
     PhaseScope ph(PH_FORWARD, s);
-    hipError_t e = tu.hash ? launch_hash_count(a, b.hkeys, b.hvals, b.log2cap, b.item_cnt, b.max_items, b.cb, s)
-                           : launch_forward(a, false, b.bounds, b.chunks, b.nb, b.istart, b.item_cnt, nullptr,
-                                            b.max_items, b.pin, b.pout, b.cb, s);
+    hipError_t e = tu.hash ? launch_hash_count(a, b.hkeys, b.hvals, b.log2cap, nb, b.item_cnt, s)
+                           : launch_forward(a, false, b.bounds, nb, b.item_cnt, nullptr, b.pin, b.pout, b.cb, s);
     if (e == hipSuccess) e = scan_exclusive_u32(b.item_cnt, b.item_off, b.max_items, &b.cb->n_pairs, b.scan_tmp, s);
     if (e == hipSuccess)
-      e = launch_forward(a, true, b.bounds, b.chunks, nb, b.istart, b.item_cnt, b.item_off, b.max_items, b.pin,
-                         b.pout, b.cb, s);
+      e = launch_forward(a, true, b.bounds, nb, b.item_cnt, b.item_off, b.pin, b.pout, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "forward search"));
   }
   {
@@ -678,7 +668,6 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     if (hc->err & kErrSpin) return bail(fail(SPCONV_EHIP, "a look-back exceeded its wait bound"));
     if (hc->err & kErrUnsorted)
       return bail(fail(SPCONV_EINVAL, "rows declared presorted are not in ascending (b, x, y, z) order"));
-    if (hc->n_items > (uint32_t)b.max_items) return bail(fail(SPCONV_EHIP, "work items exceed the launch bound"));
     if (mode == SPCONV_DOWN) m->n_out = hc->n_q;
     for (int k = 0; k < K3; ++k) {
       m->counts[k] = (int64_t)hc->seg_pair_start[k + 1] - hc->seg_pair_start[k];

@@ -65,7 +65,6 @@ constexpr int kMaxOffsets = 125;  // K <= 5
 struct ControlBlock {
   uint32_t err;           // kErr* flags
   uint32_t n_q;           // number of distinct output coordinates (DOWN)
-  uint32_t n_items;       // forward-search work items of the balance step
   uint32_t n_pairs;       // total matches
   uint32_t seg_pair_start[kMaxOffsets + 3];  // first pair of offset k; [K3] = n_pairs
   KeyLayout layout;       // key layout, computed on the device from the coordinate bounds
@@ -160,9 +159,6 @@ struct SearchArgs {
   // entries come from a fill before it, or (sym != 0) from the write pass itself.
   int32_t* ts;
   int64_t ts_stride;
-  // Per work item, written by the count pass and read by the write pass:
-  // x = first sorted query position, y = query count | (offset << 16).
-  uint2* item_desc;
   int64_t pair_cap;       // capacity of the pair lists (K3 * queries)
   // Submanifold map with odd K: query q misses offset k exactly when source q
   // has no partner at the mirrored offset K^3 - 1 - k, so the write pass marks
@@ -178,16 +174,15 @@ struct SearchArgs {
 constexpr size_t kPubFlagOffset = 1024;
 constexpr size_t kPubBytes = 4096;
 static_assert(kControlHeadBytes % 4 == 0 && kControlHeadBytes <= kPubFlagOffset, "head fits before the flag");
-// Section 5.1.2, backward search fused with the per-(k, b) chunk counts of the
-// balancing step (and the duplicate-key check).
-hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, uint32_t* chunks,
-                           ControlBlock* cb, hipStream_t s);
-// Forward search over the balanced work items: count pass (write = false) fills
-// item_cnt; write pass places pairs at item_off and fills cb->seg_pair_start.
-hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, const uint32_t* chunks,
-                          int64_t nb, const uint32_t* istart, uint32_t* item_cnt, const uint32_t* item_off,
-                          int64_t max_items, int32_t* pin, int32_t* pout, ControlBlock* cb,
-                          hipStream_t s);
+// Section 5.1.2, backward search: bounds[k nb + b] = the end of the query block of
+// offset k and source block b (its start is the previous block's end, 0 for b = 0);
+// also the repeat check of transposed maps' query keys.
+hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, ControlBlock* cb, hipStream_t s);
+// Forward search over the work items (k, b), each query block in chunks of at most
+// Cq queries: count pass (write = false) fills T_q and item_cnt[k nb + b]; write
+// pass places pairs from item_off[k nb + b] on and fills cb->seg_pair_start.
+hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, int64_t nb, uint32_t* item_cnt,
+                          const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb, hipStream_t s);
 
 // Hash-table search (the prior-art Map, kept as an ablation): open addressing
 // with linear probing over 64-bit keys, 2^log2cap slots (load <= 1/2).
@@ -196,12 +191,12 @@ constexpr uint64_t kHashEmpty = ~0ull;
 // idx[i] = i, and inserts (key, i); repeated keys set kErrDup in *err.
 hipError_t launch_hash_build(const int32_t* coords, int64_t n, const KeyLayout* L, uint64_t* hkeys, uint32_t* hvals,
                              int log2cap, uint64_t* keys, uint32_t* idx, uint32_t* err, hipStream_t s);
-// Work items of the probe: one query block of all n_q queries per offset
-// (bounds[k] = n_q, chunks[k] = its number of Cq chunks), i.e. one source block.
-hipError_t launch_hash_items(int K3, int64_t n_q, int Cq, uint32_t* bounds, uint32_t* chunks, hipStream_t s);
+// Work items of the probe: nb = ceil(n_q / Cq) blocks of Cq queries per offset,
+// recorded as bounds[k nb + b] = min((b + 1) Cq, n_q) for the write pass.
+hipError_t launch_hash_items(int K3, int64_t n_q, int Cq, int64_t nb, uint32_t* bounds, hipStream_t s);
 // Probe pass: res[k][q] = matching input row or -1, item_cnt = matches per item.
 hipError_t launch_hash_count(const SearchArgs& a, const uint64_t* hkeys, const uint32_t* hvals, int log2cap,
-                             uint32_t* item_cnt, int64_t max_items, ControlBlock* cb, hipStream_t s);
+                             int64_t nb, uint32_t* item_cnt, hipStream_t s);
 
 // gmas_kernels.hip.  Metadata tables are offset-major over sorted positions:
 // entry [k * stride + p] is the buffer row of point p's pair at offset k, or -1;

@@ -44,7 +44,6 @@ __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int6
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     cb->err = 0;
     cb->n_q = 0;
-    cb->n_items = 0;
     cb->n_pairs = 0;
   }
   int32_t mn[4] = {INT_MAX, INT_MAX, INT_MAX, INT_MAX};
@@ -907,50 +906,19 @@ __device__ __forceinline__ int64_t wave_upper_bound(const T* a, int64_t n, V thr
   return lo + popc64(__ballot(pred));
 }
 
-// Two such searches of the same array in lock step (two independent loads per
-// lane and round), so that they cost the latency of one.
-template <typename T, typename V>
-__device__ __forceinline__ void wave_upper_bound2(const T* a, int64_t n, V thr1, V thr2, int64_t* r1, int64_t* r2) {
-  const int lane = threadIdx.x & (kWave - 1);
-  int64_t lo1 = 0, hi1 = n, lo2 = 0, hi2 = n;
-  while (hi1 - lo1 > kWave || hi2 - lo2 > kWave) {
-    const int64_t st1 = (hi1 - lo1 + kWave - 1) / kWave, st2 = (hi2 - lo2 + kWave - 1) / kWave;
-    const int64_t p1 = lo1 + (int64_t)(lane + 1) * st1 - 1, p2 = lo2 + (int64_t)(lane + 1) * st2 - 1;
-    const bool a1 = hi1 - lo1 > kWave && p1 < hi1 && (V)a[p1] <= thr1;
-    const bool a2 = hi2 - lo2 > kWave && p2 < hi2 && (V)a[p2] <= thr2;
-    const int c1 = popc64(__ballot(a1)), c2 = popc64(__ballot(a2));
-    if (hi1 - lo1 > kWave) {
-      const int64_t nlo = lo1 + (int64_t)c1 * st1;
-      hi1 = min(lo1 + (int64_t)(c1 + 1) * st1 - 1, hi1);
-      lo1 = nlo;
-    }
-    if (hi2 - lo2 > kWave) {
-      const int64_t nlo = lo2 + (int64_t)c2 * st2;
-      hi2 = min(lo2 + (int64_t)(c2 + 1) * st2 - 1, hi2);
-      lo2 = nlo;
-    }
-  }
-  const int64_t q1 = lo1 + lane, q2 = lo2 + lane;
-  const bool b1 = q1 < hi1 && (V)a[q1] <= thr1;
-  const bool b2 = q2 < hi2 && (V)a[q2] <= thr2;
-  *r1 = lo1 + popc64(__ballot(b1));
-  *r2 = lo2 + popc64(__ballot(b2));
-}
-
 // ----------------------------------------------------------------------------
-// Backward binary search (Section 5.1.2) fused with the balancing count.  For
-// source block b and offset k the query block is the run of sorted queries q
-// with key(q) + dk in (pivot_{b-1}, pivot_b], pivot_b being the block's last
-// key.  One wave per (k, b) finds bounds[k][b] = #{q : key(q) + dk <= pivot_b}
-// and the same for pivot_{b-1}, and writes the number of <= Cq chunks the
-// query block splits into.  The last block also takes the queries beyond its
+// Backward binary search (Section 5.1.2).  For source block b and offset k the
+// query block is the run of sorted queries q with key(q) + dk in (pivot_{b-1},
+// pivot_b], pivot_b being the block's last key.  One wave per (k, b) finds
+// bounds[k][b] = #{q : key(q) + dk <= pivot_b}; the block's queries are then
+// [bounds[k][b - 1], bounds[k][b]), which the forward passes split into chunks
+// of at most Cq (the balancing step).  The last block also takes the queries beyond its
 // pivot (they all miss), so that every (offset, query) pair is searched once and
 // the per-query tables come out complete.  For transposed maps the k = 0 waves
 // also check the sorted query keys for repeats (a point cloud is a set); the
 // count pass checks the source keys in LDS.
 // ----------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb, uint32_t* bounds, uint32_t* chunks,
-                                                       ControlBlock* cb) {
+__global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb, uint32_t* bounds, ControlBlock* cb) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t wid = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
   if (wid >= (int64_t)a.K3 * nb) return;  // wave-uniform
@@ -964,16 +932,11 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
   // (a bound without a neighbouring pivot uses a threshold that every key, or no
   // key, passes)
   const int64_t thr_hi = (b == nb - 1) ? INT64_MAX : (int64_t)a.skeys[last] - dk;
-  const int64_t thr_lo = (b == 0) ? INT64_MIN : (int64_t)a.skeys[b * a.B - 1] - dk;
-  int64_t hi, lo;
-  wave_upper_bound2<uint64_t, int64_t>(a.qkeys, nq, thr_hi, thr_lo, &hi, &lo);
-  if (lane == 0) {
-    bounds[wid] = (uint32_t)hi;
-    // keys that are not in order (a build whose sort was planned too short, or rows
-    // wrongly declared presorted; both are reported) can invert a block's bounds:
-    // such a block gets no work, so no pass reads past the query keys
-    chunks[wid] = (hi > lo) ? (uint32_t)((hi - lo + a.Cq - 1) / a.Cq) : 0u;
-  }
+  const int64_t hi = wave_upper_bound<uint64_t, int64_t>(a.qkeys, nq, thr_hi);
+  // keys that are not in order (a build whose sort was planned too short, or rows
+  // wrongly declared presorted; both are reported) can invert a block's bounds:
+  // the passes then give the block no queries, so none reads past the query keys
+  if (lane == 0) bounds[wid] = (uint32_t)hi;
   if (k == 0 && a.check_q) {
     // the query keys of a transposed map (the coarse inputs) must be strictly
     // increasing too; the count pass checks the source keys
@@ -990,11 +953,11 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
 }
 
 // ----------------------------------------------------------------------------
-// Forward binary search (Section 5.1.2) over the load-balanced work items
-// (query chunks of at most Cq queries of one (offset, source block) pair): the
-// source block is staged in LDS and each lane binary-searches its queries
-// there, recording the match (or -1) in T_q.  Count pass: matches per work
-// item.  Write pass: matches ranked with wave ballots; pair e of the item goes
+// Forward binary search (Section 5.1.2) over the work items, one per (offset,
+// source block) pair, whose query block is run in chunks of at most Cq queries
+// (the load balancing): the source block is staged in LDS and each lane
+// binary-searches its queries there, recording the match (or -1) in T_q.  Count
+// pass: matches per work item.  Write pass: matches ranked with wave ballots; pair e of the item goes
 // to index o = item_off + e, so every offset's pairs come out in sorted-query
 // order, and o, the pair's GEMM buffer row, is also stored in both metadata
 // tables (T_q in place of the source position, T_s at the source position).
@@ -1032,36 +995,37 @@ __device__ __forceinline__ void lds_search(const uint64_t* lkey, const uint64_t 
   }
 }
 
-// Forward search, write pass: one workgroup per work item.  The count pass left
-// each query's result in T_q (matching sorted source position, or -1) and the
-// item's query range in item_desc; matches are ranked with wave ballots from the
-// item's scanned match offset, so every offset's pairs come out in sorted-query
-// order, and pair index o (the pair's GEMM buffer row) replaces the source
-// position in T_q and is stored in T_s.  The loads of all rounds are issued
-// together: results first, then the rows of the matches.
+// Forward search, write pass: one workgroup per work item (k, b), the query
+// block [bounds[k][b - 1], bounds[k][b]) in chunks of at most Cq queries.  The
+// count pass left each query's result in T_q (matching sorted source position,
+// or -1); matches are ranked with wave ballots from the item's scanned match
+// offset onward, chunk after chunk, so every offset's pairs come out in
+// sorted-query order, and pair index o (the pair's GEMM buffer row) replaces the
+// source position in T_q and is stored in T_s.  The loads of all rounds of a
+// chunk are issued together: results first, then the rows of the matches.
 template <int ROUNDS>
-__global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const uint32_t* istart, int64_t nb,
+__global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const uint32_t* bounds, int64_t nb,
                                                             const uint32_t* item_off, int32_t* pin, int32_t* pout,
                                                             ControlBlock* cb) {
   __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
-  const int64_t w = blockIdx.x;
-  // requested before the item count is known (the grid covers max_items items,
-  // so w indexes both arrays)
-  const uint2 d = a.item_desc[w];
-  const uint64_t base = item_off[w];
-  const int64_t n_items = cb->n_items;
+  const int64_t w = blockIdx.x;  // k nb + b
+  const int k = (int)(w / nb);
+  const int64_t b = w - (int64_t)k * nb;
+  const int64_t q_hi = bounds[w];
+  // min(): keys out of order can invert the bounds (the block then has no queries)
+  const int64_t q_lo = (b == 0) ? 0 : min((int64_t)bounds[w - 1], q_hi);
+  const uint64_t base0 = item_off[w];
 
   if (w == 0 && wave == 0) {
-    // per-offset pair counts: the items of offset k are [istart[k nb], istart[(k+1) nb])
-    for (int k = lane; k <= a.K3; k += kWave) {
-      const int64_t first = (k < a.K3) ? (int64_t)istart[(int64_t)k * nb] : n_items;
-      const uint32_t off = (first < n_items) ? item_off[first] : cb->n_pairs;
-      cb->seg_pair_start[k] = off;
+    // per-offset pair starts: offset k's items are k nb .. k nb + nb - 1
+    for (int kk = lane; kk <= a.K3; kk += kWave) {
+      const uint32_t off = (kk < a.K3) ? item_off[(int64_t)kk * nb] : cb->n_pairs;
+      cb->seg_pair_start[kk] = off;
       if (a.pub)
-        __hip_atomic_store(&a.pub[offsetof(ControlBlock, seg_pair_start) / 4 + k], off, __ATOMIC_RELAXED,
+        __hip_atomic_store(&a.pub[offsetof(ControlBlock, seg_pair_start) / 4 + kk], off, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_SYSTEM);
     }
     if (a.pub) {
@@ -1079,85 +1043,85 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
         __hip_atomic_store(&a.pub[kPubFlagOffset / 4], a.pub_seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
-  if (w >= n_items) return;  // workgroup-uniform: the grid is sized for the worst case
 
-  const int64_t q0 = d.x;
-  const int64_t q1 = q0 + (d.y & 0xFFFFu);
-  const int k = (int)(d.y >> 16);
   int32_t* res = a.res + (int64_t)k * a.res_stride;
-  int32_t sp[ROUNDS];
-#pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-    const int64_t qp = q0 + (int64_t)r * kThreads + tid;
-    sp[r] = (qp < q1) ? res[qp] : -1;
-  }
-  int32_t r_in[ROUNDS], r_out[ROUNDS];
-  uint64_t bal[ROUNDS];
-#pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-    // rows of the match (a valid dummy address for lanes without one)
-    const int64_t qp = q0 + (int64_t)r * kThreads + tid;
-    const bool hit = sp[r] >= 0;
-    const int32_t src = (int32_t)a.sidx[hit ? sp[r] : 0];
-    const int32_t qry = (int32_t)a.qrow[hit ? qp : 0];
-    r_in[r] = a.swap_roles ? qry : src;
-    r_out[r] = a.swap_roles ? src : qry;
-    bal[r] = __ballot(hit);
-    if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal[r]);
-  }
-  if (a.sym) {
-    // mirrored offset's T_s row, for the misses of a symmetric map
-    int32_t* ts_mirror = a.ts + (int64_t)(a.K3 - 1 - k) * a.ts_stride;
+  int32_t* ts = a.ts + (int64_t)k * a.ts_stride;
+  // mirrored offset's T_s row, for the misses of a symmetric map
+  int32_t* ts_mirror = a.ts + (int64_t)(a.K3 - 1 - k) * a.ts_stride;
+  uint64_t base = base0;
+  for (int64_t q0 = q_lo; q0 < q_hi; q0 += a.Cq) {  // workgroup-uniform
+    const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
+    int32_t sp[ROUNDS];
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) {
       const int64_t qp = q0 + (int64_t)r * kThreads + tid;
-      if (qp < q1 && sp[r] < 0) ts_mirror[qp] = -1;
+      sp[r] = (qp < q1) ? res[qp] : -1;
     }
-  }
-  __syncthreads();
-  uint32_t total = 0;
-  uint32_t before[ROUNDS];
+    int32_t r_in[ROUNDS], r_out[ROUNDS];
+    uint64_t bal[ROUNDS];
 #pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-#pragma unroll
-    for (int v = 0; v < kWavesPerBlock; ++v) {
-      if (v == wave) before[r] = total;
-      total += s_cnt[r][v];
-    }
-  }
-  int32_t* ts = a.ts + (int64_t)k * a.ts_stride;
-#pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-    if ((bal[r] >> lane) & 1ull) {
-      const uint64_t o = base + before[r] + (uint64_t)popc64(bal[r] & lanemask_lt());
+    for (int r = 0; r < ROUNDS; ++r) {
+      // rows of the match (a valid dummy address for lanes without one)
       const int64_t qp = q0 + (int64_t)r * kThreads + tid;
-      if (o >= (uint64_t)a.pair_cap) {  // only when keys were out of order (reported)
-        atomicOr(&cb->err, kErrOverflow);
-        continue;
-      }
-      pin[o] = r_in[r];
-      pout[o] = r_out[r];
-      res[qp] = (int32_t)o;
-      ts[sp[r]] = (int32_t)o;
+      const bool hit = sp[r] >= 0;
+      const int32_t src = (int32_t)a.sidx[hit ? sp[r] : 0];
+      const int32_t qry = (int32_t)a.qrow[hit ? qp : 0];
+      r_in[r] = a.swap_roles ? qry : src;
+      r_out[r] = a.swap_roles ? src : qry;
+      bal[r] = __ballot(hit);
+      if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal[r]);
     }
+    if (a.sym) {
+#pragma unroll
+      for (int r = 0; r < ROUNDS; ++r) {
+        const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+        if (qp < q1 && sp[r] < 0) ts_mirror[qp] = -1;
+      }
+    }
+    __syncthreads();
+    uint32_t total = 0;
+    uint32_t before[ROUNDS];
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+#pragma unroll
+      for (int v = 0; v < kWavesPerBlock; ++v) {
+        if (v == wave) before[r] = total;
+        total += s_cnt[r][v];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+      if ((bal[r] >> lane) & 1ull) {
+        const uint64_t o = base + before[r] + (uint64_t)popc64(bal[r] & lanemask_lt());
+        const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+        if (o >= (uint64_t)a.pair_cap) {  // only when keys were out of order (reported)
+          atomicOr(&cb->err, kErrOverflow);
+          continue;
+        }
+        pin[o] = r_in[r];
+        pout[o] = r_out[r];
+        res[qp] = (int32_t)o;
+        ts[sp[r]] = (int32_t)o;
+      }
+    }
+    base += total;
+    __syncthreads();  // s_cnt is rewritten by the next chunk
   }
 }
 
 // Forward search, count pass, with source-block reuse: one workgroup per
 // (source block b, group of G offsets) stages block b in LDS once and then runs
-// every work item of (k, b) for the offsets k of its group, chunk by chunk (the
-// items and their order are those of the balance step).  Each chunk stores its
-// queries' results, its match count and its query range (for the write pass).
+// the query block of (k, b) for every offset k of its group, in chunks of at
+// most Cq queries (the balancing step).  Each query's result goes to T_q, and
+// each (k, b) work item's match count to item_cnt[k nb + b].
 // With few source blocks the groups are small, so that the grid still fills the
 // GPU; with many, one workgroup takes all K^3 offsets of its block and reads it
 // from HBM once instead of K^3 times.  The block's keys, the first chunk's query
 // keys and its bounds are all requested before the first wait; each chunk's
 // ROUNDS searches run as independent chains.
 template <int ROUNDS, int LOG2B>
-__global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const uint32_t* bounds,
-                                                            const uint32_t* chunks, int64_t nb,
-                                                            const uint32_t* istart, uint32_t* item_cnt,
-                                                            int64_t max_items, int G, ControlBlock* cb) {
+__global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const uint32_t* bounds, int64_t nb,
+                                                            uint32_t* item_cnt, int G, ControlBlock* cb) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
   uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
@@ -1179,15 +1143,14 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
   const uint64_t key_before = a.skeys[s0 > 0 ? s0 - 1 : 0];
   const int k_first = g * G;
   const int k_end = min(a.K3, k_first + G);
-  int64_t q_lo = 0, q_hi = 0, first = 0;
+  int64_t q_lo = 0, q_hi = 0;
   uint32_t nch = 0;
   auto load_bounds = [&](int k) {
     const int64_t kb = (int64_t)k * nb + b;
     q_hi = bounds[kb];
-    // min(): keys out of order can invert the bounds (the chunks are then empty)
+    // min(): keys out of order can invert the bounds (the block then has no queries)
     q_lo = (b == 0) ? 0 : min((int64_t)bounds[kb - 1], q_hi);
-    nch = chunks[kb];
-    first = istart[kb];
+    nch = (uint32_t)((q_hi - q_lo + a.Cq - 1) / a.Cq);
   };
   uint64_t key[ROUNDS];
   // keys of the chunk [q0, q1) (lanes past q1 re-read the first key)
@@ -1225,6 +1188,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
     if (k != k_first) load_bounds(k);
     int32_t* res = a.res + (int64_t)k * a.res_stride;
     const uint64_t dk = (uint64_t)a.dk[k];
+    uint32_t item_total = 0;  // thread 0's sum over the chunks
     for (uint32_t c = 0; c < nch; ++c) {
       const int64_t q0 = min(q_lo + (int64_t)c * a.Cq, q_hi);
       const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
@@ -1241,36 +1205,28 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
         if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal);
       }
       __syncthreads();
-      if (tid == 0 && first + c < max_items) {
-        uint32_t total = 0;
+      if (tid == 0) {
 #pragma unroll
         for (int r = 0; r < ROUNDS; ++r)
 #pragma unroll
-          for (int v = 0; v < kWavesPerBlock; ++v) total += s_cnt[r][v];
-        item_cnt[first + c] = total;
-        a.item_desc[first + c] = make_uint2((uint32_t)q0, (uint32_t)(q1 - q0) | ((uint32_t)k << 16));
+          for (int v = 0; v < kWavesPerBlock; ++v) item_total += s_cnt[r][v];
       }
       __syncthreads();  // s_cnt is rewritten by the next chunk
     }
+    if (tid == 0) item_cnt[(int64_t)k * nb + b] = item_total;
   }
-  // items past the last one count zero: the match-count scan runs over max_items
-  // (last, so that the search's loads need not wait for the item count)
-  const int64_t n_items = cb->n_items;
-  for (int64_t i = n_items + (int64_t)blockIdx.x * kThreads + tid; i < max_items; i += (int64_t)gridDim.x * kThreads)
-    item_cnt[i] = 0;
 }
 
 template <int ROUNDS>
-hipError_t forward_count_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds,
-                           const uint32_t* chunks, int64_t nb, const uint32_t* istart, uint32_t* item_cnt,
-                           int64_t max_items, int G, ControlBlock* cb, int log2B) {
+hipError_t forward_count_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds, int64_t nb,
+                           uint32_t* item_cnt, int G, ControlBlock* cb, int log2B) {
   // the block plus its padding: 2^log2B + 1 keys
   const size_t lds = (((size_t)1 << log2B) + 1) * sizeof(uint64_t);
   switch (log2B) {
 #define SPC_FC(L2)                                                                                                 \
   case L2:                                                                                                         \
-    hipLaunchKernelGGL((k_forward_count<ROUNDS, L2>), dim3(grid), dim3(kThreads), lds, s, a, bounds, chunks, nb,  \
-                       istart, item_cnt, max_items, G, cb);                                                       \
+    hipLaunchKernelGGL((k_forward_count<ROUNDS, L2>), dim3(grid), dim3(kThreads), lds, s, a, bounds, nb, item_cnt, \
+                       G, cb);                                                                                     \
     break;
     SPC_FC(6) SPC_FC(7) SPC_FC(8) SPC_FC(9) SPC_FC(10) SPC_FC(11) SPC_FC(12)
 #undef SPC_FC
@@ -1281,9 +1237,9 @@ hipError_t forward_count_t(unsigned grid, hipStream_t s, const SearchArgs& a, co
 }
 
 template <int ROUNDS>
-hipError_t forward_write_t(unsigned grid, hipStream_t s, const SearchArgs& a, int64_t nb, const uint32_t* istart,
+hipError_t forward_write_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds, int64_t nb,
                            const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb) {
-  hipLaunchKernelGGL((k_forward_write<ROUNDS>), dim3(grid), dim3(kThreads), 0, s, a, istart, nb, item_off, pin, pout,
+  hipLaunchKernelGGL((k_forward_write<ROUNDS>), dim3(grid), dim3(kThreads), 0, s, a, bounds, nb, item_off, pin, pout,
                      cb);
   return hipGetLastError();
 }
@@ -1329,31 +1285,28 @@ __global__ __launch_bounds__(kThreads) void k_hash_insert(const int4* c, int64_t
   atomicOr(err, kErrOverflow);  // table full: cannot happen at load 1/2
 }
 
-__global__ void k_hash_items(int K3, int64_t n_q, int Cq, uint32_t* bounds, uint32_t* chunks) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= K3) return;
-  bounds[k] = (uint32_t)n_q;
-  chunks[k] = (uint32_t)((n_q + Cq - 1) / Cq);
+// The hash-table search's work items: block b of offset k is queries
+// [b Cq, (b + 1) Cq), recorded as the upper bounds the write pass reads.
+__global__ void k_hash_items(int K3, int64_t n_q, int Cq, int64_t nb, uint32_t* bounds) {
+  const int64_t nkb = (int64_t)K3 * nb;
+  for (int64_t kb = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; kb < nkb; kb += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t b = kb % nb;
+    bounds[kb] = (uint32_t)min((b + 1) * (int64_t)Cq, n_q);
+  }
 }
 
-// One workgroup per work item (offset k, chunk c of Cq queries).
+// One workgroup per work item (offset k, block b of Cq queries).
 template <int ROUNDS>
 __global__ __launch_bounds__(kThreads) void k_hash_count(SearchArgs a, const uint64_t* __restrict__ hkeys,
-                                                         const uint32_t* __restrict__ hvals, int log2cap,
-                                                         uint32_t* item_cnt, int64_t max_items, ControlBlock* cb) {
+                                                         const uint32_t* __restrict__ hvals, int log2cap, int64_t nb,
+                                                         uint32_t* item_cnt) {
   __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
-  const int64_t w = blockIdx.x;
-  const int64_t n_items = cb->n_items;
-  if (w >= n_items) {  // workgroup-uniform; idle items count zero matches
-    if (tid == 0 && w < max_items) item_cnt[w] = 0;
-    return;
-  }
-  const int64_t cpk = (a.n_q + a.Cq - 1) / a.Cq;  // chunks per offset
-  const int k = (int)(w / cpk);
-  const int64_t q0 = (w - (int64_t)k * cpk) * a.Cq;
+  const int64_t w = blockIdx.x;  // k nb + b
+  const int k = (int)(w / nb);
+  const int64_t q0 = (w - (int64_t)k * nb) * a.Cq;
   const int64_t q1 = min(q0 + (int64_t)a.Cq, a.n_q);
   const uint64_t dk = (uint64_t)a.dk[k];
   const uint64_t mask = (1ull << log2cap) - 1ull;
@@ -1389,7 +1342,6 @@ __global__ __launch_bounds__(kThreads) void k_hash_count(SearchArgs a, const uin
 #pragma unroll
       for (int v = 0; v < kWavesPerBlock; ++v) total += s_cnt[r][v];
     item_cnt[w] = total;
-    a.item_desc[w] = make_uint2((uint32_t)q0, (uint32_t)(q1 - q0) | ((uint32_t)k << 16));
   }
 }
 
@@ -1666,47 +1618,45 @@ hipError_t unique_keys(const uint64_t* keys, int64_t n, const KeyLayout* L, uint
   return hipGetLastError();
 }
 
-hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, uint32_t* chunks, ControlBlock* cb,
-                           hipStream_t s) {
+hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, ControlBlock* cb, hipStream_t s) {
   const int64_t nkb = (int64_t)a.K3 * nb;
   if (nkb <= 0) return hipSuccess;
   const int64_t blocks = (nkb + kWavesPerBlock - 1) / kWavesPerBlock;
   ProfScope ps(KN_BACKWARD, s);
-  hipLaunchKernelGGL(k_backward, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, nb, bounds, chunks, cb);
+  hipLaunchKernelGGL(k_backward, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, nb, bounds, cb);
   return hipGetLastError();
 }
 
 // Workgroups the count pass aims for when choosing its offset groups.
 constexpr int64_t kCountTargetGroups = 8192;
 
-hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, const uint32_t* chunks, int64_t nb,
-                          const uint32_t* istart, uint32_t* item_cnt, const uint32_t* item_off, int64_t max_items,
-                          int32_t* pin, int32_t* pout, ControlBlock* cb, hipStream_t s) {
+hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, int64_t nb, uint32_t* item_cnt,
+                          const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb, hipStream_t s) {
+  if (nb <= 0) return hipSuccess;
   int log2B = 0;
   while ((1 << log2B) < a.B) ++log2B;
   const int rounds = a.Cq / kThreads;
   if (write) {
-    const unsigned grid = (unsigned)(max_items > 0 ? max_items : 1);
+    const unsigned grid = (unsigned)((int64_t)a.K3 * nb);
     ProfScope ps(KN_FORWARD_WRITE, s);
     switch (rounds) {
-      case 1: return forward_write_t<1>(grid, s, a, nb, istart, item_off, pin, pout, cb);
-      case 2: return forward_write_t<2>(grid, s, a, nb, istart, item_off, pin, pout, cb);
-      case 4: return forward_write_t<4>(grid, s, a, nb, istart, item_off, pin, pout, cb);
-      case 8: return forward_write_t<8>(grid, s, a, nb, istart, item_off, pin, pout, cb);
+      case 1: return forward_write_t<1>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
+      case 2: return forward_write_t<2>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
+      case 4: return forward_write_t<4>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
+      case 8: return forward_write_t<8>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
       default: return hipErrorInvalidValue;
     }
   }
-  if (nb <= 0) return hipSuccess;
   const int64_t ngroups0 = std::min<int64_t>(a.K3, std::max<int64_t>(1, (kCountTargetGroups + nb - 1) / nb));
   const int G = (int)((a.K3 + ngroups0 - 1) / ngroups0);
   const int64_t ngroups = (a.K3 + G - 1) / G;
   const unsigned grid = (unsigned)(nb * ngroups);
   ProfScope ps(KN_FORWARD_COUNT, s);
   switch (rounds) {
-    case 1: return forward_count_t<1>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
-    case 2: return forward_count_t<2>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
-    case 4: return forward_count_t<4>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
-    case 8: return forward_count_t<8>(grid, s, a, bounds, chunks, nb, istart, item_cnt, max_items, G, cb, log2B);
+    case 1: return forward_count_t<1>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
+    case 2: return forward_count_t<2>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
+    case 4: return forward_count_t<4>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
+    case 8: return forward_count_t<8>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1722,21 +1672,24 @@ hipError_t launch_hash_build(const int32_t* coords, int64_t n, const KeyLayout* 
   return hipGetLastError();
 }
 
-hipError_t launch_hash_items(int K3, int64_t n_q, int Cq, uint32_t* bounds, uint32_t* chunks, hipStream_t s) {
-  hipLaunchKernelGGL(k_hash_items, dim3(1), dim3(128), 0, s, K3, n_q, Cq, bounds, chunks);
+hipError_t launch_hash_items(int K3, int64_t n_q, int Cq, int64_t nb, uint32_t* bounds, hipStream_t s) {
+  const int64_t nkb = (int64_t)K3 * nb;
+  if (nkb <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_hash_items, dim3(grid_for(nkb)), dim3(kThreads), 0, s, K3, n_q, Cq, nb, bounds);
   return hipGetLastError();
 }
 
 hipError_t launch_hash_count(const SearchArgs& a, const uint64_t* hkeys, const uint32_t* hvals, int log2cap,
-                             uint32_t* item_cnt, int64_t max_items, ControlBlock* cb, hipStream_t s) {
-  if (max_items <= 0) return hipSuccess;
+                             int64_t nb, uint32_t* item_cnt, hipStream_t s) {
+  const int64_t nkb = (int64_t)a.K3 * nb;
+  if (nkb <= 0) return hipSuccess;
   ProfScope ps(KN_HASH_PROBE, s);
-  const unsigned grid = (unsigned)max_items;
+  const unsigned grid = (unsigned)nkb;
   switch (a.Cq / kThreads) {
 #define SPC_H(R)                                                                                                   \
   case R:                                                                                                          \
-    hipLaunchKernelGGL((k_hash_count<R>), dim3(grid), dim3(kThreads), 0, s, a, hkeys, hvals, log2cap, item_cnt,   \
-                       max_items, cb);                                                                             \
+    hipLaunchKernelGGL((k_hash_count<R>), dim3(grid), dim3(kThreads), 0, s, a, hkeys, hvals, log2cap, nb,         \
+                       item_cnt);                                                                                  \
     break;
     SPC_H(1)
     SPC_H(2)

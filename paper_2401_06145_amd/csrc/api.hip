@@ -546,8 +546,12 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     delete m;
     return code;
   };
-  // key layout on the device (no host wait): bounds partials, then one workgroup
+  // key layout on the device (no host wait): bounds partials, then the layout,
+  // computed by the source sort's first kernel when that is a tile histogram of the
+  // coordinates, else by one workgroup of its own
   const KeyLayout* L = &b.cb->layout;
+  LayoutArgs la{};
+  const bool sort_first = !tu.hash && !tu.presorted;
   {
     PhaseScope ph(PH_BOUNDS, s);
     int np = 0;
@@ -557,7 +561,8 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     // bits): no sort, or every sort by bucket
     const bool all_bucket = by_bucket && radix_bucket_applies(n_src) && (mode != SPCONV_UP || radix_bucket_applies(n_in));
     const int plan = (tu.hash || (tu.presorted && mode != SPCONV_DOWN) || all_bucket) ? 8 : passes;
-    if (e == hipSuccess) e = launch_layout(b.mm_partial, np, K, stride, tensor_stride, K3, plan, b.cb, s);
+    la = LayoutArgs{b.mm_partial, np, K, stride, tensor_stride, K3, plan, b.cb};
+    if (e == hipSuccess && !sort_first) e = launch_layout(la, s);
     if (e != hipSuccess) return bail(hip_fail(e, "coordinate bounds"));
   }
   if (tu.hash) {
@@ -569,11 +574,11 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     // sorted inputs (a previous layer's outputs) only need their keys packed (Section 5.1.1)
     hipError_t e = tu.presorted ? launch_pack(src_coords, n_src, L, b.skeys, b.sidx, s)
                                 : radix_sort_kv(src_coords, L, b.skeys, b.sidx, b.kalt, b.valt, n_src, passes, by_bucket,
-                                                b.sort_tmp, &b.cb->err, s);
+                                                b.sort_tmp, &b.cb->err, &la, s);
     if (e == hipSuccess && mode == SPCONV_UP)
       e = tu.presorted ? launch_pack(d_in_coords, n_in, L, b.qkeys, b.qrow, s)
                        : radix_sort_kv(d_in_coords, L, b.qkeys, b.qrow, b.kalt, b.valt, n_in, passes, by_bucket,
-                                       b.sort_tmp, &b.cb->err, s);
+                                       b.sort_tmp, &b.cb->err, nullptr, s);
     if (e != hipSuccess) return bail(hip_fail(e, "sort"));
   }
   if (mode == SPCONV_DOWN) {
@@ -582,7 +587,7 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     hipError_t e = launch_down_keys(b.skeys, n_src, L, cell, b.dkeys, b.dvals, s);
     if (e == hipSuccess)
       e = radix_sort_kv(nullptr, L, b.dkeys, b.dvals, b.kalt, b.valt, n_src, passes, by_bucket, b.sort_tmp,
-                        &b.cb->err, s);
+                        &b.cb->err, nullptr, s);
     if (e == hipSuccess)
       e = unique_keys(b.dkeys, n_src, L, b.flags, b.pos, b.scan_tmp, b.qkeys, b.qrow, b.qcoords, b.cb, s);
     if (e != hipSuccess) return bail(hip_fail(e, "output coordinates"));

@@ -74,6 +74,15 @@ struct ControlBlock {
 // the layout's width); the offset deltas stay on the device.
 constexpr size_t kControlHeadBytes = offsetof(ControlBlock, dk);
 
+// Inputs of the device-side key layout: the bounds partials of launch_minmax and
+// the layer's geometry (kernel size, stride, tensor stride, K^3); passes = the
+// digit passes the host planned its sort for (kErrWide above that).
+struct LayoutArgs {
+  const int32_t* partial;
+  int np, K, stride, t, K3, passes;
+  ControlBlock* cb;
+};
+
 // ---------------------------------------------------------------------------
 // Measurement: HIP events around phases and around individual kernel launches,
 // recorded only for the ids enabled in the profiling mask (api.hip).
@@ -115,8 +124,7 @@ hipError_t launch_pack(const int32_t* coords, int64_t n, const KeyLayout* L, uin
 size_t radix_temp_bytes(int64_t n);
 // Device-side key layout from the bounds partials, into cb->layout and cb->dk (see
 // k_layout); flags kErrRange / kErrWide (more than 8 * passes key bits).
-hipError_t launch_layout(const int32_t* partial, int np, int K, int stride, int t, int K3, int passes,
-                         ControlBlock* cb, hipStream_t s);
+hipError_t launch_layout(const LayoutArgs& la, hipStream_t s);
 // Sorts by the low 8 * passes key bits (passes whose digit lies above the layout's
 // key bits are plain copies); the result ends in (keys, vals).  If `coords` is
 // non-null the input is those coordinates (keys packed with the device layout *L,
@@ -124,10 +132,15 @@ hipError_t launch_layout(const int32_t* partial, int np, int K, int stride, int 
 // (nothing hangs).  by_bucket: where radix_bucket_applies(n), sort by the key's top
 // digit and then each bucket in one workgroup instead (all key bits, whatever
 // `passes`); a bucket too large for that sets kErrBucket and stays unsorted.
+// lay: the layout is not computed yet; a sort of coordinates whose first kernel is a
+// tile histogram (radix_fuses_layout) computes it there, in every workgroup, from
+// these arguments (workgroup 0 publishes it), and any other sort launches the
+// layout kernel first.  NULL: *L is ready.
 bool radix_bucket_applies(int64_t n);
+bool radix_fuses_layout(int64_t n, int passes, bool by_bucket);
 hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals,
                          uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, int passes, bool by_bucket,
-                         void* d_temp, uint32_t* err, hipStream_t s);
+                         void* d_temp, uint32_t* err, const LayoutArgs* lay, hipStream_t s);
 hipError_t launch_down_keys(const uint64_t* skeys, int64_t n, const KeyLayout* L, int64_t cell,
                             uint64_t* dkeys, uint32_t* vals, hipStream_t s);
 // Distinct consecutive keys of sorted `keys` -> qkeys, qrow = position, coords; n_q into cb.

@@ -106,11 +106,12 @@ __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int6
 // read-back before the sort.
 __device__ __forceinline__ int bit_length_u64(uint64_t v) { return v ? 64 - __clzll((long long)v) : 0; }
 
-__global__ __launch_bounds__(kThreads) void k_layout(const int32_t* partial, int np, int K, int stride, int t,
-                                                     int K3, int passes, ControlBlock* cb) {
+// One workgroup of kThreads threads computes the layout into *sL (LDS) from the
+// partials; with publish it also stores the layout, the offset deltas and the
+// flags in the control block.  Every thread of the workgroup must call it.
+__device__ void layout_from_partials(const LayoutArgs& la, bool publish, KeyLayout* sL) {
   __shared__ int32_t red[kThreads];
   __shared__ int32_t mm[8];
-  __shared__ int shift_s[4];
   const int tid = threadIdx.x;
   // thread tid reduces field f = tid % 8 over partials tid / 8, tid / 8 + 32, ...
   // (all of its loads in flight together), then 32 values per field in LDS
@@ -122,7 +123,7 @@ __global__ __launch_bounds__(kThreads) void k_layout(const int32_t* partial, int
 #pragma unroll
     for (int u = 0; u < kMaxPartials / 32; ++u) {
       const int i = tid / 8 + 32 * u;
-      v[u] = (i < np) ? partial[i * 8 + f] : r;
+      v[u] = (i < la.np) ? la.partial[i * 8 + f] : r;
     }
 #pragma unroll
     for (int u = 0; u < kMaxPartials / 32; ++u) r = is_min ? min(r, v[u]) : max(r, v[u]);
@@ -136,7 +137,7 @@ __global__ __launch_bounds__(kThreads) void k_layout(const int32_t* partial, int
   }
   __syncthreads();
   if (tid == 0) {
-    const int64_t pad = (int64_t)t * (K - 1) + (int64_t)t * stride;
+    const int64_t pad = (int64_t)la.t * (la.K - 1) + (int64_t)la.t * la.stride;
     KeyLayout L;
     int w[4];
     for (int f = 0; f < 4; ++f) {
@@ -146,27 +147,37 @@ __global__ __launch_bounds__(kThreads) void k_layout(const int32_t* partial, int
       L.width[f] = w[f];
     }
     L.total_bits = w[0] + w[1] + w[2] + w[3];
-    uint32_t err = 0;
-    if (L.total_bits > 62) err |= kErrRange;
-    if (L.total_bits > 8 * passes) err |= kErrWide;
     // shifts stay below 64 even when the extent does not fit (the build then fails)
     L.shift[3] = 0;
     L.shift[2] = min(w[3], 63);
     L.shift[1] = min(w[3] + w[2], 63);
     L.shift[0] = min(w[3] + w[2] + w[1], 63);
-    cb->layout = L;
-    for (int f = 0; f < 4; ++f) shift_s[f] = L.shift[f];
-    if (err) atomicOr(&cb->err, err);
+    *sL = L;
+    if (publish) {
+      uint32_t err = 0;
+      if (L.total_bits > 62) err |= kErrRange;
+      if (L.total_bits > 8 * la.passes) err |= kErrWide;
+      la.cb->layout = L;
+      if (err) atomicOr(&la.cb->err, err);
+    }
   }
   __syncthreads();
-  // Delta(K, t): offset k = ix K^2 + iy K + iz is t (ix - c, iy - c, iz - c)
-  const int c = (K % 2 == 1) ? (K - 1) / 2 : 0;
-  for (int k = tid; k < K3; k += kThreads) {
-    const int ix = k / (K * K), iy = (k / K) % K, iz = k % K;
-    const int64_t dx = (int64_t)t * (ix - c), dy = (int64_t)t * (iy - c), dz = (int64_t)t * (iz - c);
-    cb->dk[k] = (int64_t)((uint64_t)dx << shift_s[1]) + (int64_t)((uint64_t)dy << shift_s[2]) +
-                (int64_t)((uint64_t)dz << shift_s[3]);
+  if (publish) {
+    // Delta(K, t): offset k = ix K^2 + iy K + iz is t (ix - c, iy - c, iz - c)
+    const int K = la.K;
+    const int c = (K % 2 == 1) ? (K - 1) / 2 : 0;
+    for (int k = tid; k < la.K3; k += kThreads) {
+      const int ix = k / (K * K), iy = (k / K) % K, iz = k % K;
+      const int64_t dx = (int64_t)la.t * (ix - c), dy = (int64_t)la.t * (iy - c), dz = (int64_t)la.t * (iz - c);
+      la.cb->dk[k] = (int64_t)((uint64_t)dx << sL->shift[1]) + (int64_t)((uint64_t)dy << sL->shift[2]) +
+                     (int64_t)((uint64_t)dz << sL->shift[3]);
+    }
   }
+}
+
+__global__ __launch_bounds__(kThreads) void k_layout(LayoutArgs la) {
+  __shared__ KeyLayout sL;
+  layout_from_partials(la, true, &sL);
 }
 
 // ----------------------------------------------------------------------------
@@ -544,10 +555,15 @@ constexpr int64_t kFusedScanTiles = 256;
 // Bit position of the key's top 8-bit digit (0 for keys of at most 8 bits).
 __device__ __forceinline__ int top_digit_shift(const KeyLayout& L) { return max(L.total_bits - 8, 0); }
 
+// la.partial non-null (coordinates only): the key layout is not computed yet;
+// every workgroup computes it from the bounds partials and workgroup 0 publishes
+// it (saving the layout kernel's launch).
 template <bool FROM_COORDS, bool TILE_MAJOR, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* keys, const int4* coords, const KeyLayout* __restrict__ Lp,
-                                                         int64_t n, int shift, uint32_t* hist, int64_t ntiles) {
+                                                         int64_t n, int shift, uint32_t* hist, int64_t ntiles,
+                                                         LayoutArgs la) {
   __shared__ uint32_t h[256];
+  __shared__ KeyLayout sL;
   const int64_t base = (int64_t)blockIdx.x * (kThreads * ITEMS);
   // all of the thread's keys (or coordinates) are requested first, before the key
   // layout is read (lanes past n re-read the last key and are masked out of the
@@ -563,7 +579,13 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
       key[r] = keys[i];
   }
   h[threadIdx.x] = 0;
-  const KeyLayout L = *Lp;
+  KeyLayout L;
+  if (FROM_COORDS && la.partial) {  // kernel-argument uniform
+    layout_from_partials(la, blockIdx.x == 0, &sL);
+    L = sL;
+  } else {
+    L = *Lp;
+  }
   // a digit above the key's bits is zero for every key: the scatter copies the
   // tile and needs no histogram (the tile is counted as empty rather than left by
   // an early return, which would let the compiler move the key loads after the
@@ -1369,10 +1391,9 @@ hipError_t launch_minmax(const int32_t* a, int64_t na, const int32_t* b, int64_t
   return hipGetLastError();
 }
 
-hipError_t launch_layout(const int32_t* partial, int np, int K, int stride, int t, int K3, int passes,
-                         ControlBlock* cb, hipStream_t s) {
+hipError_t launch_layout(const LayoutArgs& la, hipStream_t s) {
   ProfScope ps(KN_MINMAX, s);
-  hipLaunchKernelGGL(k_layout, dim3(1), dim3(kThreads), 0, s, partial, np, K, stride, t, K3, passes, cb);
+  hipLaunchKernelGGL(k_layout, dim3(1), dim3(kThreads), 0, s, la);
   return hipGetLastError();
 }
 
@@ -1412,7 +1433,8 @@ namespace {
 // latency-bound.
 template <int ITEMS>
 hipError_t radix_sort_tiled_t(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
-                              uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
+                              uint32_t* vals_alt, int64_t n, int passes, void* d_temp, const LayoutArgs& lay,
+                              hipStream_t s) {
   const int64_t ntiles = (n + kThreads * ITEMS - 1) / (kThreads * ITEMS);
   uint32_t* hist = static_cast<uint32_t*>(d_temp);
   void* scan_tmp = static_cast<char*>(d_temp) + align256((size_t)256 * ntiles * sizeof(uint32_t));
@@ -1437,7 +1459,7 @@ hipError_t radix_sort_tiled_t(const int32_t* coords, const KeyLayout* L, uint64_
       ProfScope ps(KN_RADIX_HIST, s);
 #define SPC_H(FC, TM)                                                                                           \
   hipLaunchKernelGGL((k_radix_tile_hist<FC, TM, ITEMS>), dim3(g), dim3(kThreads), 0, s, FC ? nullptr : kb[src],      \
-                     FC ? c4 : nullptr, L, n, shift, hist, ntiles)
+                     FC ? c4 : nullptr, L, n, shift, hist, ntiles, FC ? lay : LayoutArgs{})
       if (first) {
         if (fused) SPC_H(true, true); else SPC_H(true, false);
       } else {
@@ -1471,10 +1493,11 @@ hipError_t radix_sort_tiled_t(const int32_t* coords, const KeyLayout* L, uint64_
 }
 
 hipError_t radix_sort_tiled(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
-                            uint32_t* vals_alt, int64_t n, int passes, void* d_temp, hipStream_t s) {
+                            uint32_t* vals_alt, int64_t n, int passes, void* d_temp, const LayoutArgs& lay,
+                            hipStream_t s) {
   if ((n + kRsTileSmall - 1) / kRsTileSmall <= kFusedScanTiles)
-    return radix_sort_tiled_t<kRsItemsSmall>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
-  return radix_sort_tiled_t<kRsItems>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
+    return radix_sort_tiled_t<kRsItemsSmall>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, lay, s);
+  return radix_sort_tiled_t<kRsItems>(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, lay, s);
 }
 
 // By-bucket sort (three launches; see radix_bucket_applies for its sizes): tile histograms
@@ -1483,7 +1506,7 @@ hipError_t radix_sort_tiled(const int32_t* coords, const KeyLayout* L, uint64_t*
 // one workgroup per bucket sorting it into (keys, vals).
 hipError_t radix_sort_bucket(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals,
                              uint64_t* keys_alt, uint32_t* vals_alt, int64_t n, void* d_temp, uint32_t* err,
-                             hipStream_t s) {
+                             const LayoutArgs& lay, hipStream_t s) {
   constexpr int ITEMS = kRsItemsSmall;
   const int64_t ntiles = (n + kThreads * ITEMS - 1) / (kThreads * ITEMS);
   uint32_t* hist = static_cast<uint32_t*>(d_temp);
@@ -1497,10 +1520,10 @@ hipError_t radix_sort_bucket(const int32_t* coords, const KeyLayout* L, uint64_t
     ProfScope ps(KN_RADIX_HIST, s);
     if (coords)
       hipLaunchKernelGGL((k_radix_tile_hist<true, true, ITEMS>), dim3(g), dim3(kThreads), 0, s, nullptr, c4, L, n, -1,
-                         hist, ntiles);
+                         hist, ntiles, lay);
     else
       hipLaunchKernelGGL((k_radix_tile_hist<false, true, ITEMS>), dim3(g), dim3(kThreads), 0, s, keys, nullptr, L, n,
-                         -1, hist, ntiles);
+                         -1, hist, ntiles, LayoutArgs{});
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -1526,18 +1549,33 @@ hipError_t radix_sort_bucket(const int32_t* coords, const KeyLayout* L, uint64_t
 // itself (at most kFusedScanTiles tiles of 1024 keys).
 bool radix_bucket_applies(int64_t n) { return n > 1 && (n + kRsTileSmall - 1) / kRsTileSmall <= kFusedScanTiles; }
 
+// Whether radix_sort_kv of n coordinates starts with a tile histogram (by bucket,
+// or digit by digit below the one-kernel passes), which can compute the layout.
+bool radix_fuses_layout(int64_t n, int passes, bool by_bucket) {
+  if (by_bucket && radix_bucket_applies(n)) return true;
+  return n > 1 && passes > 0 && passes <= kRsMaxPasses && n < ((int64_t)1 << 30) &&
+         (n + kRsTile - 1) / kRsTile < kOnesweepMinTiles;
+}
+
 hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
                          uint32_t* vals_alt, int64_t n, int passes, bool by_bucket, void* d_temp, uint32_t* err,
-                         hipStream_t s) {
+                         const LayoutArgs* lay, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  const bool fuse = lay && coords && radix_fuses_layout(n, passes, by_bucket);
+  if (lay && !fuse) {
+    hipError_t e = launch_layout(*lay, s);
+    if (e != hipSuccess) return e;
+  }
+  const LayoutArgs none{};
+  const LayoutArgs& la = fuse ? *lay : none;
   if (by_bucket && radix_bucket_applies(n))
-    return radix_sort_bucket(coords, L, keys, vals, keys_alt, vals_alt, n, d_temp, err, s);
+    return radix_sort_bucket(coords, L, keys, vals, keys_alt, vals_alt, n, d_temp, err, la, s);
   if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
   if (n <= 1 || passes == 0) return hipSuccess;
   if (passes > kRsMaxPasses || n >= ((int64_t)1 << 30)) return hipErrorInvalidValue;
   const int64_t ntiles = (n + kRsTile - 1) / kRsTile;
   if (ntiles < kOnesweepMinTiles)
-    return radix_sort_tiled(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, s);
+    return radix_sort_tiled(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, la, s);
   const size_t gpart_bytes = (size_t)kRsUpBlocks * kRsMaxPasses * 256 * sizeof(uint32_t);
   uint32_t* gpart = static_cast<uint32_t*>(d_temp);
   uint32_t* gofs = reinterpret_cast<uint32_t*>(static_cast<char*>(d_temp) + align256(gpart_bytes));

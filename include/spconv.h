@@ -130,10 +130,13 @@ size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode,
  * kernel publishes them into mapped host memory as it starts, and the build
  * returns while that kernel still writes the pair lists and tables.  Work on
  * `stream` (or after synchronising it) sees the complete map; other streams must
- * wait for `stream` first.  The host plans the radix
- * sort's passes before the layout is known (from the previous build of the same
- * inputs); a key wider than planned is detected and the build redone, so a first
- * build of unusually wide coordinates costs two passes over the Map.
+ * wait for `stream` first.  Up to 262,144 points the sort goes by bucket (the
+ * key's top digit, then each bucket in one workgroup); a bucket of more than 8192
+ * points is detected and the build redone digit by digit.  The host plans the
+ * digit-by-digit sort's passes before the layout is known (from the previous build
+ * of the same inputs); a key wider than planned is detected and the build redone.
+ * Both choices are kept per input, so only a first build can cost two passes
+ * over the Map.
  * On success *out_map owns a host object to release with spconv_free_map(). */
 int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords,
                      int64_t n_out, int K, int stride, int tensor_stride, int mode,

@@ -739,27 +739,52 @@ constexpr int kBucketThreads = 1024;
 constexpr int kBucketWaves = kBucketThreads / kWave;
 constexpr int kBucketItems = 8;
 constexpr int kBucketCap = kBucketThreads * kBucketItems;
+// keys, per-wave peer masks (u64 per digit), values, per-wave digit counters, wave totals
 constexpr size_t kBucketLds = (size_t)kBucketCap * (sizeof(uint64_t) + sizeof(uint32_t)) +
-                              (size_t)kBucketWaves * 256 * sizeof(uint32_t) + 64 * sizeof(uint32_t);
+                              (size_t)kBucketWaves * 256 * (sizeof(uint64_t) + sizeof(uint32_t)) + 64 * sizeof(uint32_t);
+
+// Inclusive prefix sum over the 64 lanes: shifts within each 16-lane row (DPP
+// row_shr; a lane with no source lane adds 0), then the totals of the rows below.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, int lane) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const int row = lane >> 4;
+  return x + (row > 0 ? r0 : 0u) + (row > 1 ? r1 : 0u) + (row > 2 ? r2 : 0u);
+}
 
 // Bucket b = [bucket_start[b], bucket_start[b + 1]) of (kin, vin), sorted into the
 // same positions of (kout, vout) (which may be kin, vin: each workgroup reads its
 // whole bucket before it writes).  A bucket of m keys takes ipt = ceil(m / 1024)
 // items per lane, spread over all waves: slot s is item r of lane l of wave w for
-// s = w 64 ipt + r 64 + l, so each wave ranks a contiguous run of slots with wave
-// ballots (stable) in ipt rounds; LDS holds the permuted bucket between digits.
+// s = w 64 ipt + r 64 + l, so each wave ranks a contiguous run of slots (stable)
+// in ipt rounds; LDS holds the permuted bucket between digits.
+//
+// Ranking an item: the lane ORs its bit into its wave's mask word for its digit
+// and reads the word back, which gives the lanes of the wave holding the same
+// digit (two LDS operations in place of eight wave ballots); the lowest such lane
+// adds their count to the wave's digit counter and clears the word again.  The
+// counters are then turned into first positions by one scan over (digit, wave)
+// in digit-major order: each thread sums four waves of one digit, the waves scan
+// those sums, and the sixteen wave totals are added in.
 __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* kin, const uint32_t* vin,
                                                                 uint64_t* kout, uint32_t* vout,
                                                                 const uint32_t* __restrict__ bucket_start,
                                                                 const KeyLayout* __restrict__ Lp, uint32_t* err) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* skey = reinterpret_cast<uint64_t*>(smem);
-  uint32_t* sval = reinterpret_cast<uint32_t*>(skey + kBucketCap);
+  uint64_t(*pm)[256] = reinterpret_cast<uint64_t(*)[256]>(skey + kBucketCap);
+  uint32_t* sval = reinterpret_cast<uint32_t*>(&pm[kBucketWaves][0]);
   uint32_t(*wc)[256] = reinterpret_cast<uint32_t(*)[256]>(sval + kBucketCap);
-  uint32_t* s_part = &wc[kBucketWaves][0];  // 64 words of scan scratch
+  uint32_t* s_part = &wc[kBucketWaves][0];  // wave totals of the scan
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
+  const int bits = max(Lp->total_bits - 8, 0);  // the bucket pass sorted the bits above
   const uint32_t b0 = bucket_start[blockIdx.x];
   const uint32_t b1 = bucket_start[blockIdx.x + 1];
   const int m = (b1 > b0) ? (int)min(b1 - b0, (uint32_t)(kBucketCap + 1)) : 0;
@@ -776,11 +801,10 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* 
   }
   // Items per lane: the ranking rounds run serially, so a bucket is spread over
   // all waves (a typical bucket then takes one round).  Only the first nwv waves
-  // hold slots; the others skip every step but the barriers, and item r of a wave
-  // is skipped as a whole past ipt or once its slots start past the bucket (both
-  // wave-uniform).
+  // hold slots; the others skip every step but the barriers and the scan, and
+  // item r of a wave is skipped as a whole past ipt or once its slots start past
+  // the bucket (both wave-uniform).
   const int ipt = (m + kBucketThreads - 1) / kBucketThreads;
-  const int nwv = (m + kWave * ipt - 1) / (kWave * ipt);
   auto slot = [&](int r) { return wave * (kWave * ipt) + r * kWave + lane; };
   auto item_live = [&](int r) { return r < ipt && wave * (kWave * ipt) + r * kWave < m; };
   uint64_t key[kBucketItems];
@@ -791,48 +815,50 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* 
     key[r] = item_live(r) ? kin[i] : 0ull;
     val[r] = item_live(r) ? vin[i] : 0u;
   }
-  const KeyLayout L = *Lp;
-  const int bits = top_digit_shift(L);  // the bucket pass sorted the bits above
+  // counters (all 16 rows: 4 words per thread) and peer masks start at zero;
+  // every use of a mask word leaves it zero again
+  uint4* wc4 = reinterpret_cast<uint4*>(&wc[0][0]);
+  wc4[tid] = make_uint4(0, 0, 0, 0);
+  for (int i = tid; i < kBucketWaves * 256; i += kBucketThreads) (&pm[0][0])[i] = 0ull;
+  const uint64_t mybit = 1ull << lane;
+  const int sd = tid >> 2;        // scan: this thread's digit ...
+  const int sw = (tid & 3) * 4;   // ... and its first of four waves
+  __syncthreads();
   for (int sh = 0; sh < bits; sh += 8) {
-    for (int i = tid; i < nwv * 256; i += kBucketThreads) (&wc[0][0])[i] = 0;
-    __syncthreads();
     uint32_t rank[kBucketItems];
 #pragma unroll
     for (int r = 0; r < kBucketItems; ++r) {
       rank[r] = 0;
       if (!item_live(r)) continue;
-      const bool valid = slot(r) < m;
-      const uint32_t d = (uint32_t)(key[r] >> sh) & 255u;
-      const uint64_t peers = match_digit(d, valid);
-      if (valid) {
+      if (slot(r) < m) {
+        const uint32_t d = (uint32_t)(key[r] >> sh) & 255u;
+        __hip_atomic_fetch_or(&pm[wave][d], mybit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const uint64_t peers = __hip_atomic_load(&pm[wave][d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         const uint32_t before = (uint32_t)popc64(peers & lanemask_lt());
         rank[r] = wc[wave][d] + before;
-        if (before == 0) wc[wave][d] += (uint32_t)popc64(peers);
+        if (before == 0) {
+          wc[wave][d] += (uint32_t)popc64(peers);
+          pm[wave][d] = 0ull;
+        }
       }
     }
     __syncthreads();
-    // digit d's first position: threads 0..255 (waves 0..3) scan the digit totals
-    uint32_t tot = 0, x = 0;
-    if (tid < 256) {
-      for (int w = 0; w < nwv; ++w) tot += wc[w][tid];
-      x = tot;
+    const uint32_t c0 = wc[sw][sd], c1 = wc[sw + 1][sd], c2 = wc[sw + 2][sd], c3 = wc[sw + 3][sd];
+    const uint32_t tsum = c0 + c1 + c2 + c3;
+    const uint32_t incl = wave_incl_scan(tsum, lane);
+    if (lane == kWave - 1) s_part[wave] = incl;
+    __syncthreads();
+    uint32_t start = incl - tsum;
 #pragma unroll
-      for (int dd = 1; dd < kWave; dd <<= 1) {
-        const uint32_t y = __shfl_up(x, dd, kWave);
-        if (lane >= dd) x += y;
-      }
-      if (lane == kWave - 1) s_part[wave] = x;
+    for (int q = 0; q < kBucketWaves / 4; ++q) {
+      const uint4 v = reinterpret_cast<const uint4*>(s_part)[q];
+      start += (4 * q < wave ? v.x : 0u) + (4 * q + 1 < wave ? v.y : 0u) + (4 * q + 2 < wave ? v.z : 0u) +
+               (4 * q + 3 < wave ? v.w : 0u);
     }
-    __syncthreads();
-    if (tid < 256) {
-      uint32_t start = x - tot;
-      for (int w = 0; w < wave; ++w) start += s_part[w];
-      for (int w = 0; w < nwv; ++w) {
-        const uint32_t c = wc[w][tid];
-        wc[w][tid] = start;
-        start += c;
-      }
-    }
+    wc[sw][sd] = start;
+    wc[sw + 1][sd] = start + c0;
+    wc[sw + 2][sd] = start + c0 + c1;
+    wc[sw + 3][sd] = start + c0 + c1 + c2;
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kBucketItems; ++r) {
@@ -851,7 +877,8 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(const uint64_t* 
       key[r] = skey[sl];
       val[r] = sval[sl];
     }
-    __syncthreads();  // the next digit rewrites wc and the stage
+    wc4[tid] = make_uint4(0, 0, 0, 0);  // the next digit's counters
+    __syncthreads();                    // ... and its stage
   }
 #pragma unroll
   for (int r = 0; r < kBucketItems; ++r) {

@@ -232,17 +232,6 @@ __device__ __forceinline__ void st_coherent(uint32_t* p, uint32_t v) {
 
 // Lanes of the wave whose digit equals this lane's digit, among the active lanes
 // that pass `valid`.
-__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid = true) {
-  uint64_t m = __ballot(valid);
-#pragma unroll
-  for (int b = 0; b < 8; ++b) {
-    const bool bit = (d >> b) & 1u;
-    const uint64_t bal = __ballot(bit);
-    m &= bit ? bal : ~bal;
-  }
-  return m;
-}
-
 template <bool FROM_COORDS>
 __device__ __forceinline__ uint64_t load_key(const uint64_t* keys, const int4* coords, const KeyLayout& L, int64_t i) {
   if constexpr (FROM_COORDS) {
@@ -281,6 +270,7 @@ struct TileLds {
   uint32_t gbase[256];  // global position of the tile's first key of each digit
   uint32_t cnt[256];    // the tile's count of each digit
   uint32_t wc[kWavesPerBlock][256];  // per-wave digit counts, then each wave's first position
+  uint64_t pm[kWavesPerBlock][256];  // per-wave lanes holding each digit (zero between uses)
   uint32_t s_wave[kWavesPerBlock];
 };
 
@@ -341,8 +331,11 @@ __device__ __forceinline__ void tile_pack(const KeyLayout& L, const int4 crd[ITE
 
 // Stable ranks within the wave's run: rank[r] = number of earlier keys of the
 // wave with the same digit.  Leaves the wave's digit counts in t.wc[wave] (which
-// must be zero).  No workgroup barrier: a wave's LDS accesses complete in order,
-// so every lane reads a counter before its digit's leader bumps it.
+// must be zero).  Each lane ORs its bit into the wave's mask word of its digit
+// and reads the word back: the lanes holding the same digit.  The lowest of them
+// bumps the counter and clears the word (t.pm must be zero and is left so).  No
+// workgroup barrier: a wave's LDS accesses complete in order, so every lane reads
+// a word before its digit's leader rewrites it.
 template <int ITEMS>
 __device__ __forceinline__ void tile_rank(TileLds<ITEMS>& t, const uint64_t key[ITEMS], int64_t base, int64_t n,
                                           int shift, uint32_t rank[ITEMS]) {
@@ -351,12 +344,17 @@ __device__ __forceinline__ void tile_rank(TileLds<ITEMS>& t, const uint64_t key[
   for (int r = 0; r < ITEMS; ++r) {
     const bool valid = tile_index<ITEMS>(base, r) < n;
     const uint32_t d = (uint32_t)(key[r] >> shift) & 255u;
-    const uint64_t peers = match_digit(d, valid);
     rank[r] = 0;
     if (valid) {
+      __hip_atomic_fetch_or(&t.pm[wave][d], 1ull << (threadIdx.x & (kWave - 1)), __ATOMIC_RELAXED,
+                            __HIP_MEMORY_SCOPE_WORKGROUP);
+      const uint64_t peers = __hip_atomic_load(&t.pm[wave][d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       const uint32_t before = (uint32_t)popc64(peers & lanemask_lt());
       rank[r] = t.wc[wave][d] + before;
-      if (before == 0) t.wc[wave][d] += (uint32_t)popc64(peers);
+      if (before == 0) {
+        t.wc[wave][d] += (uint32_t)popc64(peers);
+        t.pm[wave][d] = 0ull;
+      }
     }
   }
 }
@@ -426,8 +424,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_upsweep(const uint64_t* keys
     const uint64_t key = load_key<FROM_COORDS>(keys, coords, L, i);
     for (int p = 0; p < passes; ++p) {
       const uint32_t d = (uint32_t)(key >> (8 * p)) & 255u;
-      const uint64_t peers = match_digit(d);
-      if ((peers & lanemask_lt()) == 0) atomicAdd(&h[p][d], (uint32_t)popc64(peers));
+      atomicAdd(&h[p][d], 1u);
     }
   }
   __syncthreads();
@@ -483,7 +480,10 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
   const int shift = 8 * pass;
   if (tid == 0) s_tile = atomicAdd(&tickets[pass], 1u);
 #pragma unroll
-  for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
+  for (int w = 0; w < kWavesPerBlock; ++w) {
+    t.wc[w][tid] = 0;
+    t.pm[w][tid] = 0ull;
+  }
   __syncthreads();
   const int64_t tile = s_tile;
   const int64_t base = tile * kRsTile;
@@ -605,8 +605,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_hist(const uint64_t* ke
   for (int r = 0; r < ITEMS; ++r) {
     const bool valid = active && base + r * kThreads + threadIdx.x < n;
     const uint32_t d = (uint32_t)(key[r] >> sh) & 255u;
-    const uint64_t peers = match_digit(d, valid);
-    if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)popc64(peers));
+    if (valid) atomicAdd(&h[d], 1u);
   }
   __syncthreads();
   if (TILE_MAJOR)  // 16-bit counts (a tile holds at most kThreads * ITEMS <= 2048 keys)
@@ -641,7 +640,10 @@ __global__ __launch_bounds__(kThreads) void k_radix_tile_scatter(const uint64_t*
   int4 crd[FROM_COORDS ? ITEMS : 1];
   tile_fetch<FROM_COORDS, ITEMS>(kin, vin, coords, base, n, key, crd, val);
 #pragma unroll
-  for (int w = 0; w < kWavesPerBlock; ++w) t.wc[w][tid] = 0;
+  for (int w = 0; w < kWavesPerBlock; ++w) {
+    t.wc[w][tid] = 0;
+    t.pm[w][tid] = 0ull;
+  }
   if (FUSED) {
     // A 16-byte load holds 8 counts, so a wave's load covers two tiles: lane l
     // reads digits 8 (l % 32) .. + 7 of tile 2 p + l / 32 for tile pairs

@@ -198,8 +198,9 @@ __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, con
 // LSD radix sort of (u64 key, u32 value), 8-bit digits, stable.  Large inputs
 // run one kernel per pass: an up-front kernel counts the digits of every pass
 // in one read (per-block partials, reduced by a second small kernel, no global
-// atomics); each pass kernel then takes a tile ticket, ranks its keys with
-// wave64 ballots that match equal digits, publishes its per-digit counts, and
+// atomics); each pass kernel then takes a tile ticket, ranks its keys within
+// each wave (per-wave LDS masks of the lanes holding each digit), publishes its
+// per-digit counts, and
 // adds up the counts of all earlier tiles by looking back over their published
 // words.  Tiles are numbered in start order, so every tile a workgroup waits
 // for is already running; waits are bounded and report an error flag instead
@@ -768,7 +769,7 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, int lane) {
 //
 // Ranking an item: the lane ORs its bit into its wave's mask word for its digit
 // and reads the word back, which gives the lanes of the wave holding the same
-// digit (two LDS operations in place of eight wave ballots); the lowest such lane
+// digit (two LDS operations in place of a match by eight wave ballots); the lowest such lane
 // adds their count to the wave's digit counter and clears the word again.  The
 // counters are then turned into first positions by one scan over (digit, wave)
 // in digit-major order: each thread sums four waves of one digit, the waves scan

@@ -420,6 +420,22 @@ def test_sort_bucket_over_capacity_redone_digit_by_digit():
         assert_map_equal(B.KernelMap.build(dc, 3), okm)
 
 
+@pytest.mark.parametrize("m", [1000, 1024, 1025, 2049, 8191, 8192])
+def test_sort_one_bucket_of_m_keys(m):
+    """The first m points of a 128 x 128 plane at x = 0 plus one point at x = 1000:
+    the plane fills one bucket of exactly m keys, the far point a bucket of one.
+    The sizes sit at the bucket sort's boundaries: one item per lane up to 1024
+    keys, two from 1025, three from 2049, and 8192, the most one workgroup sorts
+    without a redo.  The map must equal the oracle's."""
+    say(f"one bucket of {m} keys")
+    g = np.stack(np.meshgrid(np.arange(128), np.arange(128), indexing="ij"), -1).reshape(-1, 2)[:m]
+    plane = np.concatenate([np.zeros((m, 2), np.int64), g], 1)
+    c = np.concatenate([plane, [[0, 1000, 0, 0]]]).astype(np.int32)
+    c = c[np.random.default_rng(m).permutation(len(c))]
+    okm = oracle.kernel_map(c, None, 3, 1, "subm")
+    assert_map_equal(B.KernelMap.build(to_dev(c), 3), okm)
+
+
 def test_deterministic_pairs():
     say("deterministic pair order")
     c = scenes.workload(1).coords

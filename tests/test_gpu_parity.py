@@ -436,6 +436,25 @@ def test_sort_one_bucket_of_m_keys(m):
     assert_map_equal(B.KernelMap.build(to_dev(c), 3), okm)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_clouds_maps_match_oracle(seed):
+    """Seeded sweep of random clouds: 1 to 60k voxels in 1 to 4 batches, cubes of
+    side 4 to 119 placed anywhere in [-600, 720), K in {2, 3, 5}.  The sizes keep the
+    by-bucket sort, so bucket sizes, empty and lone-key buckets and digit
+    collisions in the ranking vary from case to case.  Maps must equal the
+    oracle's."""
+    rng = np.random.default_rng(9000 + seed)
+    K = int(rng.choice([2, 3, 5]))
+    nb = int(rng.integers(1, 5))
+    side = int(rng.integers(4, 120))
+    lo = int(rng.integers(-600, 600))
+    n = int(min(rng.integers(1, 60000), nb * side ** 3))
+    say(f"random cloud seed={seed}: n={n} batches={nb} side={side} lo={lo} K={K}")
+    c = _cloud(9100 + seed, n, lo, lo + side, nb=nb)
+    okm = oracle.kernel_map(c, None, K, 1, "subm")
+    assert_map_equal(B.KernelMap.build(to_dev(c), K), okm)
+
+
 def test_deterministic_pairs():
     say("deterministic pair order")
     c = scenes.workload(1).coords

@@ -96,7 +96,9 @@ def kernel_models(n, n_out, pairs, L, k3, passes, fused=True):
         "k_forward_count": ("hbm", 8 * n_out + 8 * n + 4 * k3 * n_out),
         # write pass: reads the results and the rows of the matches; writes the pair lists,
         # the query-side table's matches (in place) and the whole source-side table
-        "k_forward_write": ("hbm", 4 * k3 * n_out + 4 * n_out + 4 * n + 12 * pairs + 4 * k3 * n),
+        # (odd-K submanifold maps leave the source-side table to the first table-driven gather)
+        "k_forward_write": ("hbm", 4 * k3 * n_out + 4 * n_out + 4 * n + 12 * pairs
+                            + (0 if (L.mode == "subm" and L.K % 2 == 1) else 4 * k3 * n)),
         "k_backward": ("hbm", 8 * n_out),
         # source-side table fill (maps other than odd-K submanifold ones)
         "k_fill": ("hbm", 4 * k3 * n),

@@ -180,7 +180,13 @@ size_t spconv_forward_workspace_bytes(const spconv_map* m, int c_in, int c_out, 
  *   without pairs get zeros).  Products accumulate in float32.
  * Requirements: c_in, c_out in [1, 1024]; 16-byte rows (c * element size % 16 == 0)
  * and c_out % 16 == 0; d_x, d_w, d_y (and d_residual) 16-byte aligned, else
- * SPCONV_EINVAL.  Asynchronous on `stream`; no host synchronisation. */
+ * SPCONV_EINVAL.  Asynchronous on `stream`; no host synchronisation.
+ * A SPCONV_SUBM map with odd K builds the input-side metadata table of Algorithm
+ * 1's gather lazily: the first call that gathers through the table (gather =
+ * SPCONV_GATHER_BUFFER) fills it from the pair lists on its `stream`, so calls on
+ * other streams must be ordered after that one, and calls with the same map must
+ * not run concurrently from several host threads.  The fused gather (the default)
+ * reads the pair lists and never needs the table. */
 int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in,
                    int c_out, int dtype, const spconv_options* opt, void* d_workspace,
                    size_t ws_bytes, void* stream);

@@ -32,6 +32,12 @@ struct spconv_map {
   const uint32_t* in_perm = nullptr;
   const uint32_t* out_perm = nullptr;
   bool transposed = false;
+  // A symmetric submanifold map leaves its source-side table (imt) to be filled
+  // from the pair lists by the first forward call that gathers through it; the
+  // fused gather reads the pair lists and never needs it.
+  mutable bool imt_pending = false;
+  const uint32_t* seg_dev = nullptr;  // device pair starts, K3 + 1 entries
+  uint32_t* inv_scratch = nullptr;    // n_in words of the build's scratch
 };
 
 namespace {
@@ -613,6 +619,7 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
   a.ts = b.ts;
   a.ts_stride = b.ts_stride;
   a.sym = (mode == SPCONV_SUBM && K % 2 == 1) ? 1 : 0;
+  a.write_ts = a.sym ? 0 : 1;
   a.pair_cap = (int64_t)K3 * nq_max;
   PubBuffer* pb = pub_buffer();
   if (!pb) return bail(fail(SPCONV_EHIP, "mapped host buffer allocation failed"));
@@ -701,6 +708,11 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
     m->omt = b.res;
     m->omt_stride = b.res_stride;
     m->out_perm = q_perm;
+  }
+  if (!a.write_ts) {
+    m->imt_pending = true;
+    m->seg_dev = b.cb->seg_pair_start;
+    m->inv_scratch = b.valt;
   }
   *out_map = m;
   return SPCONV_OK;
@@ -873,6 +885,16 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
   const int K3 = m->omt ? m->K3 : 0;
   if (p.rows_real > 0) {
     const bool fused = p.gather == SPCONV_GATHER_FUSED;
+    if (!fused && m->imt_pending) {
+      PhaseScope ph(PH_METADATA, s);
+      int32_t* ts = const_cast<int32_t*>(m->imt);
+      SPC_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(ts), 0xFFFFFFFFu, (int64_t)m->K3 * m->imt_stride, s),
+              "source-side table fill");
+      SPC_TRY(launch_ts_from_pairs(m->pin, m->seg_dev, m->K3, m->ptr[m->K3], m->in_perm, m->n_in, m->inv_scratch, ts,
+                                   m->imt_stride, s),
+              "source-side table from the pairs");
+      m->imt_pending = false;
+    }
     if (!fused) {
       PhaseScope ph(PH_GATHER, s);
       SPC_TRY(launch_gather(d_x, m->n_in, c_in, p.elem, m->imt, m->imt_stride, m->in_perm, K3, b.buf_in, p.t_gather,

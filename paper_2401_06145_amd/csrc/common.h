@@ -114,6 +114,13 @@ hipError_t scan_exclusive_u32(const uint32_t* d_in, uint32_t* d_out, int64_t n, 
 
 // map_kernels.hip
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+// T_s from the pair lists: ts[k stride + sorted source position of pin[e]] = e
+// for every pair e of offset k (seg: the device's K3 + 1 pair starts).  perm:
+// caller row of each sorted source position, or NULL (identity); inv: n_src
+// words of scratch for its inverse.  The table must be filled with -1 first.
+hipError_t launch_ts_from_pairs(const int32_t* pin, const uint32_t* seg, int K3, int64_t n_pairs,
+                                const uint32_t* perm, int64_t n_src, uint32_t* inv, int32_t* ts,
+                                int64_t stride, hipStream_t s);
 size_t minmax_temp_bytes();
 // Per-block coordinate bounds of a[0..na) and b[0..nb): *n_partial rows of 8
 // int32 (min b,x,y,z then max b,x,y,z) in `partial`; also resets cb's counters.
@@ -177,6 +184,9 @@ struct SearchArgs {
   // has no partner at the mirrored offset K^3 - 1 - k, so the write pass marks
   // that T_s entry instead of a separate fill.
   int sym;
+  // 0: the write pass leaves T_s alone (a symmetric map's T_s is filled from the
+  // pair lists when a table-driven gather first needs it)
+  int write_ts;
   // Mapped, coherent host buffer (or NULL).  The write pass's first workgroup
   // copies the control block's head (kControlHeadBytes) into it, then stores
   // pub_seq at byte kPubFlagOffset: the host reads the counts while the rest of

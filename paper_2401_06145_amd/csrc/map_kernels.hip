@@ -1123,7 +1123,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
       bal[r] = __ballot(hit);
       if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal[r]);
     }
-    if (a.sym) {
+    if (a.sym && a.write_ts) {
 #pragma unroll
       for (int r = 0; r < ROUNDS; ++r) {
         const int64_t qp = q0 + (int64_t)r * kThreads + tid;
@@ -1153,7 +1153,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
         pin[o] = r_in[r];
         pout[o] = r_out[r];
         res[qp] = (int32_t)o;
-        ts[sp[r]] = (int32_t)o;
+        if (a.write_ts) ts[sp[r]] = (int32_t)o;
       }
     }
     base += total;
@@ -1402,6 +1402,52 @@ __global__ __launch_bounds__(kThreads) void k_hash_count(SearchArgs a, const uin
 // ----------------------------------------------------------------------------
 // Launchers
 // ----------------------------------------------------------------------------
+// ----------------------------------------------------------------------------
+// Source-side table from the pair lists (Section 2.2's metadata table of the
+// inputs): entry (k, p) = buffer row of sorted source p's pair at offset k.
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_inverse_perm(const uint32_t* __restrict__ perm, int64_t n,
+                                                           uint32_t* __restrict__ inv) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) inv[perm[i]] = (uint32_t)i;
+}
+
+__global__ __launch_bounds__(kThreads) void k_ts_from_pairs(const int32_t* __restrict__ pin,
+                                                            const uint32_t* __restrict__ seg, int K3,
+                                                            int64_t n_pairs, const uint32_t* __restrict__ inv,
+                                                            int32_t* __restrict__ ts, int64_t stride) {
+  __shared__ uint32_t s_seg[kMaxOffsets + 1];
+  for (int i = threadIdx.x; i <= K3; i += kThreads) s_seg[i] = seg[i];
+  __syncthreads();
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= n_pairs) return;
+  // the pair's offset: seg[lo] <= e < seg[hi] throughout (seg[0] = 0, seg[K3] = n_pairs)
+  int lo = 0, hi = K3;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if ((int64_t)s_seg[mid] <= e) lo = mid; else hi = mid;
+  }
+  const int32_t row = pin[e];
+  const int64_t p = inv ? (int64_t)inv[row] : (int64_t)row;
+  ts[(int64_t)lo * stride + p] = (int32_t)e;
+}
+
+hipError_t launch_ts_from_pairs(const int32_t* pin, const uint32_t* seg, int K3, int64_t n_pairs,
+                                const uint32_t* perm, int64_t n_src, uint32_t* inv, int32_t* ts,
+                                int64_t stride, hipStream_t s) {
+  if (K3 < 1 || K3 > kMaxOffsets || n_src > stride) return hipErrorInvalidValue;
+  if (n_pairs <= 0) return hipSuccess;
+  if (perm) {
+    hipLaunchKernelGGL(k_inverse_perm, dim3((unsigned)((n_src + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
+                       perm, n_src, inv);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_ts_from_pairs, dim3((unsigned)((n_pairs + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
+                     pin, seg, K3, n_pairs, perm ? inv : nullptr, ts, stride);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   ProfScope ps(KN_FILL, s);

@@ -72,9 +72,10 @@ def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = Fals
     per_launch = {
         "k_radix_scatter": (16 * n + 12 * n + (passes - 1) * 24 * n) / max(passes, 1),
         "k_forward_count": 8 * n + 8 * n + 4 * k3 * n,
-        # reads the results and the rows of the matches; writes the pair lists, the
-        # query-side table's matches and the whole source-side table
-        "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 12 * pairs + 4 * k3 * n,
+        # reads the results and the rows of the matches; writes the pair lists and the
+        # query-side table's matches (an odd-K submanifold map leaves the source-side
+        # table to the first table-driven gather)
+        "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 12 * pairs,
     }
     row = {"voxels": n, "grid": side, "search": "hash" if hash_search else "sorted", "pairs": pairs,
            "map_ms": round(map_ms, 4),

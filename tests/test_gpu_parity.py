@@ -326,6 +326,29 @@ def test_gather_forms_bit_identical(dtype, c_in, c_out, pd):
     assert rel_err(to_f64(base), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("search,K", [(0, 3), (0, 5), (1, 3), (1, 5)])
+def test_source_table_filled_on_first_table_gather(search, K):
+    """An odd-K submanifold map leaves its source-side metadata table to the first
+    forward call that gathers through it (the table is filled from the pair
+    lists then).  Sorted-search maps index the table by sorted position,
+    hash-table maps by caller row.  Two table-driven calls must equal the fused
+    gather's output bit for bit, and the oracle within tolerance."""
+    say(f"source-side table on first use, search={search} K={K}")
+    c = _cloud(300 + 10 * search + K, 5000, -11, 11)
+    x = scenes.features(len(c), 32, "f16", 301)
+    w = scenes.weights(K, 32, 32, "f16", 302)
+    km = B.KernelMap.build(to_dev(c), K, opt=B.Options.make(search=search))
+    xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
+    td = B.TORCH_DTYPES["f16"]
+    y_fused = B.Forward(km, 32, 32, td, B.Options.make(gather=B.GATHER_FUSED))(xd, wd)
+    fwd = B.Forward(km, 32, 32, td, B.Options.make(gather=B.GATHER_BUFFER))
+    for _ in range(2):
+        assert torch.equal(fwd(xd, wd), y_fused)
+    okm = oracle.kernel_map(c, None, K, 1, "subm")
+    ref = oracle.features(scenes.to_f64(x, "f16"), scenes.to_f64(w, "f16"), okm)
+    assert rel_err(to_f64(y_fused), ref) <= TOL["f16"]
+
+
 @pytest.mark.parametrize("c_in", [16, 48])
 def test_padding_lanes_feed_exact_zeros(c_in):
     """When c_in does not fill the 32-deep MFMA k-steps, the padding lanes read a

@@ -36,9 +36,10 @@ constexpr int kMinmaxBlocks = 256;
 constexpr int kMinmaxBatch = 8;  // rows in flight per thread
 constexpr int kMaxPartials = kMinmaxBlocks;  // bounds partials reduced by the layout kernel
 
-// Per-block bounds of the coordinates; the host reduces the partials (it has to
-// wait for them anyway, to lay out the keys).  Block 0 also resets the control
-// block's counters for this build.
+// Per-block bounds of the coordinates; the device reduces the partials and lays
+// out the keys (inside the first sort histogram, or k_layout), so the host does
+// not wait for them.  Block 0 also resets the control block's counters for the
+// map build.
 __global__ __launch_bounds__(kThreads) void k_minmax_partial(const int4* a, int64_t na, const int4* b, int64_t nb,
                                                              int32_t* partial, ControlBlock* cb) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {

@@ -8,6 +8,12 @@
            and a JSON record that bench.py reads for the roofline's ``traffic``
            field; the record keeps a hash of each kernel's sources, so a kernel
            changed since the counters were taken reports no traffic.
+  counters MFMA utilisation (the derived ``MfmaUtil`` counter: MFMA-busy cycles
+           over GPU-active cycles times SIMDs, in percent), MFMA flops executed
+           (``SQ_INSTS_VALU_MFMA_MOPS_F16`` x 512, padding rows included) and the
+           L2 hit ratio (``TCC_HIT_sum`` / (``TCC_HIT_sum`` + ``TCC_MISS_sum``)) per
+           kernel, from counter runs of one workload.  Writes a Markdown table and
+           a JSON record (with the kernels' source hashes) that bench.py reports.
 
 Kernel names are folded to the ids of the library's timing API (e.g. both radix
 scatter variants are ``k_radix_scatter``), so per-dispatch figures line up with
@@ -34,7 +40,8 @@ SOURCES = {
     "k_backward": "map_kernels.hip", "k_forward_count": "map_kernels.hip", "k_forward_write": "map_kernels.hip",
     "k_fill": "map_kernels.hip", "k_scan": "scan.hip", "k_gather": "gmas_kernels.hip",
     "k_scatter": "gmas_kernels.hip", "k_concat": "gmas_kernels.hip", "k_gemm": "gemm_mfma.hip",
-    "k_transpose_w": "gemm_mfma.hip",
+    "k_transpose_w": "gemm_mfma.hip", "k_ts_from_pairs": "map_kernels.hip", "k_inverse_perm": "map_kernels.hip",
+    "k_hash_insert": "map_kernels.hip", "k_hash_count": "map_kernels.hip", "k_hash_items": "map_kernels.hip",
 }
 
 FOLD = [
@@ -147,6 +154,44 @@ def cmd_traffic(a) -> None:
     print("\n".join(lines))
 
 
+def cmd_counters(a) -> None:
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for path in a.csv:
+        for r in csv.DictReader(open(path)):
+            vals[fold(r["Kernel_Name"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    rec = {"workload": a.workload, "commands": a.command, "kernels": {}}
+    lines = [f"# {a.title}", "", "Counter runs (one rocprofv3 pass per counter group):", ""]
+    lines += [f"* `{c}`" for c in a.command]
+    lines += ["", "Per dispatch, over all dispatches of the runs.  MFMA utilisation is rocprofv3's derived",
+              "`MfmaUtil`; executed MFMA flops count every row the MFMAs process (padding and masked",
+              "rows included); L2 hit ratio = TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum).", "",
+              "| timing id | dispatches | MFMA util % | MFMA flops executed / dispatch | L2 hit % | L2 requests / dispatch |",
+              "|---|---|---|---|---|---|"]
+    for kid, d in sorted(vals.items()):
+        k = {"source_sha256": source_hash(kid)}
+        n = max(len(v) for v in d.values())
+        if d.get("MfmaUtil"):
+            k["mfma_util_pct"] = sum(d["MfmaUtil"]) / len(d["MfmaUtil"])
+        if d.get("SQ_INSTS_VALU_MFMA_MOPS_F16"):
+            k["mfma_flops_executed"] = 512.0 * sum(d["SQ_INSTS_VALU_MFMA_MOPS_F16"]) / len(d["SQ_INSTS_VALU_MFMA_MOPS_F16"])
+        if d.get("TCC_HIT_sum") and d.get("TCC_MISS_sum"):
+            hit, miss = sum(d["TCC_HIT_sum"]), sum(d["TCC_MISS_sum"])
+            if hit + miss > 0:
+                k["l2_hit_pct"] = 100.0 * hit / (hit + miss)
+                k["l2_requests_per_dispatch"] = (hit + miss) / len(d["TCC_HIT_sum"])
+        if len(k) == 1:
+            continue
+        rec["kernels"][kid] = k
+
+        def f(key, fmt):
+            return fmt.format(k[key]) if key in k else "-"
+        lines.append(f"| {kid} | {n} | {f('mfma_util_pct', '{:.1f}')} | {f('mfma_flops_executed', '{:.3e}')} | "
+                     f"{f('l2_hit_pct', '{:.1f}')} | {f('l2_requests_per_dispatch', '{:.3e}')} |")
+    with open(a.json, "w") as fh:
+        json.dump(rec, fh, indent=1, sort_keys=True)
+    print("\n".join(lines))
+
+
 def main(argv=None) -> None:
     p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     sub = p.add_subparsers(dest="cmd", required=True)
@@ -166,8 +211,14 @@ def main(argv=None) -> None:
     t.add_argument("--workload", required=True)
     t.add_argument("--title", required=True)
     t.add_argument("--json", required=True)
+    c = sub.add_parser("counters")
+    c.add_argument("csv", nargs="+")
+    c.add_argument("--command", action="append", required=True)
+    c.add_argument("--workload", required=True)
+    c.add_argument("--title", required=True)
+    c.add_argument("--json", required=True)
     a = p.parse_args(argv)
-    (cmd_stats if a.cmd == "stats" else cmd_traffic)(a)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "counters": cmd_counters}[a.cmd](a)
 
 
 if __name__ == "__main__":

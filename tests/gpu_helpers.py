@@ -61,5 +61,14 @@ def rel_err(y: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.abs(y - ref)) / den)
 
 
+def elem_err(y: np.ndarray, ref: np.ndarray) -> float:
+    """Element-wise statistic reported next to the gated normwise error (not gated):
+    max |y - ref| / (|ref| + rms(ref))."""
+    if not ref.size:
+        return 0.0
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    return float(np.max(np.abs(y - ref) / (np.abs(ref) + rms))) if rms > 0 else float(np.max(np.abs(y)))
+
+
 def features_f64(a: np.ndarray, dtype: str) -> np.ndarray:
     return scenes.to_f64(a, dtype)

@@ -18,7 +18,9 @@
  * Conventions shared by every entry point:
  *   - Pointers named d_* are DEVICE pointers, h_* HOST pointers.  The caller owns
  *     and allocates every buffer, including both workspaces; the library never
- *     allocates device memory.  `stream` is a hipStream_t (NULL = default stream).
+ *     allocates device memory (the one device array it holds, the workspace of
+ *     spconv_forward_noalloc, is set aside when the library is loaded).  `stream`
+ *     is a hipStream_t (NULL = default stream).
  *   - Coordinates are int32 [n][4] rows (b, x, y, z); b is the batch index and is
  *     never offset.  Input coordinates must be unique (the paper's point cloud is
  *     a set, Section 2.1).
@@ -198,6 +200,25 @@ int spconv_forward(const spconv_map* m, const void* d_x, const void* d_w, void* 
 int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in,
                       int c_out, int dtype, const void* d_residual, int relu,
                       const spconv_options* opt, void* d_workspace, size_t ws_bytes, void* stream);
+
+/* Maximum forward workspace of spconv_forward_noalloc (64 MiB). */
+#define SPCONV_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* spconv_forward_ex for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the forward
+ * workspace is a device array the library holds itself, one per GPU, of
+ * SPCONV_NOALLOC_SCRATCH_BYTES, set aside when the library is loaded and kept until
+ * the process ends.  The caller still owns d_x, d_w, d_y and d_residual (same
+ * meaning, layout and alignment rules as spconv_forward_ex).  A layer whose
+ * spconv_forward_workspace_bytes() exceeds the limit gets SPCONV_ENOSPC before any
+ * device work.  The call allocates nothing and does not synchronise; the first call
+ * on a device looks up that device's array address (a HIP symbol query).  Every
+ * call on one GPU shares that GPU's array and nothing in it needs clearing between
+ * calls, but calls whose work overlaps on one GPU (different streams, or several
+ * host threads without ordering) race on it: order them on one stream. */
+int spconv_forward_noalloc(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in,
+                           int c_out, int dtype, const void* d_residual, int relu, const spconv_options* opt,
+                           void* stream);
 
 /* Row-wise channel concatenation d_out[i] = [d_a[i] | d_b[i]] of [n][c_a] and
  * [n][c_b] in `dtype` (c * element size a multiple of 16 bytes); for the skip

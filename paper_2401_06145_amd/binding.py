@@ -28,7 +28,8 @@ EXPORTED = [
     "spconv_map_workspace_bytes", "spconv_build_map", "spconv_map_transpose", "spconv_map_n_in",
     "spconv_map_n_out", "spconv_map_kvol", "spconv_map_out_coords", "spconv_map_counts",
     "spconv_map_pairs", "spconv_map_copy_pairs", "spconv_map_copy_out_coords", "spconv_free_map",
-    "spconv_forward_workspace_bytes", "spconv_forward", "spconv_forward_ex", "spconv_concat_rows",
+    "spconv_forward_workspace_bytes", "spconv_forward", "spconv_forward_ex", "spconv_forward_noalloc",
+    "spconv_concat_rows",
     "spconv_forward_plan", "spconv_profile_enable", "spconv_profile_phase_count",
     "spconv_profile_phase_name", "spconv_profile_read", "spconv_last_error",
 ]
@@ -104,6 +105,8 @@ def lib() -> ctypes.CDLL:
     L.spconv_forward.restype = c_int
     L.spconv_forward_ex.argtypes = [vp, vp, vp, vp, c_int, c_int, c_int, vp, c_int, optp, vp, sz, vp]
     L.spconv_forward_ex.restype = c_int
+    L.spconv_forward_noalloc.argtypes = [vp, vp, vp, vp, c_int, c_int, c_int, vp, c_int, optp, vp]
+    L.spconv_forward_noalloc.restype = c_int
     L.spconv_concat_rows.argtypes = [vp, c_int, vp, c_int, vp, i64, c_int, vp]
     L.spconv_concat_rows.restype = c_int
     L.spconv_forward_plan.argtypes = [vp, c_int, c_int, c_int, optp, ctypes.POINTER(PlanInfo)]
@@ -203,6 +206,14 @@ def spconv_forward_ex(m, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, c_in
     st = lib().spconv_forward_ex(m, _ptr(x), _ptr(w), _ptr(y), c_in, c_out, dtype, _ptr(residual), 1 if relu else 0,
                                  _opt(opt), _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "spconv_forward_ex")
+
+
+def spconv_forward_noalloc(m, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, c_in: int, c_out: int,
+                           dtype: int, residual: torch.Tensor | None = None, relu: bool = False,
+                           opt: Options | None = None, stream=None) -> None:
+    st = lib().spconv_forward_noalloc(m, _ptr(x), _ptr(w), _ptr(y), c_in, c_out, dtype, _ptr(residual),
+                                      1 if relu else 0, _opt(opt), _stream(stream))
+    _check(st, "spconv_forward_noalloc")
 
 
 def spconv_concat_rows(a: torch.Tensor, b: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

@@ -863,9 +863,13 @@ int spconv_concat_rows(const void* d_a, int c_a, const void* d_b, int c_b, void*
   return SPCONV_OK;
 }
 
-int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in, int c_out,
-                      int dtype, const void* d_residual, int relu, const spconv_options* opt, void* d_workspace,
-                      size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int forward_impl(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in, int c_out, int dtype,
+                 const void* d_residual, int relu, const spconv_options* opt, void* d_workspace, size_t ws_bytes,
+                 void* stream) {
   GmasPlan p;
   int st = make_plan(m, c_in, c_out, dtype, opt, &p);
   if (st != SPCONV_OK) return st;
@@ -921,6 +925,59 @@ int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, voi
             "scatter");
   }
   return SPCONV_OK;
+}
+
+// Scratch of the allocation-free forward: device memory the library holds itself,
+// one copy per GPU for the whole process.  In host code `scratch` names a host-side
+// stand-in, so host code only ever uses the device address that hipGetSymbolAddress
+// returns for the current device, kept per device below.
+static __device__ __align__(256) unsigned char scratch[SPCONV_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_addr;  // by device ordinal; NULL until looked up
+
+// The current device's address of `scratch`, looked up on the first call on that
+// device (with it current) and kept.
+int scratch_address(void** out) {
+  int dev = 0;
+  SPC_TRY(hipGetDevice(&dev), "hipGetDevice");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (dev < 0) return fail(SPCONV_EHIP, "negative device ordinal");
+  if ((size_t)dev >= g_scratch_addr.size()) g_scratch_addr.resize((size_t)dev + 1, nullptr);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    SPC_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "scratch address");
+    if (!p) return fail(SPCONV_EHIP, "scratch address is NULL");
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return SPCONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int spconv_forward_ex(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in, int c_out,
+                      int dtype, const void* d_residual, int relu, const spconv_options* opt, void* d_workspace,
+                      size_t ws_bytes, void* stream) {
+  return forward_impl(m, d_x, d_w, d_y, c_in, c_out, dtype, d_residual, relu, opt, d_workspace, ws_bytes, stream);
+}
+
+int spconv_forward_noalloc(const spconv_map* m, const void* d_x, const void* d_w, void* d_y, int c_in, int c_out,
+                           int dtype, const void* d_residual, int relu, const spconv_options* opt, void* stream) {
+  GmasPlan p;
+  int st = make_plan(m, c_in, c_out, dtype, opt, &p);
+  if (st != SPCONV_OK) return st;
+  FwdBufs b;
+  const size_t need = plan_forward_ws(nullptr, m, c_in, c_out, p, &b);
+  if (need > (size_t)SPCONV_NOALLOC_SCRATCH_BYTES)
+    return fail(SPCONV_ENOSPC, "layer needs " + std::to_string(need) + " bytes of forward workspace; the "
+                "allocation-free forward holds " + std::to_string((size_t)SPCONV_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws)) != SPCONV_OK) return st;
+  return forward_impl(m, d_x, d_w, d_y, c_in, c_out, dtype, d_residual, relu, opt, ws,
+                      (size_t)SPCONV_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 // --------------------------------------------------------------- measurement

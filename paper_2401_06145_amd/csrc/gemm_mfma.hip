@@ -167,6 +167,12 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmLaunchArgs g, const T* __
 constexpr int kWideThreads = 512;
 constexpr int kWideWaves = kWideThreads / kWave;
 constexpr size_t kLdsMax = 160 * 1024;
+// Per-wave LDS stage of the partial stores: 16 rows of one segment of at most 128
+// bytes, each row padded by 16 bytes.
+constexpr int kStageRow = 128 + 16;
+constexpr size_t kStageBytes = (size_t)kWideWaves * 16 * kStageRow;
+// LDS of one full-width workgroup: the W_k^T slice plus the store stages.
+constexpr size_t wide_lds(int nt, int ldk) { return (size_t)16 * nt * ldk * 2 + kStageBytes; }
 
 // Register blocking of the full-width kernel.  A wave computes MB 16-row blocks
 // times NTW 16-column tiles, so every W^T fragment it reads from LDS feeds MB
@@ -179,15 +185,16 @@ constexpr size_t kLdsMax = 160 * 1024;
 // flight need 160 registers and the kernel spills).  The columns of a two-block
 // wave are produced in NCH chunks of at most 8 tiles, so that operands,
 // accumulators and fragments stay within the 256 registers a wave has at two
-// waves per SIMD.  Measured on gfx950: C = 128 GEMM 0.142 -> 0.132 ms; at C = 64
+// waves per SIMD (and at 385 to 512 input channels in chunks of two tiles, as the
+// operands alone take 128 registers there).  Measured on gfx950: C = 128 GEMM 0.142 -> 0.132 ms; at C = 64
 // one block per wave is faster (26.5 vs 28.5 us on the 120k LiDAR layer), at
 // C = 32 the two are equal; one block per wave stays faster in one chunk; CG > 1
 // cost more occupancy than it saved.
 constexpr int wide_cg(int) { return 1; }
 constexpr int wide_mb(int, int ksteps) { return (ksteps == 3 || ksteps == 4) ? 2 : 1; }
-constexpr int wide_nch(int ntw, int mb) {
+constexpr int wide_nch(int ntw, int mb, int ksteps) {
   int nch = 1;
-  while (mb > 1 && ntw / nch > 8 && ntw % (2 * nch) == 0) nch *= 2;
+  while ((mb > 1 || ksteps >= 16) && ntw / nch > (mb > 1 ? 8 : 2) && ntw % (2 * nch) == 0) nch *= 2;
   return nch;
 }
 
@@ -212,7 +219,7 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   constexpr int CG = wide_cg(NT);
   constexpr int NTW = NT / CG;
   constexpr int MB = wide_mb(NTW, KSTEPS);
-  constexpr int NCH = wide_nch(NTW, MB);
+  constexpr int NCH = wide_nch(NTW, MB, KSTEPS);
   constexpr int NTC = NTW / NCH;  // column tiles per chunk
   static_assert(NTW % NCH == 0, "chunks must split the tiles");
   constexpr int RG = kWideWaves / CG;   // row groups
@@ -242,6 +249,15 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   const int col = lane & 15;
   const int nw = 16 * NTW * cg;  // this wave's first column within the slice
   const T* lwp = lw + (nw + col) * ldk + 8 * sub;
+  // store stage: GC tiles per segment (128 bytes, or fewer tiles when the chunk's
+  // tile count is not a multiple), SLANES lanes of 16 bytes per row, SROWS rows
+  // per read, SREADS reads for the 16 rows
+  unsigned char* stg = smem + (size_t)BN * ldk * sizeof(T) + (size_t)wave * 16 * kStageRow;
+  constexpr int GC0 = 128 / (16 * (int)sizeof(TO));
+  constexpr int GC = (NTC % GC0 == 0) ? GC0 : ((NTC % 2 == 0 && GC0 >= 2) ? 2 : 1);
+  constexpr int SLANES = GC * 16 * (int)sizeof(TO) / 16;
+  constexpr int SROWS = kWave / SLANES;
+  constexpr int SREADS = (16 + SROWS - 1) / SROWS;
   const int row_lim = min(rows, r_end);  // rows of this tile that hold data
   // raw: the next blocks as loaded (dummy data where masked); cur: the blocks in use
   F raw[MB][KSTEPS], cur[MB][KSTEPS];
@@ -388,14 +404,35 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
 #pragma unroll
           for (int b = 0; b < MB; ++b) acc[b][t] = M::mma(wf[t], cur[b][q], acc[b][t]);
       }
-      // lanes without a row store into the dump row instead of branching, so the
-      // store count is fixed and the wait for the next blocks below skips the stores
+      // The partials leave through this wave's LDS stage: a lane holds 4 channels
+      // of one row per tile (16 rows x 8 or 16 bytes per tile and store), and
+      // stored straight the 16 rows would take 16 partial-line writes per store.
+      // Staged, each store writes whole row segments of GC tiles (up to 128 bytes).
+      // Lanes without a row store into the dump row instead of branching, so the
+      // store count is fixed and the wait for the next blocks below skips the stores.
 #pragma unroll
       for (int b = 0; b < MB; ++b) {
-        const int row = m0 + 16 * b + col;
-        TO* crow = (row < row_lim ? C + (row0 + row) * (int64_t)c_out : dump) + n0 + nw + 4 * sub;
 #pragma unroll
-        for (int t = 0; t < NTC; ++t) store4(crow + 16 * (ch * NTC + t), acc[b][t]);
+        for (int t0 = 0; t0 < NTC; t0 += GC) {
+#pragma unroll
+          for (int u = 0; u < GC; ++u)
+            store4(reinterpret_cast<TO*>(stg + col * kStageRow) + 16 * u + 4 * sub, acc[b][t0 + u]);
+          // the stage is written and read through different types: keep the compiler
+          // from moving the reads above these writes, or the next segment's writes
+          // above these reads (the LDS itself serves one wave's accesses in order)
+          asm volatile("" ::: "memory");
+#pragma unroll
+          for (int h = 0; h < SREADS; ++h) {
+            const int rr = lane / SLANES + SROWS * h;
+            const int row = m0 + 16 * b + rr;
+            // (with two lanes per row, rows 16..31 of the read repeat row 15 and are not stored)
+            const uint4 v = *reinterpret_cast<const uint4*>(stg + (rr < 16 ? rr : 15) * kStageRow + (lane % SLANES) * 16);
+            TO* dst = (row < row_lim ? C + (row0 + row) * (int64_t)c_out : dump) + n0 + nw +
+                      16 * (ch * NTC + t0) + (lane % SLANES) * (16 / (int)sizeof(TO));
+            if (rr < 16) *reinterpret_cast<uint4*>(dst) = v;
+          }
+          asm volatile("" ::: "memory");
+        }
       }
     }
     take(m1);
@@ -418,7 +455,7 @@ int wide_ksteps(int c_in) {
 }
 
 // Instantiated (NT, KSTEPS) pairs: the W^T slice fits the LDS.
-constexpr bool wide_fits(int nt, int ks) { return (size_t)16 * nt * (32 * ks + 8) * 2 <= kLdsMax; }
+constexpr bool wide_fits(int nt, int ks) { return wide_lds(nt, 32 * ks + 8) <= kLdsMax; }
 
 // Column tiles per workgroup for the wide kernel: the widest instantiated divisor
 // of c_out / 16 whose W^T slice fits the LDS; 0 if the wide kernel does not apply.
@@ -429,7 +466,7 @@ int wide_nt(int c_in, int c_out, int elem) {
   const int ldk = 32 * ks + 8;
   const int nt_all = c_out / 16;
   for (int nt : {16, 12, 8, 6, 4, 3, 2, 1})
-    if (nt_all % nt == 0 && (size_t)16 * nt * ldk * 2 <= kLdsMax) return nt;
+    if (nt_all % nt == 0 && wide_lds(nt, ldk) <= kLdsMax) return nt;
   return 0;
 }
 
@@ -593,7 +630,7 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
     nt = wide_nt(c_in, c_out, 2);
     ks = wide_ksteps(c_in);
     ldk = 32 * ks + 8;
-    lds = (size_t)16 * nt * ldk * 2;
+    lds = wide_lds(nt, ldk);
     wfn = wide_kernel_for(dtype, part_dtype, a_rows != nullptr, nt, ks);
     if (!wfn) return hipErrorInvalidValue;
     int per_cu = 0, cus = 0;

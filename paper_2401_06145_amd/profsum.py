@@ -170,10 +170,11 @@ def cmd_counters(a) -> None:
     for kid, d in sorted(vals.items()):
         k = {"source_sha256": source_hash(kid)}
         n = max(len(v) for v in d.values())
-        if d.get("MfmaUtil"):
-            k["mfma_util_pct"] = sum(d["MfmaUtil"]) / len(d["MfmaUtil"])
-        if d.get("SQ_INSTS_VALU_MFMA_MOPS_F16"):
+        # MFMA figures only for kernels that run MFMAs
+        if d.get("SQ_INSTS_VALU_MFMA_MOPS_F16") and sum(d["SQ_INSTS_VALU_MFMA_MOPS_F16"]) > 0:
             k["mfma_flops_executed"] = 512.0 * sum(d["SQ_INSTS_VALU_MFMA_MOPS_F16"]) / len(d["SQ_INSTS_VALU_MFMA_MOPS_F16"])
+            if d.get("MfmaUtil"):
+                k["mfma_util_pct"] = sum(d["MfmaUtil"]) / len(d["MfmaUtil"])
         if d.get("TCC_HIT_sum") and d.get("TCC_MISS_sum"):
             hit, miss = sum(d["TCC_HIT_sum"]), sum(d["TCC_MISS_sum"])
             if hit + miss > 0:

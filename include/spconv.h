@@ -138,7 +138,12 @@ size_t spconv_map_workspace_bytes(int64_t n_in, int64_t n_out, int K, int mode,
  * digit-by-digit sort's passes before the layout is known (from the previous build
  * of the same inputs); a key wider than planned is detected and the build redone.
  * Both choices are kept per input, so only a first build can cost two passes
- * over the Map.
+ * over the Map.  An input is recognised by its device address, sizes and layer
+ * arguments (the host never reads the coordinates): a different cloud later
+ * placed at the same address (a caching allocator reuses addresses) inherits the
+ * plan; a plan too short for it is detected and costs one redo, a longer one
+ * runs its extra digit passes as copies.  While it waits for the counts the
+ * calling thread spins for at most 2 ms, then blocks on the stream.
  * On success *out_map owns a host object to release with spconv_free_map(). */
 int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_out_coords,
                      int64_t n_out, int K, int stride, int tensor_stride, int mode,

@@ -371,11 +371,11 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
   if (c_in < 1 || c_out < 1 || c_in > 1024 || c_out > 1024) return fail(SPCONV_EUNSUPPORTED, "channels must be in [1, 1024]");
   if ((c_in * p->elem) % 16 != 0) return fail(SPCONV_EUNSUPPORTED, "c_in rows must be whole 16-byte vectors");
   if (c_out % 16 != 0) return fail(SPCONV_EUNSUPPORTED, "c_out must be a multiple of 16");
-  // GEMM partials: 1 = float32, 2 = the layer dtype; default float32 for f32 layers and
-  // the layer dtype otherwise (the scatter still sums them in float32)
+  // GEMM partials: 1 = float32, 2 = the layer dtype; default the layer dtype (the
+  // scatter sums them in float32 either way)
   const int pd = opt ? opt->partial_dtype : 0;
   if (pd < 0 || pd > 2) return fail(SPCONV_EINVAL, "partial_dtype must be 0, 1 or 2");
-  p->part_dtype = (pd == 1) ? SPCONV_F32 : (pd == 2 ? dtype : dtype);
+  p->part_dtype = (pd == 1) ? SPCONV_F32 : dtype;
   p->pelem = elem_bytes(p->part_dtype);
   // tiles: default one 16-byte vector per thread for gather and for the partial reads of scatter
   p->t_gather = (opt && opt->t_gather) ? opt->t_gather : 16 / p->elem;
@@ -480,7 +480,9 @@ namespace {
 // computed on the device, so the host never waits for the bounds): the count the
 // same inputs needed last time, else the last count needed on this thread (start:
 // 4 passes, a 32-bit key).  A build whose key turns out wider is redone with the
-// passes it needs.
+// passes it needs.  Inputs are told apart by address, sizes and layer arguments
+// only, so a new cloud at a reused address inherits a plan; a wrong plan costs at
+// most that redo (or, planned too long, digit passes that copy).
 // Sort plan of a map build, kept per input from the previous build of it: the
 // digit passes of the digit-by-digit sort, and whether the small sorts may go by
 // bucket (no bucket of the previous build was too large for one workgroup).

@@ -176,16 +176,15 @@ struct SearchArgs {
   int64_t res_stride;
   // Per-(offset, source) table T_s [K3][ts_stride], indexed by sorted source
   // position: pair index or -1.  The write pass stores the matches; the -1
-  // entries come from a fill before it, or (sym != 0) from the write pass itself.
+  // entries come from a fill before it.
   int32_t* ts;
   int64_t ts_stride;
   int64_t pair_cap;       // capacity of the pair lists (K3 * queries)
-  // Submanifold map with odd K: query q misses offset k exactly when source q
-  // has no partner at the mirrored offset K^3 - 1 - k, so the write pass marks
-  // that T_s entry instead of a separate fill.
+  // Submanifold map with odd K (offset k and K^3 - 1 - k are mirror images).
   int sym;
   // 0: the write pass leaves T_s alone (a symmetric map's T_s is filled from the
-  // pair lists when a table-driven gather first needs it)
+  // pair lists when a table-driven gather first needs it); else it stores T_s's
+  // matches after a -1 fill.
   int write_ts;
   // Mapped, coherent host buffer (or NULL).  The write pass's first workgroup
   // copies the control block's head (kControlHeadBytes) into it, then stores

@@ -498,6 +498,8 @@ const void* wide_kernel_for(int dtype, int part_dtype, bool gather, int nt, int 
   if (dtype == 2 && part_dtype == 2)
     return gather ? wide_kernel<__hip_bfloat16, __hip_bfloat16, true>(nt, ks)
                   : wide_kernel<__hip_bfloat16, __hip_bfloat16, false>(nt, ks);
+  if (dtype == 2 && part_dtype == 0)
+    return gather ? wide_kernel<__hip_bfloat16, float, true>(nt, ks) : wide_kernel<__hip_bfloat16, float, false>(nt, ks);
   return nullptr;
 }
 
@@ -527,12 +529,13 @@ hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const
   const int KS = Mfma<T>::KS;
   const int kp = (c_in + KS - 1) / KS * KS;
   const int ldk = kp + 16 / (int)sizeof(T);
-  // widest column slice whose W^T tile fits 64 KiB of LDS
+  // widest column slice whose W^T tile fits 64 KiB of LDS (a single 16-column tile
+  // may take up to the 160 KiB of the CU: f32 at 1024 input channels needs 65.8 KB)
   const int nt_all = c_out / 16;
   int nt = 0;
   const int cand[] = {8, 6, 4, 3, 2, 1};
   for (int c : cand)
-    if (nt_all % c == 0 && (size_t)16 * c * ldk * sizeof(T) <= 65536) {
+    if (nt_all % c == 0 && (size_t)16 * c * ldk * sizeof(T) <= (c == 1 ? kLdsMax : 65536)) {
       nt = c;
       break;
     }
@@ -567,8 +570,8 @@ hipError_t gemm_t(const GemmLaunchArgs& g, int total_tiles, const void* A, const
 bool gemm_wide_transposed(int c_in, int c_out) { return c_in * c_out >= 128 * 128; }
 
 bool gemm_wide(int c_in, int c_out, int dtype, int part_dtype) {
-  // built for 16-bit operands with partials of the same type, and f16 with f32 partials
-  const bool pair = part_dtype == dtype || (dtype == 1 && part_dtype == 0);
+  // built for 16-bit operands with partials of the same type or of float32
+  const bool pair = part_dtype == dtype || part_dtype == 0;
   return dtype != 0 && pair && wide_nt(c_in, c_out, 2) > 0;
 }
 

@@ -4,8 +4,9 @@
 //
 // MI355X notes: atomics on one address from many workgroups serialise across the
 // eight XCDs, so no kernel here has such a hot spot: reductions go through
-// per-block partials, and the match compaction is count -> scan -> write
-// (re-running the cheap LDS search) instead of a single pass with a look-back.
+// per-block partials, and the match compaction is count -> scan -> write (the
+// count pass leaves each query's search result in the query-side table, which
+// the write pass reads back) instead of a single pass with a look-back.
 #include <algorithm>
 #include <climits>
 
@@ -1099,8 +1100,6 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
 
   int32_t* res = a.res + (int64_t)k * a.res_stride;
   int32_t* ts = a.ts + (int64_t)k * a.ts_stride;
-  // mirrored offset's T_s row, for the misses of a symmetric map
-  int32_t* ts_mirror = a.ts + (int64_t)(a.K3 - 1 - k) * a.ts_stride;
   uint64_t base = base0;
   for (int64_t q0 = q_lo; q0 < q_hi; q0 += a.Cq) {  // workgroup-uniform
     const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
@@ -1123,13 +1122,6 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
       r_out[r] = a.swap_roles ? src : qry;
       bal[r] = __ballot(hit);
       if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal[r]);
-    }
-    if (a.sym && a.write_ts) {
-#pragma unroll
-      for (int r = 0; r < ROUNDS; ++r) {
-        const int64_t qp = q0 + (int64_t)r * kThreads + tid;
-        if (qp < q1 && sp[r] < 0) ts_mirror[qp] = -1;
-      }
     }
     __syncthreads();
     uint32_t total = 0;

@@ -502,6 +502,44 @@ def test_bf16_layer():
     assert rel_err(to_f64(y), ref) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("K,c", [(5, 64), (3, 256)])
+def test_bf16_partial_precision(K, c):
+    """bf16 layers sum per-offset GEMM partials in float32, the partials themselves
+    stored in bf16 (the default) or float32.  With float32 partials the only error
+    left is the output's rounding to bf16, at most 2^-8 of max|y| normwise (8
+    significant bits); the default adds one bf16 rounding per offset and must meet
+    the tolerance.  Both errors are printed."""
+    say(f"bf16 partial precision K={K} C={c}")
+    cl = _cloud(41 + K, 6000, -12, 12)
+    x = scenes.features(len(cl), c, "bf16", 15)
+    w = scenes.weights(K, c, c, "bf16", 16)
+    okm = oracle.kernel_map(cl, None, K, 1, "subm")
+    ref = oracle.features(scenes.to_f64(x, "bf16"), scenes.to_f64(w, "bf16"), okm)
+    km = B.KernelMap.build(to_dev(cl), K)
+    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    y32 = B.Forward(km, c, c, torch.bfloat16, B.Options.make(partial_dtype=1))(xd, wd)
+    y16 = B.Forward(km, c, c, torch.bfloat16)(xd, wd)
+    torch.cuda.synchronize()
+    assert_map_equal(km, okm)
+    e32, e16 = rel_err(to_f64(y32), ref), rel_err(to_f64(y16), ref)
+    print(f"bf16 K={K} C={c}: normwise error with float32 partials {e32:.2e}, with bf16 partials {e16:.2e}",
+          flush=True)
+    assert e32 <= 2.0 ** -8 * 1.01
+    assert e16 <= TOL["bf16"]
+
+
+def test_f32_widest_input():
+    """f32 at the widest input the boundary takes (1024 channels): the general
+    GEMM holds one 16-column tile of W_k^T (65.8 KB) in LDS."""
+    say("f32 c_in = 1024")
+    cl = _cloud(44, 1500, -7, 7)
+    x = scenes.features(len(cl), 1024, "f32", 17)
+    w = scenes.weights(3, 1024, 16, "f32", 18)
+    km, y = _conv_gpu(cl, x, w, 3)
+    okm = oracle.kernel_map(cl, None, 3, 1, "subm")
+    assert rel_err(to_f64(y), oracle.features(x, w, okm)) <= TOL["f32"]
+
+
 # ----------------------------------------------------------------------------
 # Edge cases and error paths
 # ----------------------------------------------------------------------------

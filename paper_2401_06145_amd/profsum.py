@@ -106,6 +106,17 @@ def cmd_stats(a) -> None:
     print("\n".join(out))
 
 
+def robust_mean(vals: list[float]) -> float:
+    """Mean over dispatches, leaving out readings above 4x the median: the first
+    dispatch of a kernel in a counter run has read tens to millions of times its
+    steady value (a cold first build, or a wrapped-around counter), while the
+    dispatches of one kernel in a run otherwise differ by well under 2x."""
+    s = sorted(vals)
+    med = s[len(s) // 2]
+    keep = [v for v in vals if med <= 0 or v <= 4 * med]
+    return sum(keep) / len(keep)
+
+
 def _counter(path: str, counter: str) -> dict[str, list[float]]:
     per = collections.defaultdict(list)
     for r in csv.DictReader(open(path)):
@@ -117,8 +128,8 @@ def _counter(path: str, counter: str) -> dict[str, list[float]]:
 def _copy_scale(path: str, counter: str, true_bytes: float) -> float:
     per = _counter(path, counter)
     # the copy's dispatches are the ones with the most traffic
-    name = max(per, key=lambda k: sum(per[k]) / len(per[k]))
-    kib = sum(per[name]) / len(per[name])
+    name = max(per, key=lambda k: robust_mean(per[k]))
+    kib = robust_mean(per[name])
     return true_bytes / (kib * 1024.0)
 
 
@@ -139,13 +150,14 @@ def cmd_traffic(a) -> None:
     lines = [f"# {a.title}", "", f"Counter runs: `{a.command_fetch}` and `{a.command_write}`;",
              f"calibration: the same two counters over a plain {a.copy_mib} MiB device copy "
              f"(`{a.command_copy}`), giving scale factors FETCH x{fs:.3f}, WRITE x{ws:.3f}.", "",
-             "Bytes per dispatch (mean over the run's dispatches), after scaling.", "",
+             "Bytes per dispatch (mean over the run's dispatches, readings above 4x the median left out),",
+             "after scaling.", "",
              "| timing id | dispatches | HBM read MB | HBM write MB | total MB |", "|---|---|---|---|---|"]
     for kid, d in sorted(agg.items(), key=lambda t: -(sum(t[1]["fetch"]) + sum(t[1]["write"]))):
         if not d["fetch"] or not d["write"]:
             continue
-        fb = sum(d["fetch"]) / len(d["fetch"]) * 1024 * fs
-        wb = sum(d["write"]) / len(d["write"]) * 1024 * ws
+        fb = robust_mean(d["fetch"]) * 1024 * fs
+        wb = robust_mean(d["write"]) * 1024 * ws
         rec["kernels"][kid] = {"dispatches": len(d["fetch"]), "fetch_bytes": fb, "write_bytes": wb,
                                "source_sha256": source_hash(kid)}
         lines.append(f"| {kid} | {len(d['fetch'])} | {fb / 1e6:.3f} | {wb / 1e6:.3f} | {(fb + wb) / 1e6:.3f} |")
@@ -162,7 +174,8 @@ def cmd_counters(a) -> None:
     rec = {"workload": a.workload, "commands": a.command, "kernels": {}}
     lines = [f"# {a.title}", "", "Counter runs (one rocprofv3 pass per counter group):", ""]
     lines += [f"* `{c}`" for c in a.command]
-    lines += ["", "Per dispatch, over all dispatches of the runs.  MFMA utilisation is rocprofv3's derived",
+    lines += ["", "Per dispatch, mean over the runs' dispatches (readings above 4x the median left out).",
+              "MFMA utilisation is rocprofv3's derived",
               "`MfmaUtil`; executed MFMA flops count every row the MFMAs process (padding and masked",
               "rows included); L2 hit ratio = TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum).", "",
               "| timing id | dispatches | MFMA util % | MFMA flops executed / dispatch | L2 hit % | L2 requests / dispatch |",
@@ -172,14 +185,14 @@ def cmd_counters(a) -> None:
         n = max(len(v) for v in d.values())
         # MFMA figures only for kernels that run MFMAs
         if d.get("SQ_INSTS_VALU_MFMA_MOPS_F16") and sum(d["SQ_INSTS_VALU_MFMA_MOPS_F16"]) > 0:
-            k["mfma_flops_executed"] = 512.0 * sum(d["SQ_INSTS_VALU_MFMA_MOPS_F16"]) / len(d["SQ_INSTS_VALU_MFMA_MOPS_F16"])
+            k["mfma_flops_executed"] = 512.0 * robust_mean(d["SQ_INSTS_VALU_MFMA_MOPS_F16"])
             if d.get("MfmaUtil"):
-                k["mfma_util_pct"] = sum(d["MfmaUtil"]) / len(d["MfmaUtil"])
+                k["mfma_util_pct"] = robust_mean(d["MfmaUtil"])
         if d.get("TCC_HIT_sum") and d.get("TCC_MISS_sum"):
-            hit, miss = sum(d["TCC_HIT_sum"]), sum(d["TCC_MISS_sum"])
+            hit, miss = robust_mean(d["TCC_HIT_sum"]), robust_mean(d["TCC_MISS_sum"])
             if hit + miss > 0:
                 k["l2_hit_pct"] = 100.0 * hit / (hit + miss)
-                k["l2_requests_per_dispatch"] = (hit + miss) / len(d["TCC_HIT_sum"])
+                k["l2_requests_per_dispatch"] = hit + miss
         if len(k) == 1:
             continue
         rec["kernels"][kid] = k

@@ -5,9 +5,16 @@ with 10^4 .. 10^6 points) to 16M voxels, to show where the Map kernels leave the
 latency-bound regime.  For each size it builds the submanifold K = 3 map
 (bounds, sort, backward search, balance, forward search, compaction) and reports
 phase times from HIP events, the compulsory Map bytes per second, and each main
-kernel's algorithmic bytes over its own event time.
+kernel's algorithmic bytes over its own event time.  Two scenes: uniform random
+cells (the paper's Random set), and batches of LiDAR-like frames (~120k voxels
+each, the outdoor recipe) up to the same sizes.
 
-    python -m paper_2401_06145_amd.scaling --sizes 10000 100000 1000000 4000000 16000000
+    python -m paper_2401_06145_amd.scaling --scene uniform --sizes 10000 100000 1000000 4000000 16000000
+    python -m paper_2401_06145_amd.scaling --scene lidar --search sorted --sizes 1000000 4000000 16000000
+
+``summarize`` turns the JSON rows (and rocprofv3 counter records of single-size
+runs, made by profsum's ``counters`` and ``traffic`` summaries) into a Markdown
+table.
 """
 from __future__ import annotations
 
@@ -26,9 +33,16 @@ from paper_2401_06145_amd import scenes  # noqa: E402
 HBM_PEAK_GBS = 8000.0
 
 
-def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = False):
+def cloud(scene: str, n: int, side: int):
+    if scene == "lidar":
+        return scenes.lidar_batch(n, 7000)
+    return scenes.uniform_cells_large(n, side, 5000 + n % 997) if n > 1_000_000 else scenes.uniform_cells(n, side, 5000)
+
+
+def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = False, scene: str = "uniform"):
     dev = torch.device("cuda:0")
-    c = scenes.uniform_cells_large(n, side, 5000 + n % 997) if n > 1_000_000 else scenes.uniform_cells(n, side, 5000)
+    c = cloud(scene, n, side)
+    n = len(c)
     coords = torch.from_numpy(c).to(dev)
     opt = B.Options.make(search=1) if hash_search else None
     ws = torch.empty(B.spconv_map_workspace_bytes(n, 0, K, B.SPCONV_SUBM, opt), dtype=torch.uint8, device=dev)
@@ -77,7 +91,8 @@ def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = Fals
         # table to the first table-driven gather)
         "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 12 * pairs,
     }
-    row = {"voxels": n, "grid": side, "search": "hash" if hash_search else "sorted", "pairs": pairs,
+    row = {"scene": scene, "voxels": n, "grid": side if scene == "uniform" else None,
+           "search": "hash" if hash_search else "sorted", "pairs": pairs,
            "map_ms": round(map_ms, 4),
            "phases_ms": {k: round(v, 4) for k, v in phases.items()},
            "map_gbps_compulsory": round(map_bytes / (map_ms * 1e-3) / 1e9, 1),
@@ -99,13 +114,58 @@ def main(argv=None):
     p.add_argument("--rounds", type=int, default=10)
     p.add_argument("--search", choices=["sorted", "hash", "both"], default="both",
                    help="sorted-array search (the method), hash-table search (ablation), or both")
+    p.add_argument("--scene", choices=["uniform", "lidar"], default="uniform")
     a = p.parse_args(argv)
     if not torch.cuda.is_available():
         raise SystemExit("the sweep needs a GPU")
     for n in a.sizes:
         side = 400 if n <= 1_000_000 else 800
         for hs in ((False, True) if a.search == "both" else ((a.search == "hash"),)):
-            print(json.dumps(measure(n, side, a.rounds, hash_search=hs)), flush=True)
+            print(json.dumps(measure(n, side, a.rounds, hash_search=hs, scene=a.scene)), flush=True)
+
+
+def summarize(rows_jsonl, counters, title, command, out=sys.stdout):
+    """Markdown table of sorted-search rows (JSON lines) with, per size, the L2 hit
+    ratio and measured HBM bytes of the Map kernels from counter records.
+
+    counters: list of (voxels, counters_json_path, traffic_json_path)."""
+    allrows = [json.loads(x) for x in open(rows_jsonl) if x.strip().startswith("{")]
+    rows = [r for r in allrows if r["search"] == "sorted"]
+    hashed = {r["voxels"]: r for r in allrows if r["search"] == "hash"}
+    ctr = {}
+    for v, cp, tp in counters:
+        c = json.load(open(cp))["kernels"] if cp else {}
+        t = json.load(open(tp))["kernels"] if tp else {}
+        ctr[int(v)] = (c, t)
+    kern = ("k_radix_scatter", "k_forward_count", "k_forward_write", "k_backward")
+    lines = [f"# {title}", "", f"Command: `{command}`", "",
+             "Map = bounds, sort, backward search, forward count, match scan and write pass (cold, with sort).",
+             "GB/s columns: algorithmic bytes per launch over the kernel's mean event time; Map GB/s counts the",
+             "compulsory bytes (28 B/voxel sort, 8|Q| + 12|P| + 8M search).  L2 hit % and measured MB/launch come",
+             "from single-size rocprofv3 runs (TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum); FETCH_SIZE + WRITE_SIZE",
+             "scaled by a 256 MiB copy), where taken.", "",
+             "The hash-table search (the ablation: `spconv_options.search = 1`) builds the same map on the same",
+             "cloud; its Map time and its ratio to the sorted search are the last two columns.", "",
+             "| voxels | pairs | map ms | sort ms | forward ms | Map GB/s | radix pass GB/s | count GB/s | write GB/s |"
+             " L2 hit % (radix / count / write / backward) | measured MB/launch (radix / count / write) |"
+             " hash: map ms | hash / sorted |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        ph = r["phases_ms"]
+        k = r["kernels"]
+        c, t = ctr.get(r["voxels"], ({}, {}))
+        hit = " / ".join(f"{c[x]['l2_hit_pct']:.1f}" if x in c and "l2_hit_pct" in c[x] else "-" for x in kern)
+        mb = " / ".join(f"{(t[x]['fetch_bytes'] + t[x]['write_bytes']) / 1e6:.1f}" if x in t else "-"
+                        for x in kern[:3])
+
+        def g(name):
+            return f"{k[name]['gbps']:.0f}" if name in k and "gbps" in k[name] else "-"
+        lines.append(f"| {r['voxels']:,} | {r['pairs']:,} | {r['map_ms']:.4f} | {ph.get('sort', 0):.4f} | "
+                     f"{ph.get('forward', 0):.4f} | {r['map_gbps_compulsory']:.1f} | {g('k_radix_scatter')} | "
+                     f"{g('k_forward_count')} | {g('k_forward_write')} | {hit if c else '-'} | {mb if t else '-'} | "
+                     + (f"{hashed[r['voxels']]['map_ms']:.4f} | {hashed[r['voxels']]['map_ms'] / r['map_ms']:.2f}x |"
+                        if r["voxels"] in hashed else "- | - |"))
+    print("\n".join(lines), file=out)
 
 
 if __name__ == "__main__":

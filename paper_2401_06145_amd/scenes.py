@@ -220,6 +220,23 @@ def lidar_scene(seed: int, budget: int = LIDAR_BUDGET_120K, batch: int = 0) -> n
     return _finish(v, np.random.default_rng(seed + 7919))
 
 
+def lidar_batch(n_target: int, seed: int, distinct: int = 8) -> np.ndarray:
+    """A batch of LiDAR-like frames of about ``n_target`` voxels in all: whole frames
+    of ~120k voxels, frame f at batch index f.  The first ``distinct`` frames have
+    their own geometry (seeds seed + f); later frames repeat those geometries under
+    new batch indices.  Rows in a seeded random order."""
+    frames = max(1, -(-n_target // 120_357))
+    geo = [lidar_scene(seed + f, LIDAR_BUDGET_120K, batch=0) for f in range(min(frames, distinct))]
+    parts = []
+    for f in range(frames):
+        g = geo[f % len(geo)].copy()
+        g[:, 0] = f
+        parts.append(g)
+    c = np.concatenate(parts, axis=0)
+    rng = np.random.default_rng(seed + 104729)
+    return np.ascontiguousarray(c[rng.permutation(c.shape[0])])
+
+
 # ----------------------------------------------------------------------------
 # Indoor-like room
 # ----------------------------------------------------------------------------

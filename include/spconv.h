@@ -80,8 +80,10 @@ typedef enum {
  * limit); the GMaS fields are the Gather / Scatter tile sizes of Algorithm 1
  * (channels per thread) and the GEMM grouping of Section 5.2.2. */
 typedef struct {
-  int B;             /* source block size, power of two in [64, 4096]; default 1024 */
-  int Cq;            /* query block limit (the paper's C): 256, 512, 1024 or 2048; default 1024 */
+  int B;             /* source block size, power of two in [64, 4096] */
+  int Cq;            /* query block limit (the paper's C): 256, 512, 1024 or 2048.  B, Cq and wg
+                        all 0: 1024, 1024 and 256 below 2^18 source points, 4096, 2048 and 512
+                        from there on; any of them given: the others default to 1024 / 1024 / 256 */
   int t_gather;      /* gather tile T in channels; must divide c_in; default: tuned rule */
   int t_scatter;     /* scatter tile T in channels; must divide c_out; default: tuned rule */
   int grouping;      /* spconv_grouping + 1 (0 = default SPCONV_GROUP_RAGGED) */
@@ -100,7 +102,13 @@ typedef struct {
                         per-pair buffer that the GEMMs read; SPCONV_GATHER_FUSED = the GEMMs load
                         each pair's input row directly (no buffer); 0 = default (fused).  Results
                         are bit-identical */
-  int reserved[6];
+  int wg;            /* spconv_build_map: threads per workgroup of the forward search's count and
+                        write passes (Section 5.1.4's thread-block size): 128, 256 or 512, and
+                        Cq / wg must be 1, 2, 4 or 8 */
+  int gemm_tile_rows; /* spconv_forward: output rows per GEMM workgroup tile, rounded up to the
+                        kernel's rows per round (16 to 128); default 0 = about two tiles per
+                        workgroup slot of the GPU */
+  int reserved[4];
 } spconv_options;
 
 typedef struct spconv_map spconv_map; /* opaque host-side object */

@@ -45,7 +45,8 @@ class Options(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int), ("Cq", ctypes.c_int), ("t_gather", ctypes.c_int),
                 ("t_scatter", ctypes.c_int), ("grouping", ctypes.c_int), ("partial_dtype", ctypes.c_int),
                 ("launch_cost_rows", ctypes.c_int), ("presorted", ctypes.c_int), ("search", ctypes.c_int),
-                ("gather", ctypes.c_int), ("reserved", ctypes.c_int * 6)]
+                ("gather", ctypes.c_int), ("wg", ctypes.c_int), ("gemm_tile_rows", ctypes.c_int),
+                ("reserved", ctypes.c_int * 4)]
 
     @classmethod
     def make(cls, **kw) -> "Options":

@@ -180,6 +180,7 @@ struct SearchArgs {
   int32_t* ts;
   int64_t ts_stride;
   int64_t pair_cap;       // capacity of the pair lists (K3 * queries)
+  int wg;                 // threads per workgroup of the count and write passes (0: 256)
   // Submanifold map with odd K (offset k and K^3 - 1 - k are mirror images).
   int sym;
   // 0: the write pass leaves T_s alone (a symmetric map's T_s is filled from the
@@ -257,8 +258,9 @@ hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_o
 // a_rows[r] (buf_in is then the layer's input features, a_rows the pairs' input rows).
 // wt: transposed weights (launch_transpose_w) or NULL;
 // dump_row: one spare row of c_out partials the full-width kernel may overwrite.
+// tile_rows: output rows per workgroup tile (0: about two tiles per workgroup slot)
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
                        const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
-                       hipStream_t s);
+                       int tile_rows, hipStream_t s);
 
 }  // namespace spc

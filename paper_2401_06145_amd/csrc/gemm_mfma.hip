@@ -618,7 +618,7 @@ hipError_t wide_occupancy(const void* fn, size_t lds, int* per_cu, int* cus) {
 
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
                        const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
-                       hipStream_t s) {
+                       int tile_rows, hipStream_t s) {
   if (c_out % 16 != 0) return hipErrorInvalidValue;
   const bool wide = dump_row && gemm_wide(c_in, c_out, dtype, part_dtype);
   int64_t rows_all = 0;
@@ -641,8 +641,11 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
     if (e != hipSuccess) return e;
     const int64_t slots = (int64_t)std::max(per_cu, 1) * std::max(cus, 1);
     const int round = wide_round_rows(nt, ks);
-    const int64_t want = (rows_all + 2 * slots - 1) / (2 * slots);
-    rows_per_tile = (int)std::min<int64_t>(std::max<int64_t>((want + round - 1) / round, 1) * round, 16 * round);
+    const int64_t want = tile_rows > 0 ? tile_rows : (rows_all + 2 * slots - 1) / (2 * slots);
+    const int64_t cap = tile_rows > 0 ? (int64_t)1 << 20 : 16 * round;
+    rows_per_tile = (int)std::min<int64_t>(std::max<int64_t>((want + round - 1) / round, 1) * round, cap);
+  } else if (tile_rows > 0) {
+    rows_per_tile = (tile_rows + 15) / 16 * 16;
   } else {
     // enough workgroups to fill 256 CUs several times, at most 1024 rows each
     while (rows_per_tile < 1024 && rows_all / (rows_per_tile * 2) >= 2048) rows_per_tile *= 2;

@@ -1057,11 +1057,11 @@ __device__ __forceinline__ void lds_search(const uint64_t* lkey, const uint64_t 
 // sorted-query order, and pair index o (the pair's GEMM buffer row) replaces the
 // source position in T_q and is stored in T_s.  The loads of all rounds of a
 // chunk are issued together: results first, then the rows of the matches.
-template <int ROUNDS>
-__global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const uint32_t* bounds, int64_t nb,
+template <int ROUNDS, int TH>
+__global__ __launch_bounds__(TH) void k_forward_write(SearchArgs a, const uint32_t* bounds, int64_t nb,
                                                             const uint32_t* item_off, int32_t* pin, int32_t* pout,
                                                             ControlBlock* cb) {
-  __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
+  __shared__ uint32_t s_cnt[ROUNDS][(TH / kWave)];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
@@ -1106,7 +1106,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
     int32_t sp[ROUNDS];
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) {
-      const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+      const int64_t qp = q0 + (int64_t)r * TH + tid;
       sp[r] = (qp < q1) ? res[qp] : -1;
     }
     int32_t r_in[ROUNDS], r_out[ROUNDS];
@@ -1114,7 +1114,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) {
       // rows of the match (a valid dummy address for lanes without one)
-      const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+      const int64_t qp = q0 + (int64_t)r * TH + tid;
       const bool hit = sp[r] >= 0;
       const int32_t src = (int32_t)a.sidx[hit ? sp[r] : 0];
       const int32_t qry = (int32_t)a.qrow[hit ? qp : 0];
@@ -1129,7 +1129,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) {
 #pragma unroll
-      for (int v = 0; v < kWavesPerBlock; ++v) {
+      for (int v = 0; v < (TH / kWave); ++v) {
         if (v == wave) before[r] = total;
         total += s_cnt[r][v];
       }
@@ -1138,7 +1138,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
     for (int r = 0; r < ROUNDS; ++r) {
       if ((bal[r] >> lane) & 1ull) {
         const uint64_t o = base + before[r] + (uint64_t)popc64(bal[r] & lanemask_lt());
-        const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+        const int64_t qp = q0 + (int64_t)r * TH + tid;
         if (o >= (uint64_t)a.pair_cap) {  // only when keys were out of order (reported)
           atomicOr(&cb->err, kErrOverflow);
           continue;
@@ -1164,11 +1164,11 @@ __global__ __launch_bounds__(kThreads) void k_forward_write(SearchArgs a, const 
 // from HBM once instead of K^3 times.  The block's keys, the first chunk's query
 // keys and its bounds are all requested before the first wait; each chunk's
 // ROUNDS searches run as independent chains.
-template <int ROUNDS, int LOG2B>
-__global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const uint32_t* bounds, int64_t nb,
+template <int ROUNDS, int LOG2B, int TH>
+__global__ __launch_bounds__(TH) void k_forward_count(SearchArgs a, const uint32_t* bounds, int64_t nb,
                                                             uint32_t* item_cnt, int G, ControlBlock* cb) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ uint32_t s_cnt[ROUNDS][kWavesPerBlock];
+  __shared__ uint32_t s_cnt[ROUNDS][(TH / kWave)];
   uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -1179,12 +1179,12 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
 
   const int64_t s0 = b * (int64_t)a.B;
   const int nB = (int)min((int64_t)a.B, a.n_src - s0);
-  // Requested together before the first wait: the block's first 4 * kThreads keys,
+  // Requested together before the first wait: the block's first 4 * TH keys,
   // the key before the block (repeat check), the first offset's bounds and the
   // keys of its first chunk.
   uint64_t sv[4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) sv[u] = a.skeys[s0 + min(u * kThreads + tid, nB - 1)];
+  for (int u = 0; u < 4; ++u) sv[u] = a.skeys[s0 + min(u * TH + tid, nB - 1)];
   const uint64_t key_before = a.skeys[s0 > 0 ? s0 - 1 : 0];
   const int k_first = g * G;
   const int k_end = min(a.K3, k_first + G);
@@ -1202,7 +1202,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
   auto load_keys = [&](int64_t q0, int64_t q1, uint64_t dk) {
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) {
-      const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+      const int64_t qp = q0 + (int64_t)r * TH + tid;
       key[r] = a.qkeys[qp < q1 ? qp : 0] + dk;
     }
   };
@@ -1210,15 +1210,15 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
   if (nch > 0) load_keys(q_lo, min(q_lo + (int64_t)a.Cq, q_hi), (uint64_t)a.dk[k_first]);
 #pragma unroll
   for (int u = 0; u < 4; ++u)
-    if (u * kThreads + tid < nB) lkey[u * kThreads + tid] = sv[u];
-  for (int e = 4 * kThreads + tid; e < nB; e += kThreads) lkey[e] = a.skeys[s0 + e];  // B > 4 * kThreads
-  for (int e = nB + tid; e <= (1 << LOG2B); e += kThreads) lkey[e] = ~0ull;   // padding
+    if (u * TH + tid < nB) lkey[u * TH + tid] = sv[u];
+  for (int e = 4 * TH + tid; e < nB; e += TH) lkey[e] = a.skeys[s0 + e];  // B > 4 * TH
+  for (int e = nB + tid; e <= (1 << LOG2B); e += TH) lkey[e] = ~0ull;   // padding
   __syncthreads();
   if (g == 0) {
     // the sorted source keys must be strictly increasing: equal neighbours are
     // repeated coordinates, decreasing ones an unsorted input declared sorted
     bool dup = false, unsorted = false;
-    for (int e = tid; e < nB; e += kThreads) {
+    for (int e = tid; e < nB; e += TH) {
       const uint64_t prev = (e > 0) ? lkey[e - 1] : key_before;
       if (e > 0 || s0 > 0) {
         dup |= lkey[e] == prev;
@@ -1243,7 +1243,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
       lds_search<ROUNDS, LOG2B>(lkey, key, pos, hit);
 #pragma unroll
       for (int r = 0; r < ROUNDS; ++r) {
-        const int64_t qp = q0 + (int64_t)r * kThreads + tid;
+        const int64_t qp = q0 + (int64_t)r * TH + tid;
         const bool valid = qp < q1;
         if (valid) res[qp] = hit[r] ? (int32_t)(s0 + pos[r]) : -1;
         const uint64_t bal = __ballot(valid && hit[r]);
@@ -1254,7 +1254,7 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
 #pragma unroll
         for (int r = 0; r < ROUNDS; ++r)
 #pragma unroll
-          for (int v = 0; v < kWavesPerBlock; ++v) item_total += s_cnt[r][v];
+          for (int v = 0; v < (TH / kWave); ++v) item_total += s_cnt[r][v];
       }
       __syncthreads();  // s_cnt is rewritten by the next chunk
     }
@@ -1262,16 +1262,16 @@ __global__ __launch_bounds__(kThreads) void k_forward_count(SearchArgs a, const 
   }
 }
 
-template <int ROUNDS>
+template <int ROUNDS, int TH>
 hipError_t forward_count_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds, int64_t nb,
                            uint32_t* item_cnt, int G, ControlBlock* cb, int log2B) {
   // the block plus its padding: 2^log2B + 1 keys
   const size_t lds = (((size_t)1 << log2B) + 1) * sizeof(uint64_t);
   switch (log2B) {
-#define SPC_FC(L2)                                                                                                 \
-  case L2:                                                                                                         \
-    hipLaunchKernelGGL((k_forward_count<ROUNDS, L2>), dim3(grid), dim3(kThreads), lds, s, a, bounds, nb, item_cnt, \
-                       G, cb);                                                                                     \
+#define SPC_FC(L2)                                                                                              \
+  case L2:                                                                                                      \
+    hipLaunchKernelGGL((k_forward_count<ROUNDS, L2, TH>), dim3(grid), dim3(TH), lds, s, a, bounds, nb, item_cnt, \
+                       G, cb);                                                                                  \
     break;
     SPC_FC(6) SPC_FC(7) SPC_FC(8) SPC_FC(9) SPC_FC(10) SPC_FC(11) SPC_FC(12)
 #undef SPC_FC
@@ -1281,11 +1281,10 @@ hipError_t forward_count_t(unsigned grid, hipStream_t s, const SearchArgs& a, co
   return hipGetLastError();
 }
 
-template <int ROUNDS>
+template <int ROUNDS, int TH>
 hipError_t forward_write_t(unsigned grid, hipStream_t s, const SearchArgs& a, const uint32_t* bounds, int64_t nb,
                            const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb) {
-  hipLaunchKernelGGL((k_forward_write<ROUNDS>), dim3(grid), dim3(kThreads), 0, s, a, bounds, nb, item_off, pin, pout,
-                     cb);
+  hipLaunchKernelGGL((k_forward_write<ROUNDS, TH>), dim3(grid), dim3(TH), 0, s, a, bounds, nb, item_off, pin, pout, cb);
   return hipGetLastError();
 }
 
@@ -1742,30 +1741,32 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
   if (nb <= 0) return hipSuccess;
   int log2B = 0;
   while ((1 << log2B) < a.B) ++log2B;
-  const int rounds = a.Cq / kThreads;
+  const int th = a.wg > 0 ? a.wg : kThreads;
+  const int rounds = a.Cq / th;
+  // (threads, rounds) pairs: each chunk of Cq queries is rounds x threads
+#define SPC_TR(TH_, R_, CALL) \
+  if (th == TH_ && rounds == R_) return CALL;
+#define SPC_TR_ALL(F, ...)                                                                                      \
+  SPC_TR(128, 2, (F<2, 128>(__VA_ARGS__))) SPC_TR(128, 4, (F<4, 128>(__VA_ARGS__)))                            \
+  SPC_TR(128, 8, (F<8, 128>(__VA_ARGS__))) SPC_TR(256, 1, (F<1, 256>(__VA_ARGS__)))                            \
+  SPC_TR(256, 2, (F<2, 256>(__VA_ARGS__))) SPC_TR(256, 4, (F<4, 256>(__VA_ARGS__)))                            \
+  SPC_TR(256, 8, (F<8, 256>(__VA_ARGS__))) SPC_TR(512, 1, (F<1, 512>(__VA_ARGS__)))                            \
+  SPC_TR(512, 2, (F<2, 512>(__VA_ARGS__))) SPC_TR(512, 4, (F<4, 512>(__VA_ARGS__)))
   if (write) {
     const unsigned grid = (unsigned)((int64_t)a.K3 * nb);
     ProfScope ps(KN_FORWARD_WRITE, s);
-    switch (rounds) {
-      case 1: return forward_write_t<1>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
-      case 2: return forward_write_t<2>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
-      case 4: return forward_write_t<4>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
-      case 8: return forward_write_t<8>(grid, s, a, bounds, nb, item_off, pin, pout, cb);
-      default: return hipErrorInvalidValue;
-    }
+    SPC_TR_ALL(forward_write_t, grid, s, a, bounds, nb, item_off, pin, pout, cb)
+    return hipErrorInvalidValue;
   }
   const int64_t ngroups0 = std::min<int64_t>(a.K3, std::max<int64_t>(1, (kCountTargetGroups + nb - 1) / nb));
   const int G = (int)((a.K3 + ngroups0 - 1) / ngroups0);
   const int64_t ngroups = (a.K3 + G - 1) / G;
   const unsigned grid = (unsigned)(nb * ngroups);
   ProfScope ps(KN_FORWARD_COUNT, s);
-  switch (rounds) {
-    case 1: return forward_count_t<1>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
-    case 2: return forward_count_t<2>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
-    case 4: return forward_count_t<4>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
-    case 8: return forward_count_t<8>(grid, s, a, bounds, nb, item_cnt, G, cb, log2B);
-    default: return hipErrorInvalidValue;
-  }
+  SPC_TR_ALL(forward_count_t, grid, s, a, bounds, nb, item_cnt, G, cb, log2B)
+#undef SPC_TR_ALL
+#undef SPC_TR
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_hash_build(const int32_t* coords, int64_t n, const KeyLayout* L, uint64_t* hkeys, uint32_t* hvals,

@@ -120,10 +120,12 @@ class Network:
     """GPU runner of an op list: builds and caches the kernel maps, then runs the ops."""
 
     def __init__(self, coords: torch.Tensor, dtype: torch.dtype = torch.float16, ops: list[Op] | None = None,
-                 weights: dict | None = None):
+                 weights: dict | None = None, layer_opts: dict | None = None):
         self.dev = coords.device
         self.dtype = dtype
         self.ops = ops or unet_ops()
+        # per-layer forward options (a tuned table: op name -> binding.Options), else defaults
+        self.layer_opts = layer_opts or {}
         self.coords = {0: coords}
         self.maps: dict = {}
         self.fwd: dict = {}
@@ -172,9 +174,10 @@ class Network:
                 t[op.out] = B.spconv_concat_rows(t[op.inp], t[op.other])
             else:
                 km = self._map(op.level, op.K, op.mode)
-                key = (id(km), op.c_in, op.c_out)
+                lo = self.layer_opts.get(op.out)
+                key = (id(km), op.c_in, op.c_out, op.out if lo is not None else None)
                 if key not in self.fwd:
-                    self.fwd[key] = B.Forward(km, op.c_in, op.c_out, self.dtype)
+                    self.fwd[key] = B.Forward(km, op.c_in, op.c_out, self.dtype, lo)
                 res = t[op.residual] if op.residual else None
                 t[op.out] = self.fwd[key](t[op.inp], self.w[op.out], residual=res, relu=op.relu)
         return t if keep else {"out": t[self.ops[-1].out]}

@@ -39,12 +39,13 @@ def cloud(scene: str, n: int, side: int):
     return scenes.uniform_cells_large(n, side, 5000 + n % 997) if n > 1_000_000 else scenes.uniform_cells(n, side, 5000)
 
 
-def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = False, scene: str = "uniform"):
+def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = False, scene: str = "uniform",
+            search_opts: dict | None = None):
     dev = torch.device("cuda:0")
     c = cloud(scene, n, side)
     n = len(c)
     coords = torch.from_numpy(c).to(dev)
-    opt = B.Options.make(search=1) if hash_search else None
+    opt = B.Options.make(search=1 if hash_search else 0, **(search_opts or {}))
     ws = torch.empty(B.spconv_map_workspace_bytes(n, 0, K, B.SPCONV_SUBM, opt), dtype=torch.uint8, device=dev)
 
     def build():
@@ -92,7 +93,7 @@ def measure(n: int, side: int, rounds: int, K: int = 3, hash_search: bool = Fals
         "k_forward_write": 4 * k3 * n + 4 * n + 4 * n + 12 * pairs,
     }
     row = {"scene": scene, "voxels": n, "grid": side if scene == "uniform" else None,
-           "search": "hash" if hash_search else "sorted", "pairs": pairs,
+           "search": "hash" if hash_search else "sorted", "pairs": pairs, "search_opts": search_opts or {},
            "map_ms": round(map_ms, 4),
            "phases_ms": {k: round(v, 4) for k, v in phases.items()},
            "map_gbps_compulsory": round(map_bytes / (map_ms * 1e-3) / 1e9, 1),
@@ -115,13 +116,17 @@ def main(argv=None):
     p.add_argument("--search", choices=["sorted", "hash", "both"], default="both",
                    help="sorted-array search (the method), hash-table search (ablation), or both")
     p.add_argument("--scene", choices=["uniform", "lidar"], default="uniform")
+    p.add_argument("--B", type=int, default=0, help="source block size (0: the library default)")
+    p.add_argument("--Cq", type=int, default=0, help="query block limit (0: the library default)")
+    p.add_argument("--wg", type=int, default=0, help="search workgroup size (0: the library default)")
     a = p.parse_args(argv)
+    so = {k: v for k, v in (("B", a.B), ("Cq", a.Cq), ("wg", a.wg)) if v}
     if not torch.cuda.is_available():
         raise SystemExit("the sweep needs a GPU")
     for n in a.sizes:
         side = 400 if n <= 1_000_000 else 800
         for hs in ((False, True) if a.search == "both" else ((a.search == "hash"),)):
-            print(json.dumps(measure(n, side, a.rounds, hash_search=hs, scene=a.scene)), flush=True)
+            print(json.dumps(measure(n, side, a.rounds, hash_search=hs, scene=a.scene, search_opts=so)), flush=True)
 
 
 def summarize(rows_jsonl, counters, title, command, out=sys.stdout):

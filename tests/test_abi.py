@@ -39,6 +39,11 @@ def test_workspace_bytes_host_only():
     assert B.spconv_map_workspace_bytes(10, 0, 3, 7) == 0                    # bad mode
     bad = B.Options.make(B=100)
     assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, bad) == 0
+    # search workgroup size: 128, 256 or 512 threads, Cq / wg in {1, 2, 4, 8}
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(wg=100)) == 0
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(wg=512, Cq=256)) == 0
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(wg=128, Cq=2048)) == 0
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(wg=512, Cq=1024)) > 0
     assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(search=2)) == 0
     # the hash-table search adds its table (2^11 slots of 12 bytes for 1000 inputs)
     hashed = B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(search=1))

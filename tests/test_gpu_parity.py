@@ -58,6 +58,36 @@ def test_subm_small(K, Bsz, Cq):
     assert rel_err(to_f64(y), ref) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("wg,Cq", [(128, 256), (128, 1024), (512, 512), (512, 2048)])
+def test_search_workgroup_sizes(wg, Cq):
+    """The forward search's workgroup size (Section 5.1.4's thread-block size) changes
+    only the launch shape: maps equal the oracle's, SUBM and DOWN."""
+    say(f"search workgroup size {wg}, Cq {Cq}")
+    c = _cloud(60, 6000, -12, 12)
+    opt = B.Options.make(B=256, Cq=Cq, wg=wg)
+    km = B.KernelMap.build(to_dev(c), 3, opt=opt)
+    assert_map_equal(km, oracle.kernel_map(c, None, 3, 1, "subm"))
+    kd = B.KernelMap.build(to_dev(c), 2, 2, 1, "down", opt=opt)
+    q = oracle.out_coords(c, 2, 1)
+    assert np.array_equal(kd.out_coords().cpu().numpy(), q)
+    assert_map_equal(kd, oracle.kernel_map(c, q, 2, 1, "down"))
+
+
+@pytest.mark.parametrize("c", [64, 256])
+def test_gemm_tile_rows_result_neutral(c):
+    """Rows per GEMM workgroup tile change the launch shape only: bit-identical output."""
+    say(f"GEMM tile rows, C={c}")
+    cl = scenes.workload(1).coords[:30000].copy()
+    x = scenes.features(len(cl), c, "f16", 21)
+    w = scenes.weights(3, c, c, "f16", 22)
+    km = B.KernelMap.build(to_dev(cl), 3)
+    xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
+    base = B.Forward(km, c, c, torch.float16)(xd, wd)
+    for rows in (16, 100, 512, 5000, 1 << 20):
+        y = B.Forward(km, c, c, torch.float16, B.Options.make(gemm_tile_rows=rows))(xd, wd)
+        assert torch.equal(y, base), f"gemm_tile_rows={rows} changed the result"
+
+
 @pytest.mark.parametrize("K,s,t", [(2, 2, 1), (3, 2, 1), (2, 2, 2), (2, 3, 1), (3, 3, 2)])
 @pytest.mark.parametrize("Bsz", [64, 256])
 def test_down_up_small(K, s, t, Bsz):

@@ -86,7 +86,7 @@ def copy_calibration(mib: int) -> None:
                       "dispatches": 3}))
 
 
-def kernel_models(n, n_out, pairs, L, k3, passes, fused=True, pelem=None):
+def kernel_models(n, n_out, pairs, L, k3, passes, fused=True, pelem=None, centre=False):
     """Algorithmic (compulsory) bytes or flops per launch of each kernel.
 
     Returns name -> (bound, amount).  See the measurement section of the design
@@ -94,6 +94,10 @@ def kernel_models(n, n_out, pairs, L, k3, passes, fused=True, pelem=None):
     """
     e = 4 if L.dtype == "f32" else 2
     ep = e if pelem is None else pelem  # GEMM partial element size
+    # with the submanifold centre offset multiplied inside the scatter, the GEMMs skip
+    # its n_out pairs
+    cr = n_out if centre else 0
+    pg = pairs - cr  # the GEMMs' pairs
     P = max(passes, 1)
     # scans per step: the match-count scan (one entry per work item, K^3 x source blocks
     # of 1024), plus one digit-offset scan per radix pass when the sort has between 257
@@ -125,9 +129,14 @@ def kernel_models(n, n_out, pairs, L, k3, passes, fused=True, pelem=None):
         "k_scatter": ("hbm", pairs * L.c_out * ep + n_out * L.c_out * e + 4 * n_out * (k3 + 1)),
         # GEMM: A rows (the gathered buffer, or with the fused gather each input row once
         # plus one row index per pair), partial rows, weights
-        "k_gemm_bytes": ("hbm", (pairs * L.c_in * e if not fused else n * L.c_in * e + 4 * pairs)
-                         + pairs * L.c_out * ep + k3 * L.c_in * L.c_out * e),
-        "k_gemm_flops": ("mfma", 2.0 * pairs * L.c_in * L.c_out),
+        "k_gemm_bytes": ("hbm", (pg * L.c_in * e if not fused else n * L.c_in * e + 4 * pg)
+                         + pg * L.c_out * ep + (k3 - (1 if centre else 0)) * L.c_in * L.c_out * e),
+        "k_gemm_flops": ("mfma", 2.0 * pg * L.c_in * L.c_out),
+        # scatter with the centre offset: each output's own input row, the other offsets'
+        # partial rows, one table entry per (offset, output), the row map, W_c, the output
+        "k_scatter_centre": ("hbm", n_out * L.c_in * e + pg * L.c_out * ep + n_out * L.c_out * e
+                             + 4 * n_out * (k3 + 1) + L.c_in * L.c_out * e),
+        "k_scatter_centre_flops": ("mfma", 2.0 * cr * L.c_in * L.c_out),
     }
     return m
 
@@ -324,6 +333,11 @@ def roofline_for(kernel, models, mean_launch_ms, L, workload):
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None, "kernel": kernel,
                 "algorithmic_bytes_per_launch": int(work)}
+        if kernel + "_flops" in models:
+            # the centre offset's MFMA work inside the same launch, against the MFMA peak
+            fl = models[kernel + "_flops"][1]
+            roof["mfma_flops_per_launch"] = fl
+            roof["mfma_frac"] = round(fl / (mean_launch_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS[L.dtype], 5)
     tb = measured_traffic(kernel, workload)
     roof["traffic"] = round(tb) if tb is not None else None
     return roof
@@ -359,7 +373,8 @@ def main():
 
     k3 = L.K ** 3
     passes = int(round(kern.get("k_radix_scatter", (0, 0))[1]))
-    models = kernel_models(lb.n, lb.n_out, lb.pairs, L, k3, passes, fused=lb.fused, pelem=lb.pelem)
+    models = kernel_models(lb.n, lb.n_out, lb.pairs, L, k3, passes, fused=lb.fused, pelem=lb.pelem,
+                           centre=bool(lb.plan.centre))
     roof = roofline_for(dominant, models, mean_launch_ms, L, lb.wl.name)
     roof.update({"mean_launch_ms": round(mean_launch_ms, 6), "launches_per_step": launches_per_step,
                  "timed_launches": timed_launches, "event_steps": f"1 in {EVENT_EVERY} timed steps"})
@@ -386,7 +401,8 @@ def main():
         "dtype": L.dtype,
         "data": "synthetic",
         "config": {"workload": lb.wl.name, "voxels": n, "out_voxels": n_out, "pairs": pairs, "K": L.K,
-                   "c_in": L.c_in, "c_out": L.c_out, "mode": L.mode, "gemm_partials": pname},
+                   "c_in": L.c_in, "c_out": L.c_out, "mode": L.mode, "gemm_partials": pname,
+                   "centre_in_scatter": bool(lb.plan.centre)},
         "map_ms": round(map_ms, 5),
         "gmas_ms": round(gmas_ms, 5),
         "phases_ms": {k: round(v, 5) for k, v in ph_ms.items()},
@@ -416,6 +432,9 @@ def main():
         other_g = B.GATHER_BUFFER if lb.fused else B.GATHER_FUSED
         out["gmas_ms_other_gather"] = {"gather": "buffer" if lb.fused else "fused",
                                        **gmas_of(lb.phases(gather=other_g))}
+        if lb.plan.centre:
+            # the centre offset through the GEMM and its partial buffer, like the other offsets
+            out["gmas_ms_centre_through_gemm"] = gmas_of(lb.phases(centre=1))
     lb_cpu = (lb.coords_np, lb.x_np, lb.w_np, L)
     lb.close()
     del lb
@@ -446,7 +465,7 @@ def quick_layer(workload, channels, steps=20):
         lb.step()
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
-    flops = 2.0 * lb.pairs * lb.L.c_in * lb.L.c_out
+    flops = 2.0 * lb.plan.rows_real * lb.L.c_in * lb.L.c_out  # the GEMMs' real pairs
     res = {"ms_per_layer": round(ms, 5), "map_ms": round(sum(ph.get(p, 0.0) for p in MAP_PHASES), 5),
            "gmas_ms": round(sum(ph.get(p, 0.0) for p in GMAS_PHASES), 5),
            "gemm_ms": round(ph.get("gemm", 0.0), 5),

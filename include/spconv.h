@@ -106,9 +106,17 @@ typedef struct {
                         write passes (Section 5.1.4's thread-block size): 128, 256 or 512, and
                         Cq / wg must be 1, 2, 4 or 8 */
   int gemm_tile_rows; /* spconv_forward: output rows per GEMM workgroup tile, rounded up to the
-                        kernel's rows per round (16 to 128); default 0 = about two tiles per
-                        workgroup slot of the GPU */
-  int reserved[4];
+                        kernel's rows per round (16 to 256); default 0 = about two tiles per
+                        workgroup slot of the GPU, at least 512 rows */
+  int centre;        /* spconv_forward, odd-K SPCONV_SUBM maps: 0 = default, the centre offset (which
+                        pairs every output with its own input row) is multiplied inside the scatter
+                        and the GEMMs skip it, where the layer allows (fused gather, 16-bit layer,
+                        c_in % 8 == 0 and c_out % 32 == 0, both at most 256); 1 = off, the centre goes
+                        through the GEMM and its partial buffer like every offset; 2 = on, and
+                        SPCONV_EUNSUPPORTED where it does not apply.  The sums differ from the
+                        unfused path only in rounding (the centre's product is not rounded to the
+                        partial type) */
+  int reserved[3];
 } spconv_options;
 
 typedef struct spconv_map spconv_map; /* opaque host-side object */
@@ -250,6 +258,7 @@ typedef struct {
   int t_scatter;
   int grouping;
   int gather; /* spconv_gather */
+  int centre; /* 1: the centre offset is computed in the scatter (rows_* then leave out its rows) */
 } spconv_plan_info;
 int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype,
                         const spconv_options* opt, spconv_plan_info* info);
@@ -260,7 +269,7 @@ int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype,
  * spconv_forward (ids 0..10: bounds, sort, outcoords, backward, balance, forward,
  * readback, metadata (the table fill of maps other than odd-K submanifold ones),
  * gather, gemm, scatter) or around each launch of that kernel
- * (ids 16..31; spconv_profile_phase_name() gives the names, "" for unused ids).
+ * (ids 16..39; spconv_profile_phase_name() gives the names, "" for unused ids).
  * mask = 0 turns timing off.  spconv_profile_read() waits for the recorded events
  * and writes the summed milliseconds and the number of timed intervals per id
  * into host arrays of at least spconv_profile_phase_count() entries; reset != 0

@@ -90,7 +90,7 @@ const char* prof_name(int id) {
       "scatter", "hash", "", "", "", "",
       "k_minmax", "k_radix_hist", "k_radix_scatter", "k_scan", "k_copy", "k_down_keys", "k_unique", "k_backward",
       "k_forward_count", "k_forward_write", "k_fill", "k_radix_local", "k_gather", "k_gemm", "k_scatter", "k_pack",
-      "k_hash_insert", "k_hash_probe", "", "", "", "", "", ""};
+      "k_hash_insert", "k_hash_probe", "k_scatter_centre", "", "", "", "", ""};
   return (id >= 0 && id < PROF_IDS) ? kNames[id] : "";
 }
 struct PhaseRec {
@@ -358,7 +358,11 @@ struct GmasPlan {
   int grouping = SPCONV_GROUP_RAGGED;
   int gather = 2;  // 1: Algorithm 1 into a buffer; 2: fused into the GEMM's operand loads
   int gemm_tile_rows = 0;  // 0: the occupancy rule
-  int64_t rows_real = 0, rows_padded = 0;
+  // odd-K submanifold maps: the centre offset's product is computed inside the
+  // scatter (k_scatter_centre) and the GEMMs skip that offset; -1: not fused
+  int centre_k = -1;
+  int64_t rows_pairs = 0;                 // all pairs of the map (partial buffer rows)
+  int64_t rows_real = 0, rows_padded = 0;  // the GEMMs' rows, without and with padding
   int n_launches = 0;
   std::vector<std::vector<GemmSeg>> launches;  // one entry per GEMM launch (group)
 };
@@ -424,15 +428,31 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
     return fail(SPCONV_EINVAL, "gather must be 0, SPCONV_GATHER_BUFFER or SPCONV_GATHER_FUSED");
 
   const int K3 = m->K3;
-  p->rows_real = m->ptr[K3];
+  p->rows_pairs = m->ptr[K3];
   p->rows_padded = 0;
   p->launches.clear();
+  const int centre = opt ? opt->centre : 0;
+  if (centre < 0 || centre > 2) return fail(SPCONV_EINVAL, "centre must be 0, 1 or 2");
+  p->centre_k = -1;
+  if (centre != 1) {
+    const int kc = (K3 - 1) / 2;
+    const bool applies = m->mode == SPCONV_SUBM && m->K % 2 == 1 && m->omt && m->n_out > 0 &&
+                         m->counts[kc] == m->n_out && p->gather == SPCONV_GATHER_FUSED &&
+                         c_in <= 256 && c_out <= 256 && centre_fusable(c_in, c_out, dtype, p->part_dtype);
+    if (applies) p->centre_k = kc;
+    else if (centre == 2)
+      return fail(SPCONV_EUNSUPPORTED, "centre = 2: the centre offset cannot be fused into the scatter here (needs "
+                                       "an odd-K submanifold map, the fused gather, a 16-bit layer, c_in % 8 == 0 "
+                                       "and c_out % 32 == 0, both at most 256)");
+  }
+  auto in_gemm = [&](int k) { return m->counts[k] > 0 && k != p->centre_k; };
+  p->rows_real = p->rows_pairs - (p->centre_k >= 0 ? m->counts[p->centre_k] : 0);
   // Buffer rows follow the concatenated pair lists (row of pair e of offset k =
   // ptr[k] + e); grouping decides launches and padded heights only.
   if (p->grouping == SPCONV_GROUP_RAGGED) {
     std::vector<int> order;
     for (int k = 0; k < K3; ++k)
-      if (m->counts[k] > 0) order.push_back(k);
+      if (in_gemm(k)) order.push_back(k);
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return m->counts[a] > m->counts[b]; });
     std::vector<GemmSeg> segs;
     for (int k : order) segs.push_back(GemmSeg{k, m->ptr[k], m->counts[k], m->counts[k]});
@@ -445,7 +465,7 @@ int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_
       std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return m->counts[a] < m->counts[b]; });
     std::vector<int> nz;
     for (int k : order)
-      if (m->counts[k] > 0) nz.push_back(k);
+      if (in_gemm(k)) nz.push_back(k);
     const int64_t L = (opt && opt->launch_cost_rows > 0) ? opt->launch_cost_rows : 32768;
     const std::vector<int> cuts = dp_groups(nz, m->counts, L);
     for (size_t g = 0; g + 1 < cuts.size(); ++g) {
@@ -476,9 +496,10 @@ size_t plan_forward_ws(void* base, const spconv_map* m, int c_in, int c_out, con
               ? a.take_bytes((size_t)m->K3 * c_in * c_out * p.elem)
               : nullptr;
   // the fused gather reads the input rows directly: no gathered buffer
-  b->buf_in = (p.gather == SPCONV_GATHER_BUFFER) ? a.take_bytes((size_t)p.rows_real * c_in * p.elem) : nullptr;
+  b->buf_in = (p.gather == SPCONV_GATHER_BUFFER) ? a.take_bytes((size_t)p.rows_pairs * c_in * p.elem) : nullptr;
   // one spare row past the partials: the full-width GEMM's stores of rows without data
-  b->buf_out = a.take_bytes((size_t)(p.rows_real + 1) * c_out * p.pelem);
+  // (rows are pair indices: with the centre fused its rows stay unused)
+  b->buf_out = a.take_bytes((size_t)(p.rows_pairs + 1) * c_out * p.pelem);
   return align_up(a.off, 256);
 }
 
@@ -877,6 +898,7 @@ int spconv_forward_plan(const spconv_map* m, int c_in, int c_out, int dtype, con
   info->t_scatter = p.t_scatter;
   info->grouping = p.grouping;
   info->gather = p.gather;
+  info->centre = p.centre_k >= 0 ? 1 : 0;
   return SPCONV_OK;
 }
 
@@ -908,7 +930,7 @@ int forward_impl(const spconv_map* m, const void* d_x, const void* d_w, void* d_
   int st = make_plan(m, c_in, c_out, dtype, opt, &p);
   if (st != SPCONV_OK) return st;
   if (m->n_out > 0 && !d_y) return fail(SPCONV_EINVAL, "d_y is NULL");
-  if (p.rows_real > 0 && (!d_x || !d_w)) return fail(SPCONV_EINVAL, "d_x / d_w is NULL");
+  if (p.rows_pairs > 0 && (!d_x || !d_w)) return fail(SPCONV_EINVAL, "d_x / d_w is NULL");
   auto misaligned = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) != 0; };
   if (misaligned(d_x) || misaligned(d_w) || misaligned(d_y) || misaligned(d_residual))
     return fail(SPCONV_EINVAL, "d_x, d_w, d_y and d_residual must be 16-byte aligned");
@@ -921,7 +943,7 @@ int forward_impl(const spconv_map* m, const void* d_x, const void* d_w, void* d_
   hipStream_t s = static_cast<hipStream_t>(stream);
   // a map without tables has no pairs: the scatter then writes zeros (plus the epilogue)
   const int K3 = m->omt ? m->K3 : 0;
-  if (p.rows_real > 0) {
+  if (p.rows_pairs > 0) {
     const bool fused = p.gather == SPCONV_GATHER_FUSED;
     if (!fused && m->imt_pending) {
       PhaseScope ph(PH_METADATA, s);
@@ -947,16 +969,21 @@ int forward_impl(const spconv_map* m, const void* d_x, const void* d_w, void* d_
       const int32_t* a_rows = fused ? m->pin : nullptr;
       for (const auto& segs : p.launches)
         SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), a_src, a_rows, d_w, b.wt, b.buf_out,
-                            static_cast<char*>(b.buf_out) + (size_t)p.rows_real * c_out * p.pelem, c_in, c_out,
+                            static_cast<char*>(b.buf_out) + (size_t)p.rows_pairs * c_out * p.pelem, c_in, c_out,
                             dtype, p.part_dtype, p.gemm_tile_rows, s),
                 "grouped GEMM");
     }
   }
   {
     PhaseScope ph(PH_SCATTER, s);
-    SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, m->omt, m->omt_stride, m->out_perm, K3, d_y,
-                           dtype, p.t_scatter, d_residual, relu, s),
-            "scatter");
+    if (p.centre_k >= 0)
+      SPC_TRY(launch_scatter_centre(d_x, m->out_perm, d_w, b.wt, p.centre_k, b.buf_out, m->omt, m->omt_stride, K3,
+                                    d_y, d_residual, relu, m->n_out, c_in, c_out, dtype, p.part_dtype, s),
+              "scatter with the centre offset");
+    else
+      SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, m->omt, m->omt_stride, m->out_perm, K3, d_y,
+                             dtype, p.t_scatter, d_residual, relu, s),
+              "scatter");
   }
   return SPCONV_OK;
 }

@@ -94,7 +94,7 @@ enum ProfId : int {
   // kernels
   KN_MINMAX = 16, KN_RADIX_HIST, KN_RADIX_SCATTER, KN_SCAN, KN_COPY, KN_DOWN_KEYS, KN_UNIQUE,
   KN_BACKWARD, KN_FORWARD_COUNT, KN_FORWARD_WRITE, KN_FILL, KN_RADIX_LOCAL, KN_GATHER, KN_GEMM, KN_SCATTER,
-  KN_PACK, KN_HASH_INSERT, KN_HASH_PROBE,
+  KN_PACK, KN_HASH_INSERT, KN_HASH_PROBE, KN_SCATTER_CENTRE,
   PROF_IDS = 40
 };
 struct ProfScope {
@@ -262,5 +262,15 @@ hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_o
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
                        const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
                        int tile_rows, hipStream_t s);
+// The submanifold centre offset computed inside the scatter (odd K): y[perm[p]] =
+// relu?(x[perm[p]] W_kc + sum over k != kc of buf_out[omt[k][p]] + residual), the
+// centre first, then k ascending, in float32.  Whether an instance exists for the
+// layer (16-bit layers, c_in % 8 == 0 up to 256, c_out % 32 == 0 up to 256), and
+// its launcher.  wt: transposed weights or NULL.
+bool centre_fusable(int c_in, int c_out, int dtype, int part_dtype);
+hipError_t launch_scatter_centre(const void* x, const uint32_t* perm, const void* w, const void* wt, int kc,
+                                 const void* buf_out, const int32_t* omt, int64_t mt_stride, int K3, void* y,
+                                 const void* residual, int relu, int64_t n_out, int c_in, int c_out, int dtype,
+                                 int part_dtype, hipStream_t s);
 
 }  // namespace spc

@@ -42,6 +42,7 @@ SOURCES = {
     "k_scatter": "gmas_kernels.hip", "k_concat": "gmas_kernels.hip", "k_gemm": "gemm_mfma.hip",
     "k_transpose_w": "gemm_mfma.hip", "k_ts_from_pairs": "map_kernels.hip", "k_inverse_perm": "map_kernels.hip",
     "k_hash_insert": "map_kernels.hip", "k_hash_count": "map_kernels.hip", "k_hash_items": "map_kernels.hip",
+    "k_scatter_centre": "gemm_mfma.hip",
 }
 
 FOLD = [

@@ -89,7 +89,9 @@ def tune_tiles(workloads, rounds: int, samples: int, channels):
                     ms = _timed(lambda: f(x, w), "k_gather", rounds)
                     res["gather"].setdefault(t, []).append(ms)
                 for t in [t for t in tile_candidates(L.c_out, e) if t <= 64 and (t & (t - 1)) == 0 and t >= 4]:
-                    f = B.Forward(km, L.c_in, L.c_out, tdt, B.Options.make(t_scatter=t))
+                    # the scatter of every offset's partials (the default multiplies a
+                    # submanifold layer's centre offset inside its own scatter kernel, which has no tile)
+                    f = B.Forward(km, L.c_in, L.c_out, tdt, B.Options.make(t_scatter=t, centre=1))
                     ms = _timed(lambda: f(x, w), "k_scatter", rounds)
                     res["scatter"].setdefault(t, []).append(ms)
             sel = {}
@@ -173,7 +175,7 @@ def tune_unet(rounds: int, rows_cands=(64, 128, 256, 512, 1024, 2048, 4096), for
             f = B.Forward(km, op.c_in, op.c_out, torch.float16, opt)
             return _timed(lambda: f(x, w, residual=res, relu=op.relu), kernel, rounds)
 
-        sc = {t: run(B.Options.make(t_scatter=t), "k_scatter")
+        sc = {t: run(B.Options.make(t_scatter=t, centre=1), "k_scatter")
               for t in tile_candidates(op.c_out, 2) if 8 <= t <= 64 and (t & (t - 1)) == 0}
         gm = {r: run(B.Options.make(gemm_tile_rows=r), "k_gemm") for r in (0, *rows_cands)}
         # Algorithm 1's kernel takes tiles of 1, 2, 4, 8 or 16 16-byte vectors

@@ -269,13 +269,18 @@ def test_grouping_tiles_partials_are_result_neutral():
     dc = to_dev(c)
     km = B.KernelMap.build(dc, 3)
     xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
-    base = B.Forward(km, 64, 64, torch.float16)(xd, wd)
+    # the centre offset through the GEMM, like the other offsets (the tiles apply)
+    base = B.Forward(km, 64, 64, torch.float16, B.Options.make(centre=1))(xd, wd)
+    # the default computes the centre inside the scatter
+    base_c = B.Forward(km, 64, 64, torch.float16)(xd, wd)
     infos = []
     for g in (B.GROUP_RAGGED, B.GROUP_SORTED, B.GROUP_MAPORDER):
         for tg, ts in ((8, 8), (16, 16), (64, 32), (32, 64)):
             opt = B.Options.make(grouping=g, t_gather=tg, t_scatter=ts, gather=B.GATHER_BUFFER)
             y = B.Forward(km, 64, 64, torch.float16, opt)(xd, wd)
             assert torch.equal(y, base), f"grouping {g} tiles {tg}/{ts} changed the result"
+        y = B.Forward(km, 64, 64, torch.float16, B.Options.make(grouping=g))(xd, wd)
+        assert torch.equal(y, base_c), f"grouping {g} changed the result with the centre in the scatter"
         infos.append(km.plan(64, 64, torch.float16, B.Options.make(grouping=g)))
     # sorted grouping never pads more than map-order grouping with the same cost model
     assert infos[0].rows_padded == infos[0].rows_real
@@ -285,8 +290,10 @@ def test_grouping_tiles_partials_are_result_neutral():
     # float32 partials; the default float16 partials keep a 3x margin under the f16 tolerance
     y32 = B.Forward(km, 64, 64, torch.float16, B.Options.make(partial_dtype=1, t_scatter=4))(xd, wd)
     e32, e16 = rel_err(to_f64(y32), ref), rel_err(to_f64(base), ref)
-    print(f"normwise error: float32 partials {e32:.2e}, float16 partials {e16:.2e}", flush=True)
-    assert e32 <= TOL["f16"] and e16 <= TOL["f16"] / 3
+    ec = rel_err(to_f64(base_c), ref)
+    print(f"normwise error: float32 partials {e32:.2e}, float16 partials {e16:.2e}, "
+          f"float16 partials with the centre in the scatter {ec:.2e}", flush=True)
+    assert e32 <= TOL["f16"] and e16 <= TOL["f16"] / 3 and ec <= TOL["f16"] / 3
 
 
 @pytest.mark.parametrize("K,c_out,pd", [
@@ -309,8 +316,8 @@ def test_row_scatter_matches_tiled_and_oracle(K, c_out, pd):
     km = B.KernelMap.build(to_dev(c), K)
     xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
     res = to_dev(scenes.features(len(c), c_out, "f16", 73), "f16")
-    row = B.Options.make(partial_dtype=pd)
-    tiled = B.Options.make(partial_dtype=pd, t_scatter=16)
+    row = B.Options.make(partial_dtype=pd, centre=1)
+    tiled = B.Options.make(partial_dtype=pd, t_scatter=16, centre=1)
     assert km.plan(32, c_out, torch.float16, row).t_scatter == (4 if pd else 8)
     y_row = B.Forward(km, 32, c_out, torch.float16, row)(xd, wd)
     y_tiled = B.Forward(km, 32, c_out, torch.float16, tiled)(xd, wd)
@@ -348,7 +355,7 @@ def test_gather_forms_bit_identical(dtype, c_in, c_out, pd):
     ys = {}
     for g in (B.GATHER_BUFFER, B.GATHER_FUSED):
         for grp in (B.GROUP_RAGGED, B.GROUP_SORTED):
-            opt = B.Options.make(gather=g, grouping=grp, partial_dtype=pd)
+            opt = B.Options.make(gather=g, grouping=grp, partial_dtype=pd, centre=1)
             assert km.plan(c_in, c_out, td, opt).gather == g
             ys[g, grp] = B.Forward(km, c_in, c_out, td, opt)(xd, wd)
     assert km.plan(c_in, c_out, td).gather == B.GATHER_FUSED  # the default
@@ -374,13 +381,81 @@ def test_source_table_filled_on_first_table_gather(search, K):
     km = B.KernelMap.build(to_dev(c), K, opt=B.Options.make(search=search))
     xd, wd = to_dev(x, "f16"), to_dev(w, "f16")
     td = B.TORCH_DTYPES["f16"]
-    y_fused = B.Forward(km, 32, 32, td, B.Options.make(gather=B.GATHER_FUSED))(xd, wd)
+    y_fused = B.Forward(km, 32, 32, td, B.Options.make(gather=B.GATHER_FUSED, centre=1))(xd, wd)
     fwd = B.Forward(km, 32, 32, td, B.Options.make(gather=B.GATHER_BUFFER))
     for _ in range(2):
         assert torch.equal(fwd(xd, wd), y_fused)
     okm = oracle.kernel_map(c, None, K, 1, "subm")
     ref = oracle.features(scenes.to_f64(x, "f16"), scenes.to_f64(w, "f16"), okm)
     assert rel_err(to_f64(y_fused), ref) <= TOL["f16"]
+
+
+@pytest.mark.parametrize("K,dtype,c_in,c_out,pd,epi", [
+    (3, "f16", 32, 32, 0, False),
+    (3, "f16", 48, 64, 0, True),     # padding inside the second k-step; residual + ReLU
+    (5, "f16", 64, 64, 0, False),    # 125 offsets: several table batches per row
+    (1, "f16", 64, 32, 0, True),     # K = 1: the whole layer is the centre
+    (3, "bf16", 64, 96, 0, True),
+    (3, "bf16", 128, 128, 1, False), # float32 partials
+    (3, "f16", 256, 256, 1, True),   # W^T staged from the transposed copy, float32 partials
+    (3, "f16", 96, 192, 0, False),   # six column-tile pairs, c_in rounded up to four k-steps
+])
+def test_centre_offset_in_scatter(K, dtype, c_in, c_out, pd, epi):
+    """The submanifold centre offset multiplied inside the scatter (the GEMM skips it):
+    within tolerance of the oracle, with and without the residual + ReLU epilogue, and
+    close to the path that sends the centre through the GEMM (the sums differ only in
+    rounding: the centre's product is never rounded to the partial type)."""
+    say(f"centre in scatter K={K} {dtype} {c_in}->{c_out} partials {pd} epilogue {epi}")
+    c = _cloud(500 + K, 5000, -10, 10)
+    x = scenes.features(len(c), c_in, dtype, 501)
+    w = scenes.weights(K, c_in, c_out, dtype, 502)
+    km = B.KernelMap.build(to_dev(c), K)
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    td = B.TORCH_DTYPES[dtype]
+    on = B.Options.make(partial_dtype=pd, centre=2)
+    off = B.Options.make(partial_dtype=pd, centre=1)
+    pi_on, pi_off = km.plan(c_in, c_out, td, on), km.plan(c_in, c_out, td, off)
+    assert pi_on.centre == 1 and pi_off.centre == 0
+    assert pi_off.rows_real - pi_on.rows_real == len(c)  # the GEMM skips the centre's rows
+    assert km.plan(c_in, c_out, td).centre == 1          # the default
+    res = to_dev(scenes.features(len(c), c_out, dtype, 503), dtype) if epi else None
+    y_on = B.Forward(km, c_in, c_out, td, on)(xd, wd, residual=res, relu=epi)
+    y_off = B.Forward(km, c_in, c_out, td, off)(xd, wd, residual=res, relu=epi)
+    okm = oracle.kernel_map(c, None, K, 1, "subm")
+    ref = oracle.features(scenes.to_f64(x, dtype), scenes.to_f64(w, dtype), okm)
+    if epi:
+        ref = np.maximum(ref + to_f64(res), 0.0)
+    e_on, e_off = rel_err(to_f64(y_on), ref), rel_err(to_f64(y_off), ref)
+    print(f"normwise error: centre in scatter {e_on:.2e}, through the GEMM {e_off:.2e} "
+          f"(element-wise {elem_err(to_f64(y_on), ref):.2e})", flush=True)
+    assert e_on <= TOL[dtype] and e_off <= TOL[dtype]
+    assert rel_err(to_f64(y_on), to_f64(y_off)) <= TOL[dtype]
+    # deterministic: the same call twice gives the same bits
+    assert torch.equal(B.Forward(km, c_in, c_out, td, on)(xd, wd, residual=res, relu=epi), y_on)
+
+
+def test_centre_in_scatter_unsupported_cases():
+    """centre = 2 demands the fused centre and fails cleanly where it does not apply;
+    centre = 0 falls back to the GEMM path there."""
+    say("centre in scatter: unsupported cases")
+    c = _cloud(520, 2000, -8, 8)
+    km = B.KernelMap.build(to_dev(c), 3)
+    kd = B.KernelMap.build(to_dev(c), 2, 2, 1, "down")
+    k2 = B.KernelMap.build(to_dev(c), 2)  # even K: no centre offset
+    f16 = torch.float16
+    req = B.Options.make(centre=2)
+    for m, ci, co, td, opt in ((kd, 32, 32, f16, req), (k2, 32, 32, f16, req),
+                              (km, 32, 32, torch.float32, req),
+                              (km, 32, 16, f16, req), (km, 512, 32, f16, req), (km, 32, 512, f16, req),
+                              (km, 32, 32, f16, B.Options.make(centre=2, gather=B.GATHER_BUFFER))):
+        with pytest.raises(B.SpconvError) as ei:
+            m.plan(ci, co, td, opt)
+        assert ei.value.status == B.SPCONV_EUNSUPPORTED
+        dflt = B.Options.make(gather=opt.gather)
+        assert m.plan(ci, co, td, dflt).centre == 0
+    with pytest.raises(B.SpconvError) as ei:
+        km.plan(32, 32, f16, B.Options.make(centre=3))
+    assert ei.value.status == B.SPCONV_EINVAL
 
 
 @pytest.mark.parametrize("c_in", [16, 48])

@@ -545,23 +545,28 @@ struct PartVec {
   }
 };
 
-__device__ __forceinline__ void store8(__half* p, const f32x4& lo, const f32x4& hi) {
+// 8 float32 sums rounded to the layer type, as one 16-byte vector
+__device__ __forceinline__ u32x4 pack8(__half*, const f32x4& lo, const f32x4& hi) {
   f16x8 v;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     v[i] = (_Float16)lo[i];
     v[4 + i] = (_Float16)hi[i];
   }
-  *reinterpret_cast<f16x8*>(p) = v;
+  return __builtin_bit_cast(u32x4, v);
 }
-__device__ __forceinline__ void store8(__hip_bfloat16* p, const f32x4& lo, const f32x4& hi) {
+__device__ __forceinline__ u32x4 pack8(__hip_bfloat16*, const f32x4& lo, const f32x4& hi) {
   __hip_bfloat16 h[8];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     h[i] = __float2bfloat16(lo[i]);
     h[4 + i] = __float2bfloat16(hi[i]);
   }
-  *reinterpret_cast<uint4*>(p) = *reinterpret_cast<const uint4*>(h);
+  return *reinterpret_cast<const u32x4*>(h);
+}
+// the value of lane i xor 8 (within each row of 16 lanes: a DPP row rotation by 8)
+__device__ __forceinline__ uint32_t swap8(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false);
 }
 
 // T: layer type (operands and output); TP: partial type; NT = c_out / 16 (even);
@@ -602,25 +607,44 @@ __global__ __launch_bounds__(kCentreThreads) void k_scatter_centre(
   int32_t* list = reinterpret_cast<int32_t*>(smem + (size_t)BN * ldk * sizeof(T)) +
                   (wave * 16 + col) * kCentreList;
 
-  // stage W_c^T, columns permuted: LDS row n holds channel centre_phys(n)
+  // stage W_c^T, columns permuted: LDS row n holds channel centre_phys(n); a
+  // thread's 16-byte chunks are requested in batches of kStage before they are
+  // written (one at a time they would cost a round trip each)
   {
     const T* wc_t = wt ? wt + (int64_t)kc * c_out * c_in : nullptr;
     const T* wc = w + (int64_t)kc * c_in * c_out;
     constexpr int CH_T = KP / 8, CH_N = BN / 8;
     constexpr int NCHUNK = BN * KP / 8;
-    for (int idx = tid; idx < NCHUNK; idx += kCentreThreads) {
-      if (wt) {
-        const int n = idx / CH_T, c = (idx - n * CH_T) * 8;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (c < c_in) v = *reinterpret_cast<const uint4*>(wc_t + (int64_t)centre_phys(n) * c_in + c);
-        *reinterpret_cast<uint4*>(lw + n * ldk + c) = v;
-      } else {
-        const int c = idx / CH_N, n8 = (idx - c * CH_N) * 8;  // 8 physical channels of row c
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (c < c_in) v = *reinterpret_cast<const uint4*>(wc + (int64_t)c * c_out + n8);
-        const T* e = reinterpret_cast<const T*>(&v);
+    constexpr int kStage = 8;
+    for (int i0 = 0; i0 < NCHUNK; i0 += kStage * kCentreThreads) {
+      uint4 v[kStage];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) lw[centre_logical(n8 + j) * ldk + c] = e[j];
+      for (int u = 0; u < kStage; ++u) {
+        const int idx = i0 + u * kCentreThreads + tid;
+        v[u] = make_uint4(0, 0, 0, 0);
+        if (idx < NCHUNK) {
+          if (wt) {
+            const int n = idx / CH_T, c = (idx - n * CH_T) * 8;
+            if (c < c_in) v[u] = *reinterpret_cast<const uint4*>(wc_t + (int64_t)centre_phys(n) * c_in + c);
+          } else {
+            const int c = idx / CH_N, n8 = (idx - c * CH_N) * 8;  // 8 physical channels of row c
+            if (c < c_in) v[u] = *reinterpret_cast<const uint4*>(wc + (int64_t)c * c_out + n8);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kStage; ++u) {
+        const int idx = i0 + u * kCentreThreads + tid;
+        if (idx >= NCHUNK) continue;
+        if (wt) {
+          const int n = idx / CH_T, c = (idx - n * CH_T) * 8;
+          *reinterpret_cast<uint4*>(lw + n * ldk + c) = v[u];
+        } else {
+          const int c = idx / CH_N, n8 = (idx - c * CH_N) * 8;
+          const T* e = reinterpret_cast<const T*>(&v[u]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) lw[centre_logical(n8 + j) * ldk + c] = e[j];
+        }
       }
     }
   }
@@ -679,19 +703,22 @@ __global__ __launch_bounds__(kCentreThreads) void k_scatter_centre(
   uint32_t row_n;
   int32_t r_n[NM];
   fetch(blk, &row_n, r_n);
-  for (; blk < blocks; blk += bstride) {
-    const int p = blk * 16 + col;
-    const bool valid = p < n_out;
-    const int64_t row = row_n;
-    // the centre operand: this output's own input row (requested with the first
-    // partial rows; the MFMAs wait for it)
-    F a[KSTEPS];
+  // the centre operand of a block: its outputs' own input rows, requested one block
+  // ahead (right after the previous block's MFMAs, into the same registers)
+  F a[KSTEPS];
+  auto load_a = [&](int64_t row) {
     const T* arow = x + row * c_in;
 #pragma unroll
     for (int q = 0; q < KSTEPS; ++q) {
       const int kk = 32 * q + 8 * sub;
       a[q] = M::load(kk < c_in ? arow + kk : x);
     }
+  };
+  load_a(row_n);
+  for (; blk < blocks; blk += bstride) {
+    const int p = blk * 16 + col;
+    const bool valid = p < n_out;
+    const int64_t row = row_n;
     int mx;
     int cnt = build_list(r_n, &mx);
     fetch(blk + bstride, &row_n, r_n);
@@ -730,6 +757,7 @@ __global__ __launch_bounds__(kCentreThreads) void k_scatter_centre(
       if constexpr (decltype(first)::value) {
         asm volatile("" ::: "memory");
         centre();
+        load_a(row_n);  // the next block's
       }
 #pragma unroll
       for (int e = 0; e < NE; ++e)
@@ -746,9 +774,7 @@ __global__ __launch_bounds__(kCentreThreads) void k_scatter_centre(
       for (int j0 = 0; j0 < mx; j0 += ENT2) partial_round(j0, cnt, Later{});
       asm volatile("" ::: "memory");
     }
-    if (!valid) continue;
-    T* dst = y + row * (int64_t)c_out + ch0;
-    if (residual) {
+    if (residual && valid) {
       const T* rs = residual + row * (int64_t)c_out + ch0;
 #pragma unroll
       for (int u = 0; u < NU; ++u) add8<T>(acc[2 * u], acc[2 * u + 1], rs + 32 * u);
@@ -759,8 +785,37 @@ __global__ __launch_bounds__(kCentreThreads) void k_scatter_centre(
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[t][i] = fmaxf(acc[t][i], 0.f);
     }
+    if constexpr (NU % 2 == 0) {
+      // Whole 128-byte lines: a lane holds, per 64-channel line L of its row, the
+      // chunks 2L and 2L + 1 of its lane group.  Lanes of rows r and r + 8 (lanes
+      // i and i xor 8) swap one chunk, so that one store writes line L of rows 0..7
+      // (rows r < 8 their own chunk 2L, lanes of rows r + 8 the received chunk 2L + 1
+      // of row r) and the next line L of rows 8..15.  Stores of 16 rows x 64 bytes
+      // measured 30% slower than stores of whole lines.
+      const bool lower = col < 8;
+      const uint32_t row_o = swap8((uint32_t)row);
+      const int64_t row_x = lower ? row : (int64_t)row_o, row_y = lower ? (int64_t)row_o : row;
+      const bool valid_x = blk * 16 + (col & 7) < n_out, valid_y = blk * 16 + 8 + (col & 7) < n_out;
 #pragma unroll
-    for (int u = 0; u < NU; ++u) store8(dst + 32 * u, acc[2 * u], acc[2 * u + 1]);
+      for (int L = 0; L < NU / 2; ++L) {
+        const u32x4 oa = pack8((T*)nullptr, acc[4 * L], acc[4 * L + 1]);
+        const u32x4 ob = pack8((T*)nullptr, acc[4 * L + 2], acc[4 * L + 3]);
+        const u32x4 send = lower ? ob : oa;
+        u32x4 recv;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) recv[d] = swap8(send[d]);
+        const int ch = ch0 + 32 * (2 * L + (lower ? 0 : 1));
+        const u32x4 dx = lower ? oa : recv, dy = lower ? recv : ob;
+        if (valid_x) *reinterpret_cast<u32x4*>(y + row_x * (int64_t)c_out + ch) = dx;
+        if (valid_y) *reinterpret_cast<u32x4*>(y + row_y * (int64_t)c_out + ch) = dy;
+      }
+    } else {
+      if (valid) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+          *reinterpret_cast<u32x4*>(y + row * (int64_t)c_out + ch0 + 32 * u) = pack8((T*)nullptr, acc[2 * u], acc[2 * u + 1]);
+      }
+    }
   }
 }
 

@@ -212,6 +212,9 @@ __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, con
 // run.
 // ----------------------------------------------------------------------------
 constexpr int kRsItems = 8;                   // keys per thread of a one-kernel pass
+// and from kOnesweepMinTiles tiles of that many keys per thread on (4.2M keys): longer
+// runs per digit and tile for the stores (16M keys: pass 193 -> 166 us)
+constexpr int kRsItemsLarge = 16;
 constexpr int kRsTile = kThreads * kRsItems;
 constexpr int kRsItemsSmall = 4;              // keys per thread of the small sorts' passes
 constexpr int kRsTileSmall = kThreads * kRsItemsSmall;
@@ -471,13 +474,13 @@ __global__ __launch_bounds__(1024) void k_radix_totals(const uint32_t* gpart, in
   }
 }
 
-template <bool FROM_COORDS>
+template <bool FROM_COORDS, int ITEMS>
 __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, const uint32_t* vin, const int4* coords,
                                                          const KeyLayout* __restrict__ Lp, uint64_t* kout, uint32_t* vout, int64_t n,
                                                          int pass, const uint32_t* gofs, uint32_t* status,
                                                          uint32_t* tickets, uint32_t* err) {
   const KeyLayout L = *Lp;
-  __shared__ TileLds<kRsItems> t;
+  __shared__ TileLds<ITEMS> t;
   __shared__ uint32_t s_tile;
   const int tid = threadIdx.x;
   const int shift = 8 * pass;
@@ -489,13 +492,13 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
   }
   __syncthreads();
   const int64_t tile = s_tile;
-  const int64_t base = tile * kRsTile;
+  const int64_t base = tile * (kThreads * ITEMS);
 
-  uint64_t key[kRsItems];
-  uint32_t val[kRsItems];
-  uint32_t rank[kRsItems];
-  tile_load<FROM_COORDS, kRsItems>(kin, vin, coords, L, base, n, key, val);
-  tile_rank<kRsItems>(t, key, base, n, shift, rank);
+  uint64_t key[ITEMS];
+  uint32_t val[ITEMS];
+  uint32_t rank[ITEMS];
+  tile_load<FROM_COORDS, ITEMS>(kin, vin, coords, L, base, n, key, val);
+  tile_rank<ITEMS>(t, key, base, n, shift, rank);
   __syncthreads();
 
   // publish this tile's count of digit `tid` and look back over earlier tiles
@@ -543,7 +546,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_pass(const uint64_t* kin, co
   }
   t.gbase[tid] = gofs[pass * 256 + tid] + excl;
   __syncthreads();
-  tile_place<true, kRsItems>(t, key, val, rank, base, n, shift, kout, vout);
+  tile_place<true, ITEMS>(t, key, val, rank, base, n, shift, kout, vout);
 }
 
 // Small inputs (few tiles): per-tile digit histograms, then a stable scatter.
@@ -1641,9 +1644,13 @@ hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* ke
   if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
   if (n <= 1 || passes == 0) return hipSuccess;
   if (passes > kRsMaxPasses || n >= ((int64_t)1 << 30)) return hipErrorInvalidValue;
-  const int64_t ntiles = (n + kRsTile - 1) / kRsTile;
-  if (ntiles < kOnesweepMinTiles)
+  if ((n + kRsTile - 1) / kRsTile < kOnesweepMinTiles)
     return radix_sort_tiled(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, la, s);
+  // one kernel per pass, with larger tiles from kOnesweepMinTiles of them on (the
+  // status words are sized for tiles of kRsTile keys, of which there are more)
+  const bool large = (n + kThreads * kRsItemsLarge - 1) / (kThreads * kRsItemsLarge) >= kOnesweepMinTiles;
+  const int64_t tile_keys = (int64_t)kThreads * (large ? kRsItemsLarge : kRsItems);
+  const int64_t ntiles = (n + tile_keys - 1) / tile_keys;
   const size_t gpart_bytes = (size_t)kRsUpBlocks * kRsMaxPasses * 256 * sizeof(uint32_t);
   uint32_t* gpart = static_cast<uint32_t*>(d_temp);
   uint32_t* gofs = reinterpret_cast<uint32_t*>(static_cast<char*>(d_temp) + align256(gpart_bytes));
@@ -1688,12 +1695,18 @@ hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* ke
     const int src = cur, dst = (first ? ((passes % 2 == 1) ? 0 : 1) : cur ^ 1);
     {
       ProfScope ps(KN_RADIX_SCATTER, s);
-      if (first)
-        hipLaunchKernelGGL(k_radix_pass<true>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr, nullptr, c4, L,
-                           kb[dst], vb[dst], n, p, gofs, status, tickets, err);
+      if (first && large)
+        hipLaunchKernelGGL((k_radix_pass<true, kRsItemsLarge>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr,
+                           nullptr, c4, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
+      else if (first)
+        hipLaunchKernelGGL((k_radix_pass<true, kRsItems>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr,
+                           nullptr, c4, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
+      else if (large)
+        hipLaunchKernelGGL((k_radix_pass<false, kRsItemsLarge>), dim3((unsigned)ntiles), dim3(kThreads), 0, s,
+                           kb[src], vb[src], nullptr, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
       else
-        hipLaunchKernelGGL(k_radix_pass<false>, dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src], vb[src],
-                           nullptr, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
+        hipLaunchKernelGGL((k_radix_pass<false, kRsItems>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src],
+                           vb[src], nullptr, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

@@ -498,6 +498,16 @@ def test_large_cloud_one_kernel_sort_passes():
     assert np.array_equal(qd.out_coords().cpu().numpy(), q)
 
 
+def test_larger_cloud_one_kernel_sort_passes_with_larger_tiles():
+    """4.5M voxels: past 1024 tiles of 4096 keys, so the one-kernel passes take 16
+    keys per thread; K = 2 keeps the oracle's map fast."""
+    say("large uniform cloud, 4.5M voxels")
+    c = scenes.uniform_cells_large(4_500_000, 480, 4343)
+    km = B.KernelMap.build(to_dev(c), 2)
+    okm = oracle.kernel_map(c, None, 2, 1, "subm")
+    assert_map_equal(km, okm)
+
+
 def test_mid_cloud_scanned_sort_offsets():
     """1M voxels: 489 radix tiles, between the per-workgroup offset sums and the
     one-kernel passes, so each pass scans the digit-major histograms on the device.

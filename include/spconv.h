@@ -170,17 +170,21 @@ int spconv_build_map(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_
  * device work.  The result borrows `down`'s device arrays: free it before `down`. */
 int spconv_map_transpose(const spconv_map* down, spconv_map** out_map);
 
+/* Sizes of the map: |P| input and |Q| output points (Section 2.1), and the number
+ * of offsets of the stencil Delta(K, t), K^3 (Section 2.1). */
 int64_t spconv_map_n_in(const spconv_map* m);
 int64_t spconv_map_n_out(const spconv_map* m);
 int spconv_map_kvol(const spconv_map* m); /* K^3 */
-/* Device pointer to the [n_out][4] output coordinates: SPCONV_DOWN's sorted Q,
- * SPCONV_SUBM's inputs, SPCONV_UP's given fine coordinates. */
+/* Device pointer to the [n_out][4] output coordinates Q: SPCONV_DOWN's sorted Q of
+ * Eq. 1, SPCONV_SUBM's inputs (Q = P), SPCONV_UP's given fine coordinates. */
 const int32_t* spconv_map_out_coords(const spconv_map* m);
-/* h_counts[k] = |M_k| for k in [0, K^3). */
+/* h_counts[k] = |M_k| for k in [0, K^3): the size of offset k's part of the kernel
+ * map M of Eq. 3 (Section 2.2, Step 1), from the host copy (no device work). */
 int spconv_map_counts(const spconv_map* m, int64_t* h_counts);
-/* Device pointers to offset k's pairs: (*d_in_idx)[e] meets (*d_out_idx)[e] through
- * W_k, e in [0, *count).  Order inside one offset: ascending sorted query position
- * (caller-row order for maps built with the hash-table search). */
+/* Device pointers to offset k's pairs, M_k of Eq. 3 (Section 2.2, Step 1):
+ * (*d_in_idx)[e] meets (*d_out_idx)[e] through W_k, e in [0, *count).  Order inside
+ * one offset: ascending sorted query position (caller-row order for maps built with
+ * the hash-table search).  The pointers stay valid until the map is freed. */
 int spconv_map_pairs(const spconv_map* m, int k, const int32_t** d_in_idx,
                      const int32_t** d_out_idx, int64_t* count);
 /* Stream-ordered copies into caller buffers: all pairs, offset-major (offset k's

@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
                                                             const T* __restrict__ w, const T* __restrict__ wt,
                                                             TO* __restrict__ C,
                                                             TO* __restrict__ dump, int c_in, int c_out, int ldk,
-                                                            int rows_per_tile) {
+                                                            int rows_per_tile, int nsl) {
   using M = Mfma<T>;
   using F = typename M::frag;
   static_assert(M::KS == 32, "16-bit operands only");
@@ -235,14 +235,26 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
   const int wave = tid / kWave;
   const int cg = wave % CG, rg = wave / CG;
 
+  // With nsl > 1 column slices per tile, the grid is one-dimensional and the
+  // slices of a tile take workgroup ids 8 apart: workgroups go to the eight dies
+  // in turn, so the slices of a tile run on one die at about the same time and
+  // share its L2 for the tile's input rows (slice-major, every input row would be
+  // read from memory once per slice).
+  int bx = (int)blockIdx.x, by = (int)blockIdx.y;
+  if (nsl > 1) {
+    const int grp = bx / (8 * nsl), r = bx - grp * (8 * nsl);
+    by = r / 8;
+    bx = grp * 8 + (r - by * 8);
+    if (bx >= g.tile_start[g.n_seg]) return;  // the last group's missing tiles (workgroup-uniform)
+  }
   int s = 0;
-  while (s + 1 < g.n_seg && g.tile_start[s + 1] <= (int)blockIdx.x) ++s;
+  while (s + 1 < g.n_seg && g.tile_start[s + 1] <= bx) ++s;
   const int k = g.k[s];
   const int64_t row0 = g.row0[s];
   const int rows = g.rows[s];
   const int height = g.height[s];
-  const int tile = (int)blockIdx.x - g.tile_start[s];
-  const int n0 = blockIdx.y * BN;
+  const int tile = bx - g.tile_start[s];
+  const int n0 = by * BN;
 
   const int r_begin = tile * rows_per_tile;
   const int r_end = min(r_begin + rows_per_tile, height);
@@ -1073,14 +1085,15 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
     hipError_t e = hipErrorInvalidValue;
     if (wide) {
       ProfScope ps(KN_GEMM, s);
-      const dim3 grid((unsigned)tiles, (unsigned)(c_out / 16 / nt));
+      int nsl = c_out / 16 / nt;  // column slices per tile
+      const dim3 grid = nsl > 1 ? dim3((unsigned)((tiles + 7) / 8 * 8 * nsl)) : dim3((unsigned)tiles);
       const void* a = buf_in;
       const void* wtp = wt;
       void* c = buf_out;
       void* d = dump_row;
       const void* wp = w;
       const int32_t* ar = a_rows;
-      void* args[] = {&g, &a, &ar, &wp, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile};
+      void* args[] = {&g, &a, &ar, &wp, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile, &nsl};
       e = hipLaunchKernel(wfn, grid, dim3(kWideThreads), args, lds, s);
     } else if (dtype == 0 && part_dtype == 0)
       e = gemm_t<float, float>(g, tiles, buf_in, a_rows, w, buf_out, c_in, c_out, rows_per_tile, s);

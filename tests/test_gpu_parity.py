@@ -340,6 +340,8 @@ def test_row_scatter_matches_tiled_and_oracle(K, c_out, pd):
     ("bf16", 64, 32, 1),    # fallback kernel, bf16
     ("bf16", 96, 32, 0),
     ("f16", 256, 128, 0),   # W^T staged from the transposed copy
+    ("f16", 384, 256, 0),   # two column slices per tile, their workgroups 8 ids apart
+    ("f16", 512, 256, 1),   # the same with float32 partials
 ])
 def test_gather_forms_bit_identical(dtype, c_in, c_out, pd):
     """GEMMs that load each pair's input row directly (the fused gather) see the

@@ -1027,6 +1027,10 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
 // ROUNDS reads of a step are issued together.  pos = number of keys < key (at
 // most 2^LOG2B - 1; then the final probe tells a hit from a key past the block),
 // hit = whether the key is present.
+// a value that every lane of the wave holds alike (say, read from LDS), in a
+// scalar register, so that loops and branches on it stay scalar
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 template <int ROUNDS, int LOG2B>
 __device__ __forceinline__ void lds_search(const uint64_t* lkey, const uint64_t (&key)[ROUNDS], int (&pos)[ROUNDS],
                                            bool (&hit)[ROUNDS]) {
@@ -1045,6 +1049,10 @@ __device__ __forceinline__ void lds_search(const uint64_t* lkey, const uint64_t 
   uint64_t v[ROUNDS];
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) v[r] = *reinterpret_cast<const uint64_t*>(base + off[r]);
+  // every chain ends here, in every lane: a caller's use of a result under a lane
+  // mask must not move that chain into the masked branch, after the others
+#pragma unroll
+  for (int r = 0; r < ROUNDS; ++r) asm volatile("" ::"v"(v[r]), "v"(off[r]));
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
     hit[r] = v[r] == key[r];
@@ -1158,20 +1166,29 @@ __global__ __launch_bounds__(TH) void k_forward_write(SearchArgs a, const uint32
 }
 
 // Forward search, count pass, with source-block reuse: one workgroup per
-// (source block b, group of G offsets) stages block b in LDS once and then runs
-// the query block of (k, b) for every offset k of its group, in chunks of at
-// most Cq queries (the balancing step).  Each query's result goes to T_q, and
-// each (k, b) work item's match count to item_cnt[k nb + b].
+// (source block b, group of at most 64 offsets) stages block b in LDS once and
+// then searches the query block of (k, b) for every offset k of its group, in
+// chunks of at most Cq queries (the balancing step).  Each query's result goes to
+// T_q, and each (k, b) work item's match count to item_cnt[k nb + b].
 // With few source blocks the groups are small, so that the grid still fills the
-// GPU; with many, one workgroup takes all K^3 offsets of its block and reads it
-// from HBM once instead of K^3 times.  The block's keys, the first chunk's query
-// keys and its bounds are all requested before the first wait; each chunk's
-// ROUNDS searches run as independent chains.
+// GPU; with many, one workgroup takes several offsets of its block and reads the
+// block from HBM once instead of once per offset.  The query blocks of offsets
+// that differ only in y or z nearly coincide (their key deltas are below one
+// x-slab), so consecutive offsets whose blocks together span little more than
+// the largest of them form a run: each chunk of the run's span is read once and
+// searched for every offset of the run, each lane keeping only the queries inside
+// that offset's own block (read per offset, these keys missed L2 once the cloud
+// outgrew it).  Match counts are kept per wave (lane j counts the group's offset
+// j), so the chunks need no workgroup barrier.  The block's keys, the group's
+// query bounds and, for a lone offset, the keys of its first chunk are all
+// requested before the first wait; each chunk's ROUNDS searches run as
+// independent chains.
 template <int ROUNDS, int LOG2B, int TH>
 __global__ __launch_bounds__(TH) void k_forward_count(SearchArgs a, const uint32_t* bounds, int64_t nb,
                                                             uint32_t* item_cnt, int G, ControlBlock* cb) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ uint32_t s_cnt[ROUNDS][(TH / kWave)];
+  __shared__ int32_t s_lo[kWave], s_hi[kWave];   // query block of the group's offset j
+  __shared__ uint32_t s_tot[TH / kWave][kWave];  // matches of offset j found by each wave
   uint64_t* lkey = reinterpret_cast<uint64_t*>(smem);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -1182,40 +1199,45 @@ __global__ __launch_bounds__(TH) void k_forward_count(SearchArgs a, const uint32
 
   const int64_t s0 = b * (int64_t)a.B;
   const int nB = (int)min((int64_t)a.B, a.n_src - s0);
-  // Requested together before the first wait: the block's first 4 * TH keys,
-  // the key before the block (repeat check), the first offset's bounds and the
-  // keys of its first chunk.
+  const int k_first = g * G;
+  const int nk = min(a.K3 - k_first, G);  // 1 .. 64 (the host caps G)
+  auto block_of = [&](int j, int64_t* lo, int64_t* hi) {
+    const int64_t kb = (int64_t)(k_first + j) * nb + b;
+    *hi = bounds[kb];
+    // min(): keys out of order can invert the bounds (the block then has no queries)
+    *lo = (b == 0) ? 0 : min((int64_t)bounds[kb - 1], *hi);
+  };
   uint64_t sv[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) sv[u] = a.skeys[s0 + min(u * TH + tid, nB - 1)];
   const uint64_t key_before = a.skeys[s0 > 0 ? s0 - 1 : 0];
-  const int k_first = g * G;
-  const int k_end = min(a.K3, k_first + G);
-  int64_t q_lo = 0, q_hi = 0;
-  uint32_t nch = 0;
-  auto load_bounds = [&](int k) {
-    const int64_t kb = (int64_t)k * nb + b;
-    q_hi = bounds[kb];
-    // min(): keys out of order can invert the bounds (the block then has no queries)
-    q_lo = (b == 0) ? 0 : min((int64_t)bounds[kb - 1], q_hi);
-    nch = (uint32_t)((q_hi - q_lo + a.Cq - 1) / a.Cq);
-  };
-  uint64_t key[ROUNDS];
-  // keys of the chunk [q0, q1) (lanes past q1 re-read the first key)
-  auto load_keys = [&](int64_t q0, int64_t q1, uint64_t dk) {
+  int64_t my_lo = 0, my_hi = 0;
+  if (tid < nk) block_of(tid, &my_lo, &my_hi);
+  uint64_t qk[ROUNDS];  // the current chunk's query keys (lanes past its end re-read its first key)
+  auto load_keys = [&](int64_t q0, int64_t q1) {
+    const uint64_t* qb = a.qkeys + q0;
+    const int n = (int)(q1 - q0);
 #pragma unroll
-    for (int r = 0; r < ROUNDS; ++r) {
-      const int64_t qp = q0 + (int64_t)r * TH + tid;
-      key[r] = a.qkeys[qp < q1 ? qp : 0] + dk;
-    }
+    for (int r = 0; r < ROUNDS; ++r) qk[r] = qb[r * TH + tid < n ? r * TH + tid : 0];
   };
-  load_bounds(k_first);
-  if (nch > 0) load_keys(q_lo, min(q_lo + (int64_t)a.Cq, q_hi), (uint64_t)a.dk[k_first]);
+  int64_t pre_lo = -1;  // first query of the chunk already in qk, if any
+  if (nk == 1) {
+    int64_t lo, hi;
+    block_of(0, &lo, &hi);
+    if (lo < hi) {
+      load_keys(lo, min(lo + (int64_t)a.Cq, hi));
+      pre_lo = lo;
+    }
+  }
 #pragma unroll
   for (int u = 0; u < 4; ++u)
     if (u * TH + tid < nB) lkey[u * TH + tid] = sv[u];
   for (int e = 4 * TH + tid; e < nB; e += TH) lkey[e] = a.skeys[s0 + e];  // B > 4 * TH
   for (int e = nB + tid; e <= (1 << LOG2B); e += TH) lkey[e] = ~0ull;   // padding
+  if (tid < nk) {  // (query positions fit 31 bits: the bounds are 32-bit)
+    s_lo[tid] = (int32_t)my_lo;
+    s_hi[tid] = (int32_t)my_hi;
+  }
   __syncthreads();
   if (g == 0) {
     // the sorted source keys must be strictly increasing: equal neighbours are
@@ -1232,36 +1254,67 @@ __global__ __launch_bounds__(TH) void k_forward_count(SearchArgs a, const uint32
     if (__ballot(unsorted) != 0 && lane == 0) atomicOr(&cb->err, kErrUnsorted);
   }
 
-  for (int k = k_first; k < k_end; ++k) {
-    if (k != k_first) load_bounds(k);
-    int32_t* res = a.res + (int64_t)k * a.res_stride;
-    const uint64_t dk = (uint64_t)a.dk[k];
-    uint32_t item_total = 0;  // thread 0's sum over the chunks
-    for (uint32_t c = 0; c < nch; ++c) {
-      const int64_t q0 = min(q_lo + (int64_t)c * a.Cq, q_hi);
-      const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
-      if (k != k_first || c != 0) load_keys(q0, q1, dk);
-      int pos[ROUNDS];
-      bool hit[ROUNDS];
-      lds_search<ROUNDS, LOG2B>(lkey, key, pos, hit);
-#pragma unroll
-      for (int r = 0; r < ROUNDS; ++r) {
-        const int64_t qp = q0 + (int64_t)r * TH + tid;
-        const bool valid = qp < q1;
-        if (valid) res[qp] = hit[r] ? (int32_t)(s0 + pos[r]) : -1;
-        const uint64_t bal = __ballot(valid && hit[r]);
-        if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal);
+  uint32_t tot = 0;  // lane j: this wave's matches of offset k_first + j
+  for (int j = 0; j < nk;) {  // workgroup-uniform
+    // the run j .. je - 1: its blocks span [u_lo, u_hi), at most 1/8 (+ 64 queries)
+    // more than the largest of them; empty blocks join any run
+    int u_lo = uniform(s_lo[j]), u_hi = uniform(s_hi[j]), mx = u_hi - u_lo;
+    int je = j + 1;
+    for (; je < nk; ++je) {
+      const int lo = uniform(s_lo[je]), hi = uniform(s_hi[je]);
+      if (lo >= hi) continue;
+      if (u_lo >= u_hi) {
+        u_lo = lo;
+        u_hi = hi;
+        mx = hi - lo;
+        continue;
       }
-      __syncthreads();
-      if (tid == 0) {
-#pragma unroll
-        for (int r = 0; r < ROUNDS; ++r)
-#pragma unroll
-          for (int v = 0; v < (TH / kWave); ++v) item_total += s_cnt[r][v];
-      }
-      __syncthreads();  // s_cnt is rewritten by the next chunk
+      const int nlo = min(u_lo, lo), nhi = max(u_hi, hi), nmx = max(mx, hi - lo);
+      if (nhi - nlo > nmx + nmx / 8 + 64) break;
+      u_lo = nlo;
+      u_hi = nhi;
+      mx = nmx;
     }
-    if (tid == 0) item_cnt[(int64_t)k * nb + b] = item_total;
+    for (int q0 = u_lo; q0 < u_hi; q0 += a.Cq) {
+      const int q1 = min(q0 + a.Cq, u_hi);
+      if (q0 != pre_lo) load_keys(q0, q1);
+      pre_lo = -1;
+      for (int jj = j; jj < je; ++jj) {
+        const int lo = uniform(s_lo[jj]), hi = uniform(s_hi[jj]);
+        if (q1 <= lo || q0 >= hi) continue;  // the chunk misses this offset's block
+        // the chunk's part of the block, relative to q0
+        const int r_lo = max(lo, q0) - q0, r_hi = min(hi, q1) - q0;
+        int32_t* res = a.res + (int64_t)(k_first + jj) * a.res_stride + q0;
+        const uint64_t dk = (uint64_t)a.dk[k_first + jj];
+        // the shifted keys take the raw keys' registers and give them back after
+        // the search (modular arithmetic: exact)
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) qk[r] += dk;
+        int pos[ROUNDS];
+        bool hit[ROUNDS];
+        lds_search<ROUNDS, LOG2B>(lkey, qk, pos, hit);
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) qk[r] -= dk;
+        uint32_t nh = 0;
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) {
+          const int e = r * TH + tid;
+          const bool valid = e >= r_lo && e < r_hi;
+          if (valid) res[e] = hit[r] ? (int32_t)(s0 + pos[r]) : -1;
+          nh += (uint32_t)popc64(__ballot(valid && hit[r]));
+        }
+        if (lane == jj) tot += nh;
+      }
+    }
+    j = je;
+  }
+  s_tot[wave][lane] = tot;
+  __syncthreads();
+  if (tid < nk) {
+    uint32_t sum = 0;
+#pragma unroll
+    for (int v = 0; v < TH / kWave; ++v) sum += s_tot[v][tid];
+    item_cnt[(int64_t)(k_first + tid) * nb + b] = sum;
   }
 }
 
@@ -1772,7 +1825,8 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
     return hipErrorInvalidValue;
   }
   const int64_t ngroups0 = std::min<int64_t>(a.K3, std::max<int64_t>(1, (kCountTargetGroups + nb - 1) / nb));
-  const int G = (int)((a.K3 + ngroups0 - 1) / ngroups0);
+  // (at most 64 offsets per group: the kernel counts an offset's matches in one lane)
+  const int G = std::min<int>(kWave, (int)((a.K3 + ngroups0 - 1) / ngroups0));
   const int64_t ngroups = (a.K3 + G - 1) / G;
   const unsigned grid = (unsigned)(nb * ngroups);
   ProfScope ps(KN_FORWARD_COUNT, s);

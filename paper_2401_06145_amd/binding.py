@@ -46,7 +46,7 @@ class Options(ctypes.Structure):
                 ("t_scatter", ctypes.c_int), ("grouping", ctypes.c_int), ("partial_dtype", ctypes.c_int),
                 ("launch_cost_rows", ctypes.c_int), ("presorted", ctypes.c_int), ("search", ctypes.c_int),
                 ("gather", ctypes.c_int), ("wg", ctypes.c_int), ("gemm_tile_rows", ctypes.c_int),
-                ("centre", ctypes.c_int), ("reserved", ctypes.c_int * 3)]
+                ("centre", ctypes.c_int), ("count_group", ctypes.c_int), ("reserved", ctypes.c_int * 2)]
 
     @classmethod
     def make(cls, **kw) -> "Options":

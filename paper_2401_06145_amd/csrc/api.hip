@@ -241,6 +241,7 @@ struct Tunables {
   int B = 1024;
   int Cq = 1024;
   int wg = 256;
+  int count_group = 0;  // offsets per count-pass workgroup (0: size rule)
   bool presorted = false;
   bool hash = false;  // hash-table search instead of the sorted-array search
 };
@@ -283,6 +284,8 @@ int read_tunables(const spconv_options* opt, Tunables* t) {
     if (t->Cq % t->wg != 0 || !(r == 1 || r == 2 || r == 4 || r == 8))
       return fail(SPCONV_EINVAL, "Cq / wg must be 1, 2, 4 or 8");
   }
+  if (opt->count_group < 0 || opt->count_group > 64) return fail(SPCONV_EINVAL, "count_group must be in [0, 64]");
+  t->count_group = opt->count_group;
   t->presorted = opt->presorted != 0;
   if (opt->search < 0 || opt->search > 1) return fail(SPCONV_EINVAL, "search must be 0 or 1");
   t->hash = opt->search == 1;
@@ -667,6 +670,7 @@ int build_map_impl(const int32_t* d_in_coords, int64_t n_in, const int32_t* d_ou
   a.B = tu.B;
   a.Cq = tu.Cq;
   a.wg = tu.wg;
+  a.count_group = tu.count_group;
   a.swap_roles = (mode == SPCONV_UP) ? 1 : 0;
   a.check_q = (mode == SPCONV_UP) ? 1 : 0;
   a.res = b.res;

@@ -1800,7 +1800,7 @@ hipError_t launch_backward(const SearchArgs& a, int64_t nb, uint32_t* bounds, Co
 }
 
 // Workgroups the count pass aims for when choosing its offset groups.
-constexpr int64_t kCountTargetGroups = 8192;
+constexpr int64_t kCountTargetGroups = 4096;
 
 hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bounds, int64_t nb, uint32_t* item_cnt,
                           const uint32_t* item_off, int32_t* pin, int32_t* pout, ControlBlock* cb, hipStream_t s) {
@@ -1826,7 +1826,8 @@ hipError_t launch_forward(const SearchArgs& a, bool write, const uint32_t* bound
   }
   const int64_t ngroups0 = std::min<int64_t>(a.K3, std::max<int64_t>(1, (kCountTargetGroups + nb - 1) / nb));
   // (at most 64 offsets per group: the kernel counts an offset's matches in one lane)
-  const int G = std::min<int>(kWave, (int)((a.K3 + ngroups0 - 1) / ngroups0));
+  const int G = std::min<int>(std::min(kWave, a.K3),
+                              a.count_group > 0 ? a.count_group : (int)((a.K3 + ngroups0 - 1) / ngroups0));
   const int64_t ngroups = (a.K3 + G - 1) / G;
   const unsigned grid = (unsigned)(nb * ngroups);
   ProfScope ps(KN_FORWARD_COUNT, s);

@@ -45,6 +45,10 @@ def test_workspace_bytes_host_only():
     assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(wg=128, Cq=2048)) == 0
     assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(wg=512, Cq=1024)) > 0
     assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(search=2)) == 0
+    # offsets per count-pass workgroup: 0 (size rule) to 64
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(count_group=65)) == 0
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(count_group=-1)) == 0
+    assert B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(count_group=64)) > 0
     # the hash-table search adds its table (2^11 slots of 12 bytes for 1000 inputs)
     hashed = B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM, B.Options.make(search=1))
     assert hashed >= B.spconv_map_workspace_bytes(1000, 0, 3, B.SPCONV_SUBM) + 2048 * 12

@@ -73,6 +73,28 @@ def test_search_workgroup_sizes(wg, Cq):
     assert_map_equal(kd, oracle.kernel_map(c, q, 2, 1, "down"))
 
 
+@pytest.mark.parametrize("G", [2, 3, 9, 27, 64])
+def test_count_pass_offset_groups(G):
+    """Offsets per count-pass workgroup change only the launch shape.  Groups of
+    several offsets search runs of nearby query blocks together (runs split where
+    the x offset changes, blocks empty for some offsets): the maps equal the
+    oracle's, SUBM with K = 3 and 5 (K^3 = 125: groups capped at 64), DOWN and UP."""
+    say(f"count-pass offset groups G={G}")
+    c = _cloud(61, 5000, -11, 11)
+    opt = B.Options.make(B=64, Cq=256, count_group=G)
+    for K in (3, 5):
+        km = B.KernelMap.build(to_dev(c), K, opt=opt)
+        assert_map_equal(km, oracle.kernel_map(c, None, K, 1, "subm"))
+    # a sparse cloud: many source blocks see no queries at some offsets
+    sp = _cloud(62, 1500, -40, 40)
+    assert_map_equal(B.KernelMap.build(to_dev(sp), 3, opt=opt), oracle.kernel_map(sp, None, 3, 1, "subm"))
+    kd = B.KernelMap.build(to_dev(c), 2, 2, 1, "down", opt=opt)
+    q = oracle.out_coords(c, 2, 1)
+    assert_map_equal(kd, oracle.kernel_map(c, q, 2, 1, "down"))
+    ku = B.KernelMap.build(to_dev(q), 3, 2, 1, "up", to_dev(c), opt)
+    assert_map_equal(ku, oracle.kernel_map(q, c, 3, 1, "up"))
+
+
 @pytest.mark.parametrize("c", [64, 256])
 def test_gemm_tile_rows_result_neutral(c):
     """Rows per GEMM workgroup tile change the launch shape only: bit-identical output."""

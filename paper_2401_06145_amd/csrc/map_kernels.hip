@@ -1067,12 +1067,13 @@ __device__ __forceinline__ void lds_search(const uint64_t* lkey, const uint64_t 
 // offset onward, chunk after chunk, so every offset's pairs come out in
 // sorted-query order, and pair index o (the pair's GEMM buffer row) replaces the
 // source position in T_q and is stored in T_s.  The loads of all rounds of a
-// chunk are issued together: results first, then the rows of the matches.
+// chunk are issued together: results first, then the rows of the matches, and
+// the next chunk's results before the chunk's barrier.
 template <int ROUNDS, int TH>
 __global__ __launch_bounds__(TH) void k_forward_write(SearchArgs a, const uint32_t* bounds, int64_t nb,
                                                             const uint32_t* item_off, int32_t* pin, int32_t* pout,
                                                             ControlBlock* cb) {
-  __shared__ uint32_t s_cnt[ROUNDS][(TH / kWave)];
+  __shared__ uint32_t s_cnt[2][ROUNDS][(TH / kWave)];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
@@ -1112,14 +1113,20 @@ __global__ __launch_bounds__(TH) void k_forward_write(SearchArgs a, const uint32
   int32_t* res = a.res + (int64_t)k * a.res_stride;
   int32_t* ts = a.ts + (int64_t)k * a.ts_stride;
   uint64_t base = base0;
-  for (int64_t q0 = q_lo; q0 < q_hi; q0 += a.Cq) {  // workgroup-uniform
+  // a chunk's count pass results; the next chunk's are requested while this one's
+  // rows are in flight
+  int32_t sp[ROUNDS];
+  auto load_res = [&](int64_t q0, int32_t* v) {
     const int64_t q1 = min(q0 + (int64_t)a.Cq, q_hi);
-    int32_t sp[ROUNDS];
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) {
       const int64_t qp = q0 + (int64_t)r * TH + tid;
-      sp[r] = (qp < q1) ? res[qp] : -1;
+      v[r] = (qp < q1) ? res[qp] : -1;
     }
+  };
+  if (q_lo < q_hi) load_res(q_lo, sp);
+  int par = 0;  // s_cnt buffer of this chunk: two, so one barrier per chunk suffices
+  for (int64_t q0 = q_lo; q0 < q_hi; q0 += a.Cq) {  // workgroup-uniform
     int32_t r_in[ROUNDS], r_out[ROUNDS];
     uint64_t bal[ROUNDS];
 #pragma unroll
@@ -1132,8 +1139,12 @@ __global__ __launch_bounds__(TH) void k_forward_write(SearchArgs a, const uint32
       r_in[r] = a.swap_roles ? qry : src;
       r_out[r] = a.swap_roles ? src : qry;
       bal[r] = __ballot(hit);
-      if (lane == 0) s_cnt[r][wave] = (uint32_t)popc64(bal[r]);
+      if (lane == 0) s_cnt[par][r][wave] = (uint32_t)popc64(bal[r]);
     }
+    int32_t sp_next[ROUNDS];
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) sp_next[r] = -1;
+    if (q0 + a.Cq < q_hi) load_res(q0 + a.Cq, sp_next);
     __syncthreads();
     uint32_t total = 0;
     uint32_t before[ROUNDS];
@@ -1142,7 +1153,7 @@ __global__ __launch_bounds__(TH) void k_forward_write(SearchArgs a, const uint32
 #pragma unroll
       for (int v = 0; v < (TH / kWave); ++v) {
         if (v == wave) before[r] = total;
-        total += s_cnt[r][v];
+        total += s_cnt[par][r][v];
       }
     }
 #pragma unroll
@@ -1161,7 +1172,11 @@ __global__ __launch_bounds__(TH) void k_forward_write(SearchArgs a, const uint32
       }
     }
     base += total;
-    __syncthreads();  // s_cnt is rewritten by the next chunk
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) sp[r] = sp_next[r];
+    // a wave reuses this chunk's s_cnt buffer two chunks on, past the next chunk's
+    // barrier, which every wave reaches only after reading it
+    par ^= 1;
   }
 }
 

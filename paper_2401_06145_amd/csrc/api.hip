@@ -397,6 +397,13 @@ std::vector<int> dp_groups(const std::vector<int>& order, const std::vector<int6
   return cuts;
 }
 
+// Large regions that the forward writes once and a later kernel reads once (the
+// GEMM partial rows, the layer's output rows) go out with non-temporal stores.
+// Otherwise their dirty lines stay in the caches, and the next kernels' traffic has to
+// write them back.
+constexpr int64_t kStreamPartialBytes = (int64_t)128 << 20;
+constexpr int64_t kStreamOutputBytes = (int64_t)64 << 20;
+
 int make_plan(const spconv_map* m, int c_in, int c_out, int dtype, const spconv_options* opt, GmasPlan* p) {
   if (!m) return fail(SPCONV_EINVAL, "map is NULL");
   if (dtype != SPCONV_F32 && dtype != SPCONV_F16 && dtype != SPCONV_BF16) return fail(SPCONV_EUNSUPPORTED, "dtype");
@@ -971,22 +978,24 @@ int forward_impl(const spconv_map* m, const void* d_x, const void* d_w, void* d_
       // fused: the A rows are the input rows of the pairs (pair r reads x[pin[r]])
       const void* a_src = fused ? d_x : b.buf_in;
       const int32_t* a_rows = fused ? m->pin : nullptr;
+      const bool stream = (int64_t)p.rows_pairs * c_out * p.pelem >= kStreamPartialBytes;
       for (const auto& segs : p.launches)
         SPC_TRY(launch_gemm(segs.data(), (int)segs.size(), a_src, a_rows, d_w, b.wt, b.buf_out,
                             static_cast<char*>(b.buf_out) + (size_t)p.rows_pairs * c_out * p.pelem, c_in, c_out,
-                            dtype, p.part_dtype, p.gemm_tile_rows, s),
+                            dtype, p.part_dtype, p.gemm_tile_rows, stream, s),
                 "grouped GEMM");
     }
   }
   {
     PhaseScope ph(PH_SCATTER, s);
+    const bool stream = m->n_out * c_out * p.elem >= kStreamOutputBytes;
     if (p.centre_k >= 0)
       SPC_TRY(launch_scatter_centre(d_x, m->out_perm, d_w, b.wt, p.centre_k, b.buf_out, m->omt, m->omt_stride, K3,
-                                    d_y, d_residual, relu, m->n_out, c_in, c_out, dtype, p.part_dtype, s),
+                                    d_y, d_residual, relu, m->n_out, c_in, c_out, dtype, p.part_dtype, stream, s),
               "scatter with the centre offset");
     else
       SPC_TRY(launch_scatter(b.buf_out, p.part_dtype, m->n_out, c_out, m->omt, m->omt_stride, m->out_perm, K3, d_y,
-                             dtype, p.t_scatter, d_residual, relu, s),
+                             dtype, p.t_scatter, d_residual, relu, stream, s),
               "scatter");
   }
   return SPCONV_OK;

@@ -47,6 +47,18 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 
 __device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
 
+// Stores of rows that no kernel reads again soon (GEMM partial rows, layer outputs):
+// non-temporal, so they stream to memory instead of leaving dirty lines in the
+// caches that later kernels' traffic would have to write back.
+__device__ __forceinline__ void store_stream(void* p, uint4 v) {
+  typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(v4u{v.x, v.y, v.z, v.w}, reinterpret_cast<v4u*>(p));
+}
+__device__ __forceinline__ void store_stream(void* p, uint2 v) {
+  typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+  __builtin_nontemporal_store(v2u{v.x, v.y}, reinterpret_cast<v2u*>(p));
+}
+
 // ---------------------------------------------------------------------------
 // Device error flags, OR-ed into ControlBlock::err by kernels.
 // ---------------------------------------------------------------------------
@@ -231,9 +243,10 @@ hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const 
                          hipStream_t s);
 // Scatter: y[perm[p]] = sum_k buf_out[omt[k][p]] (float32 sum, k ascending), tile T
 // channels per thread.  Optional epilogue: y = relu?(sum + residual) (residual NULL: none).
+// stream: the output rows go out with non-temporal stores (store_stream).
 hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out,
                           const int32_t* omt, int64_t mt_stride, const uint32_t* perm, int K3, void* y,
-                          int dtype, int tile, const void* residual, int relu, hipStream_t s);
+                          int dtype, int tile, const void* residual, int relu, bool stream, hipStream_t s);
 // out[i] = [a[i] | b[i]] for row-major a [n][ca], b [n][cb] (16-byte multiples).
 hipError_t launch_concat(const void* a, int ca, const void* b, int cb, void* out, int64_t n, int elem,
                          hipStream_t s);
@@ -260,9 +273,10 @@ hipError_t launch_transpose_w(const void* w, void* wt, int K3, int c_in, int c_o
 // wt: transposed weights (launch_transpose_w) or NULL;
 // dump_row: one spare row of c_out partials the full-width kernel may overwrite.
 // tile_rows: output rows per workgroup tile (0: about two tiles per workgroup slot)
+// stream: the full-width kernel writes the partial rows with non-temporal stores.
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
                        const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
-                       int tile_rows, hipStream_t s);
+                       int tile_rows, bool stream, hipStream_t s);
 // The submanifold centre offset computed inside the scatter (odd K): y[perm[p]] =
 // relu?(x[perm[p]] W_kc + sum over k != kc of buf_out[omt[k][p]] + residual), the
 // centre first, then k ascending, in float32.  Whether an instance exists for the
@@ -272,6 +286,6 @@ bool centre_fusable(int c_in, int c_out, int dtype, int part_dtype);
 hipError_t launch_scatter_centre(const void* x, const uint32_t* perm, const void* w, const void* wt, int kc,
                                  const void* buf_out, const int32_t* omt, int64_t mt_stride, int K3, void* y,
                                  const void* residual, int relu, int64_t n_out, int c_in, int c_out, int dtype,
-                                 int part_dtype, hipStream_t s);
+                                 int part_dtype, bool stream, hipStream_t s);
 
 }  // namespace spc

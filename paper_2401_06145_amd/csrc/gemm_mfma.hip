@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
                                                             const T* __restrict__ w, const T* __restrict__ wt,
                                                             TO* __restrict__ C,
                                                             TO* __restrict__ dump, int c_in, int c_out, int ldk,
-                                                            int rows_per_tile, int nsl) {
+                                                            int rows_per_tile, int nsl, int stream) {
   using M = Mfma<T>;
   using F = typename M::frag;
   static_assert(M::KS == 32, "16-bit operands only");
@@ -442,7 +442,12 @@ __global__ __launch_bounds__(kWideThreads) void k_gemm_wide(GemmLaunchArgs g, co
             const uint4 v = *reinterpret_cast<const uint4*>(stg + (rr < 16 ? rr : 15) * kStageRow + (lane % SLANES) * 16);
             TO* dst = (row < row_lim ? C + (row0 + row) * (int64_t)c_out : dump) + n0 + nw +
                       16 * (ch * NTC + t0) + (lane % SLANES) * (16 / (int)sizeof(TO));
-            if (rr < 16) *reinterpret_cast<uint4*>(dst) = v;
+            if (rr < 16) {
+              if (stream)
+                store_stream(dst, v);
+              else
+                *reinterpret_cast<uint4*>(dst) = v;
+            }
           }
           asm volatile("" ::: "memory");
         }
@@ -589,7 +594,7 @@ template <typename T, typename TP, int NT, int KSTEPS>
 __global__ __launch_bounds__(kCentreThreads) void k_scatter_centre(
     const T* __restrict__ x, const uint32_t* __restrict__ perm, const T* __restrict__ w, const T* __restrict__ wt,
     int kc, const TP* __restrict__ buf, const int32_t* __restrict__ omt, int64_t stride, int K3, T* y,
-    const T* residual, int relu, int n_out, int c_in, int c_out, int ldk) {
+    const T* residual, int relu, int n_out, int c_in, int c_out, int ldk, int stream) {
   using M = Mfma<T>;
   using F = typename M::frag;
   static_assert(M::KS == 32, "16-bit operands only");
@@ -818,14 +823,27 @@ __global__ __launch_bounds__(kCentreThreads) void k_scatter_centre(
         for (int d = 0; d < 4; ++d) recv[d] = swap8(send[d]);
         const int ch = ch0 + 32 * (2 * L + (lower ? 0 : 1));
         const u32x4 dx = lower ? oa : recv, dy = lower ? recv : ob;
-        if (valid_x) *reinterpret_cast<u32x4*>(y + row_x * (int64_t)c_out + ch) = dx;
-        if (valid_y) *reinterpret_cast<u32x4*>(y + row_y * (int64_t)c_out + ch) = dy;
+        T* px = y + row_x * (int64_t)c_out + ch;
+        T* py = y + row_y * (int64_t)c_out + ch;
+        if (stream) {
+          if (valid_x) store_stream(px, make_uint4(dx[0], dx[1], dx[2], dx[3]));
+          if (valid_y) store_stream(py, make_uint4(dy[0], dy[1], dy[2], dy[3]));
+        } else {
+          if (valid_x) *reinterpret_cast<u32x4*>(px) = dx;
+          if (valid_y) *reinterpret_cast<u32x4*>(py) = dy;
+        }
       }
     } else {
       if (valid) {
 #pragma unroll
-        for (int u = 0; u < NU; ++u)
-          *reinterpret_cast<u32x4*>(y + row * (int64_t)c_out + ch0 + 32 * u) = pack8((T*)nullptr, acc[2 * u], acc[2 * u + 1]);
+        for (int u = 0; u < NU; ++u) {
+          const u32x4 o = pack8((T*)nullptr, acc[2 * u], acc[2 * u + 1]);
+          T* po = y + row * (int64_t)c_out + ch0 + 32 * u;
+          if (stream)
+            store_stream(po, make_uint4(o[0], o[1], o[2], o[3]));
+          else
+            *reinterpret_cast<u32x4*>(po) = o;
+        }
       }
     }
   }
@@ -1032,7 +1050,7 @@ hipError_t wide_occupancy(const void* fn, size_t lds, int* per_cu, int* cus, int
 
 hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const int32_t* a_rows, const void* w,
                        const void* wt, void* buf_out, void* dump_row, int c_in, int c_out, int dtype, int part_dtype,
-                       int tile_rows, hipStream_t s) {
+                       int tile_rows, bool stream, hipStream_t s) {
   if (c_out % 16 != 0) return hipErrorInvalidValue;
   const bool wide = dump_row && gemm_wide(c_in, c_out, dtype, part_dtype);
   int64_t rows_all = 0;
@@ -1093,7 +1111,8 @@ hipError_t launch_gemm(const GemmSeg* segs, int n_seg, const void* buf_in, const
       void* d = dump_row;
       const void* wp = w;
       const int32_t* ar = a_rows;
-      void* args[] = {&g, &a, &ar, &wp, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile, &nsl};
+      int st = stream ? 1 : 0;
+      void* args[] = {&g, &a, &ar, &wp, &wtp, &c, &d, &c_in, &c_out, &ldk, &rows_per_tile, &nsl, &st};
       e = hipLaunchKernel(wfn, grid, dim3(kWideThreads), args, lds, s);
     } else if (dtype == 0 && part_dtype == 0)
       e = gemm_t<float, float>(g, tiles, buf_in, a_rows, w, buf_out, c_in, c_out, rows_per_tile, s);
@@ -1120,7 +1139,7 @@ bool centre_fusable(int c_in, int c_out, int dtype, int part_dtype) {
 hipError_t launch_scatter_centre(const void* x, const uint32_t* perm, const void* w, const void* wt, int kc,
                                  const void* buf_out, const int32_t* omt, int64_t mt_stride, int K3, void* y,
                                  const void* residual, int relu, int64_t n_out, int c_in, int c_out, int dtype,
-                                 int part_dtype, hipStream_t s) {
+                                 int part_dtype, bool stream, hipStream_t s) {
   if (n_out <= 0) return hipSuccess;
   const int nt = c_out / 16, ks = centre_ksteps(c_in);
   const void* fn = (c_out % 32 == 0 && ks > 0) ? centre_kernel_for(dtype, part_dtype, nt, ks) : nullptr;
@@ -1137,7 +1156,8 @@ hipError_t launch_scatter_centre(const void* x, const uint32_t* perm, const void
   const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(need, (int64_t)std::max(per_cu, 1) * std::max(cus, 1)));
   ProfScope ps(KN_SCATTER_CENTRE, s);
   int n = (int)n_out;
-  void* args[] = {&x, &perm, &w, &wt, &kc, &buf_out, &omt, &mt_stride, &K3, &y, &residual, &relu, &n, &c_in, &c_out, &ldk};
+  int st = stream ? 1 : 0;
+  void* args[] = {&x, &perm, &w, &wt, &kc, &buf_out, &omt, &mt_stride, &K3, &y, &residual, &relu, &n, &c_in, &c_out, &ldk, &st};
   e = hipLaunchKernel(fn, dim3(grid), dim3(kCentreThreads), args, lds, s);
   return e;
 }

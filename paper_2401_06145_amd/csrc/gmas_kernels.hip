@@ -81,7 +81,7 @@ template <int TILE, typename TP, typename TO>
 __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf, int64_t n_out, int c_out,
                                                       const int32_t* __restrict__ omt, int64_t stride,
                                                       const uint32_t* __restrict__ perm, int K3, TO* y,
-                                                      const TO* residual, int relu) {
+                                                      const TO* residual, int relu, int stream) {
   static_assert((TILE * sizeof(TP)) % 16 == 0, "partial tile must be whole 16-byte vectors");
   constexpr int VP = TILE * sizeof(TP) / 16;
   const int tiles = c_out / TILE;
@@ -127,10 +127,22 @@ __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf
   constexpr int BYTES = TILE * sizeof(TO);
   if constexpr (BYTES % 16 == 0) {
 #pragma unroll
-    for (int u = 0; u < BYTES / 16; ++u) reinterpret_cast<uint4*>(dst)[u] = reinterpret_cast<const uint4*>(out)[u];
+    for (int u = 0; u < BYTES / 16; ++u) {
+      const uint4 v = reinterpret_cast<const uint4*>(out)[u];
+      if (stream)
+        store_stream(reinterpret_cast<uint4*>(dst) + u, v);
+      else
+        reinterpret_cast<uint4*>(dst)[u] = v;
+    }
   } else if constexpr (BYTES % 8 == 0) {
 #pragma unroll
-    for (int u = 0; u < BYTES / 8; ++u) reinterpret_cast<uint2*>(dst)[u] = reinterpret_cast<const uint2*>(out)[u];
+    for (int u = 0; u < BYTES / 8; ++u) {
+      const uint2 v = reinterpret_cast<const uint2*>(out)[u];
+      if (stream)
+        store_stream(reinterpret_cast<uint2*>(dst) + u, v);
+      else
+        reinterpret_cast<uint2*>(dst)[u] = v;
+    }
   } else {
 #pragma unroll
     for (int c = 0; c < TILE; ++c) dst[c] = out[c];
@@ -157,7 +169,7 @@ template <typename TP, typename TO, int CH>
 __global__ __launch_bounds__(kThreads) void k_scatter_rows(const TP* __restrict__ buf, int64_t n_out, int c_out,
                                                            const int32_t* __restrict__ omt, int64_t stride,
                                                            const uint32_t* __restrict__ perm, int K3, TO* y,
-                                                           const TO* residual, int relu, int LP) {
+                                                           const TO* residual, int relu, int LP, int stream) {
   constexpr int W = 16 / (int)sizeof(TP);  // channels per 16-byte partial vector
   constexpr int WPB = kThreads / kWave;
   __shared__ int32_t s_list[WPB][kRowListWave];
@@ -239,9 +251,17 @@ __global__ __launch_bounds__(kThreads) void k_scatter_rows(const TP* __restrict_
     TO* dst = y + i * (int64_t)c_out + (int64_t)(c * LP + sub) * W;
     constexpr int BYTES = W * sizeof(TO);
     if constexpr (BYTES == 16) {
-      *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(out);
+      const uint4 v = *reinterpret_cast<const uint4*>(out);
+      if (stream)
+        store_stream(dst, v);
+      else
+        *reinterpret_cast<uint4*>(dst) = v;
     } else if constexpr (BYTES == 8) {
-      *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(out);
+      const uint2 v = *reinterpret_cast<const uint2*>(out);
+      if (stream)
+        store_stream(dst, v);
+      else
+        *reinterpret_cast<uint2*>(dst) = v;
     } else {
 #pragma unroll
       for (int e = 0; e < W; ++e) dst[e] = out[e];
@@ -264,8 +284,10 @@ int scatter_row_lanes(int c_out, int pelem, int tile) {
 
 template <typename TP, typename TO>
 hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* omt, int64_t stride,
-                     const uint32_t* perm, int K3, void* y, int tile, const void* residual, int relu, hipStream_t s) {
+                     const uint32_t* perm, int K3, void* y, int tile, const void* residual, int relu, bool stream,
+                     hipStream_t s) {
   ProfScope ps(KN_SCATTER, s);
+  const int st = stream ? 1 : 0;
   const TP* p = static_cast<const TP*>(buf);
   TO* o = static_cast<TO*>(y);
   const TO* r = static_cast<const TO*>(residual);
@@ -277,9 +299,9 @@ hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* o
     const int64_t per_block = (int64_t)(kThreads / kWave) * (kWave / lp);
     const dim3 g((unsigned)((n_out + per_block - 1) / per_block)), b(kThreads);
     switch (ch) {
-      case 1: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 1>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp); break;
-      case 2: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 2>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp); break;
-      case 4: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 4>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp); break;
+      case 1: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 1>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp, st); break;
+      case 2: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 2>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp, st); break;
+      case 4: hipLaunchKernelGGL((k_scatter_rows<TP, TO, 4>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, lp, st); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -290,7 +312,7 @@ hipError_t scatter_t(const void* buf, int64_t n_out, int c_out, const int32_t* o
 #define SPC_SC(T)                                                                                    \
   case T:                                                                                            \
     if constexpr ((T * sizeof(TP)) % 16 == 0) {                                                      \
-      hipLaunchKernelGGL((k_scatter<T, TP, TO>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu); \
+      hipLaunchKernelGGL((k_scatter<T, TP, TO>), g, b, 0, s, p, n_out, c_out, omt, stride, perm, K3, o, r, relu, st); \
       return hipGetLastError();                                                                      \
     }                                                                                                \
     return hipErrorInvalidValue;
@@ -336,11 +358,11 @@ hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const 
 
 hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out, const int32_t* omt,
                           int64_t mt_stride, const uint32_t* perm, int K3, void* y, int dtype, int tile,
-                          const void* residual, int relu, hipStream_t s) {
+                          const void* residual, int relu, bool stream, hipStream_t s) {
   if (n_out <= 0) return hipSuccess;
   if (tile <= 0 || c_out % tile != 0) return hipErrorInvalidValue;
   // part_dtype / dtype: 0 = f32, 1 = f16, 2 = bf16
-#define SPC_S(TP, TO) scatter_t<TP, TO>(buf_out, n_out, c_out, omt, mt_stride, perm, K3, y, tile, residual, relu, s)
+#define SPC_S(TP, TO) scatter_t<TP, TO>(buf_out, n_out, c_out, omt, mt_stride, perm, K3, y, tile, residual, relu, stream, s)
   if (part_dtype == 0) {
     if (dtype == 0) return SPC_S(float, float);
     if (dtype == 1) return SPC_S(float, __half);

@@ -1290,8 +1290,8 @@ __global__ __launch_bounds__(TH) void k_forward_count(SearchArgs a, const uint32
       u_hi = nhi;
       mx = nmx;
     }
-    for (int q0 = u_lo; q0 < u_hi; q0 += a.Cq) {
-      const int q1 = min(q0 + a.Cq, u_hi);
+    for (int64_t q0w = u_lo; q0w < u_hi; q0w += a.Cq) {  // (64-bit: q0 + Cq may pass 2^31)
+      const int q0 = (int)q0w, q1 = (int)min(q0w + a.Cq, (int64_t)u_hi);
       if (q0 != pre_lo) load_keys(q0, q1);
       pre_lo = -1;
       for (int jj = j; jj < je; ++jj) {

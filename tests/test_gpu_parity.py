@@ -532,12 +532,22 @@ def test_larger_cloud_one_kernel_sort_passes_with_larger_tiles():
     assert_map_equal(km, okm)
 
 
+def test_mid_cloud_summed_sort_offsets():
+    """0.7M voxels: 342 radix tiles of 2048 keys, whose offsets every scatter
+    workgroup sums from the tile histograms itself (more than the 256 tiles of the
+    1024-key sorts)."""
+    say("mid-size uniform cloud, 0.7M voxels")
+    c = scenes.uniform_cells(700_000, 400, 4341)
+    km = B.KernelMap.build(to_dev(c), 3)
+    assert_map_equal(km, oracle.kernel_map(c, None, 3, 1, "subm"))
+
+
 def test_mid_cloud_scanned_sort_offsets():
-    """1M voxels: 489 radix tiles, between the per-workgroup offset sums and the
+    """1.3M voxels: 635 radix tiles, between the per-workgroup offset sums and the
     one-kernel passes, so each pass scans the digit-major histograms on the device.
-    Also about 50k forward-search work items; features checked on sampled rows."""
-    say("mid-size uniform cloud, 1M voxels")
-    c = scenes.uniform_cells(1_000_000, 400, 4343)
+    Also about 65k forward-search work items; features checked on sampled rows."""
+    say("mid-size uniform cloud, 1.3M voxels")
+    c = scenes.uniform_cells(1_300_000, 400, 4343)
     x = scenes.features(len(c), 16, "f16", 4344)
     w = scenes.weights(3, 16, 16, "f16", 4345)
     km, y = _conv_gpu(c, x, w, 3, dtype="f16")

@@ -211,11 +211,12 @@ __global__ __launch_bounds__(kThreads) void k_pack(const int4* c, int64_t n, con
 // there, so that consecutive threads write consecutive addresses of a digit's
 // run.
 // ----------------------------------------------------------------------------
-constexpr int kRsItems = 8;                   // keys per thread of a one-kernel pass
-// and from kOnesweepMinTiles tiles of that many keys per thread on (4.2M keys): longer
-// runs per digit and tile for the stores (16M keys: pass 193 -> 166 us)
+constexpr int kRsItems = 8;                   // keys per thread of the tiled sort's larger tiles
+// keys per thread of a one-kernel pass: long runs per digit and tile for the stores
+// (16M keys: pass 193 -> 166 us against 8 keys per thread)
 constexpr int kRsItemsLarge = 16;
 constexpr int kRsTile = kThreads * kRsItems;
+constexpr int kRsTileLarge = kThreads * kRsItemsLarge;
 constexpr int kRsItemsSmall = 4;              // keys per thread of the small sorts' passes
 constexpr int kRsTileSmall = kThreads * kRsItemsSmall;
 constexpr int kRsUpBlocks = 512;
@@ -1549,7 +1550,11 @@ hipError_t launch_pack(const int32_t* coords, int64_t n, const KeyLayout* L, uin
 }
 
 // One-kernel passes need many more tiles than workgroups that run at once, so
-// that most look-backs stop at a finished predecessor.
+// that most look-backs stop at a finished predecessor: they serve from this many
+// tiles of kRsTileLarge keys (4.2M keys) on.  Below, the tiled sort with its
+// scanned offsets was faster (LiDAR keys: 0.257 -> 0.231 ms at 2.5M, 0.342 ->
+// 0.313 ms at 4.07M, against one-kernel passes of 2048-key tiles); above, the
+// one-kernel passes win (0.386 against 0.417 ms at 6M keys).
 constexpr int64_t kOnesweepMinTiles = 1024;
 
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
@@ -1697,7 +1702,7 @@ bool radix_bucket_applies(int64_t n) { return n > 1 && (n + kRsTileSmall - 1) / 
 bool radix_fuses_layout(int64_t n, int passes, bool by_bucket) {
   if (by_bucket && radix_bucket_applies(n)) return true;
   return n > 1 && passes > 0 && passes <= kRsMaxPasses && n < ((int64_t)1 << 30) &&
-         (n + kRsTile - 1) / kRsTile < kOnesweepMinTiles;
+         (n + kRsTileLarge - 1) / kRsTileLarge < kOnesweepMinTiles;
 }
 
 hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* keys, uint32_t* vals, uint64_t* keys_alt,
@@ -1716,13 +1721,11 @@ hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* ke
   if (coords && (passes == 0 || n == 1)) return launch_pack(coords, n, L, keys, vals, s);
   if (n <= 1 || passes == 0) return hipSuccess;
   if (passes > kRsMaxPasses || n >= ((int64_t)1 << 30)) return hipErrorInvalidValue;
-  if ((n + kRsTile - 1) / kRsTile < kOnesweepMinTiles)
+  if ((n + kRsTileLarge - 1) / kRsTileLarge < kOnesweepMinTiles)
     return radix_sort_tiled(coords, L, keys, vals, keys_alt, vals_alt, n, passes, d_temp, la, s);
-  // one kernel per pass, with larger tiles from kOnesweepMinTiles of them on (the
-  // status words are sized for tiles of kRsTile keys, of which there are more)
-  const bool large = (n + kThreads * kRsItemsLarge - 1) / (kThreads * kRsItemsLarge) >= kOnesweepMinTiles;
-  const int64_t tile_keys = (int64_t)kThreads * (large ? kRsItemsLarge : kRsItems);
-  const int64_t ntiles = (n + tile_keys - 1) / tile_keys;
+  // one kernel per pass (the status words are sized for tiles of kRsTile keys, of
+  // which there are more)
+  const int64_t ntiles = (n + kRsTileLarge - 1) / kRsTileLarge;
   const size_t gpart_bytes = (size_t)kRsUpBlocks * kRsMaxPasses * 256 * sizeof(uint32_t);
   uint32_t* gpart = static_cast<uint32_t*>(d_temp);
   uint32_t* gofs = reinterpret_cast<uint32_t*>(static_cast<char*>(d_temp) + align256(gpart_bytes));
@@ -1767,18 +1770,12 @@ hipError_t radix_sort_kv(const int32_t* coords, const KeyLayout* L, uint64_t* ke
     const int src = cur, dst = (first ? ((passes % 2 == 1) ? 0 : 1) : cur ^ 1);
     {
       ProfScope ps(KN_RADIX_SCATTER, s);
-      if (first && large)
+      if (first)
         hipLaunchKernelGGL((k_radix_pass<true, kRsItemsLarge>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr,
                            nullptr, c4, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
-      else if (first)
-        hipLaunchKernelGGL((k_radix_pass<true, kRsItems>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, nullptr,
-                           nullptr, c4, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
-      else if (large)
+      else
         hipLaunchKernelGGL((k_radix_pass<false, kRsItemsLarge>), dim3((unsigned)ntiles), dim3(kThreads), 0, s,
                            kb[src], vb[src], nullptr, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
-      else
-        hipLaunchKernelGGL((k_radix_pass<false, kRsItems>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, kb[src],
-                           vb[src], nullptr, L, kb[dst], vb[dst], n, p, gofs, status, tickets, err);
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

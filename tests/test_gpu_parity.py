@@ -509,9 +509,10 @@ def test_padding_lanes_feed_exact_zeros(c_in):
         assert rel_err(got, ref) <= TOL["f16"]
 
 
-def test_large_cloud_one_kernel_sort_passes():
-    """2.4M voxels: more than 1024 radix tiles, so the sort runs one kernel per pass
-    (tile ranks + look-back); K = 2 keeps the oracle's map fast."""
+def test_large_cloud_scanned_sort_many_tiles():
+    """2.4M voxels: 1172 radix tiles of 2048 keys, below the one-kernel passes (from
+    4.2M keys), so each pass scans the digit-major histograms on the device; also
+    the DOWN map's output sort.  K = 2 keeps the oracle's map fast."""
     say("large uniform cloud, 2.4M voxels")
     c = scenes.uniform_cells(2_400_000, 400, 4242)
     km = B.KernelMap.build(to_dev(c), 2)
@@ -523,8 +524,9 @@ def test_large_cloud_one_kernel_sort_passes():
 
 
 def test_larger_cloud_one_kernel_sort_passes_with_larger_tiles():
-    """4.5M voxels: past 1024 tiles of 4096 keys, so the one-kernel passes take 16
-    keys per thread; K = 2 keeps the oracle's map fast."""
+    """4.5M voxels: past 1024 tiles of 4096 keys, so the sort runs one kernel per
+    pass (tile ranks + look-back) with 16 keys per thread; K = 2 keeps the oracle's
+    map fast."""
     say("large uniform cloud, 4.5M voxels")
     c = scenes.uniform_cells_large(4_500_000, 480, 4343)
     km = B.KernelMap.build(to_dev(c), 2)

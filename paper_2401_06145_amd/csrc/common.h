@@ -194,6 +194,7 @@ struct SearchArgs {
   int64_t pair_cap;       // capacity of the pair lists (K3 * queries)
   int wg;                 // threads per workgroup of the count and write passes (0: 256)
   int count_group;        // offsets per count-pass workgroup, at most 64 (0: size rule)
+  int stream_tq;          // the count pass stores T_q with non-temporal stores
   // Submanifold map with odd K (offset k and K^3 - 1 - k are mirror images).
   int sym;
   // 0: the write pass leaves T_s alone (a symmetric map's T_s is filled from the

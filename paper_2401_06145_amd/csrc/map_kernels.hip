@@ -1320,7 +1320,13 @@ __global__ __launch_bounds__(TH) void k_forward_count(SearchArgs a, const uint32
         for (int r = 0; r < ROUNDS; ++r) {
           const int e = r * TH + tid;
           const bool valid = e >= r_lo && e < r_hi;
-          if (valid) res[e] = hit[r] ? (int32_t)(s0 + pos[r]) : -1;
+          if (valid) {
+            const int32_t v = hit[r] ? (int32_t)(s0 + pos[r]) : -1;
+            if (a.stream_tq)
+              __builtin_nontemporal_store(v, res + e);
+            else
+              res[e] = v;
+          }
           nh += (uint32_t)popc64(__ballot(valid && hit[r]));
         }
         if (lane == jj) tot += nh;

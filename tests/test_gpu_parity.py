@@ -523,6 +523,15 @@ def test_large_cloud_scanned_sort_many_tiles():
     assert np.array_equal(qd.out_coords().cpu().numpy(), q)
 
 
+def test_large_query_table_streamed():
+    """2.6M voxels at K = 3: the per-(offset, query) table holds 281 MB, past the
+    size from which the count pass writes it with non-temporal stores."""
+    say("large uniform cloud, 2.6M voxels, K=3")
+    c = scenes.uniform_cells(2_600_000, 400, 4250)
+    km = B.KernelMap.build(to_dev(c), 3)
+    assert_map_equal(km, oracle.kernel_map(c, None, 3, 1, "subm"))
+
+
 def test_larger_cloud_one_kernel_sort_passes_with_larger_tiles():
     """4.5M voxels: past 1024 tiles of 4096 keys, so the sort runs one kernel per
     pass (tile ranks + look-back) with 16 keys per thread; K = 2 keeps the oracle's

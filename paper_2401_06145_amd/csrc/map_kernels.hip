@@ -926,6 +926,78 @@ __global__ __launch_bounds__(kThreads) void k_down_keys(const uint64_t* skeys, i
   vals[i] = (uint32_t)i;
 }
 
+// Unique keys of a sorted array in two launches, for up to kUniqueTiles tiles of
+// kUniqueTile keys: per-tile counts of first occurrences, then every tile adds up
+// the counts of the tiles before it, ranks its own first occurrences with a
+// workgroup scan and writes them.  Thread t of a tile holds its keys
+// 8 t .. 8 t + 7.  Larger arrays go through a device scan of per-key flags.
+constexpr int kUniqueItems = 8;
+constexpr int kUniqueTile = kThreads * kUniqueItems;
+constexpr int64_t kUniqueTiles = 1024;
+
+// this thread's first occurrences among its keys (f), their keys (k) and count
+__device__ __forceinline__ uint32_t unique_items(const uint64_t* keys, int64_t n, uint64_t (&k)[kUniqueItems],
+                                                 bool (&f)[kUniqueItems]) {
+  const int64_t i0 = (int64_t)blockIdx.x * kUniqueTile + (int64_t)threadIdx.x * kUniqueItems;
+  uint64_t prev = (i0 > 0 && i0 - 1 < n) ? keys[i0 - 1] : 0;
+  uint32_t c = 0;
+#pragma unroll
+  for (int r = 0; r < kUniqueItems; ++r) {
+    const int64_t i = i0 + r;
+    k[r] = (i < n) ? keys[i] : 0;
+    f[r] = i < n && (i == 0 || k[r] != prev);
+    prev = k[r];
+    c += f[r] ? 1u : 0u;
+  }
+  return c;
+}
+
+// sum of one value per thread over the 256-thread block, in every thread
+__device__ __forceinline__ uint32_t block_sum256(uint32_t v, uint32_t* s_wave) {
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) v += __shfl_xor(v, d, kWave);
+  if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
+  __syncthreads();
+  uint32_t t = 0;
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) t += s_wave[w];
+  __syncthreads();  // s_wave may be reused
+  return t;
+}
+
+__global__ __launch_bounds__(kThreads) void k_unique_tile_count(const uint64_t* keys, int64_t n, uint32_t* cnt) {
+  __shared__ uint32_t s_wave[kWavesPerBlock];
+  uint64_t k[kUniqueItems];
+  bool f[kUniqueItems];
+  const uint32_t t = block_sum256(unique_items(keys, n, k, f), s_wave);
+  if (threadIdx.x == 0) cnt[blockIdx.x] = t;
+}
+
+__global__ __launch_bounds__(kThreads) void k_unique_tile_write(const uint64_t* keys, int64_t n,
+                                                                const KeyLayout* __restrict__ Lp, const uint32_t* cnt,
+                                                                uint64_t* qkeys, uint32_t* qrow, int4* coords,
+                                                                uint32_t* n_unique) {
+  __shared__ uint32_t s_wave[kWavesPerBlock];
+  const KeyLayout L = *Lp;
+  uint64_t k[kUniqueItems];
+  bool f[kUniqueItems];
+  const uint32_t c = unique_items(keys, n, k, f);
+  uint32_t part = 0;
+  for (int j = threadIdx.x; j < (int)blockIdx.x; j += kThreads) part += cnt[j];
+  const uint32_t base = block_sum256(part, s_wave);
+  uint32_t p = base + block_excl256(c, s_wave);
+#pragma unroll
+  for (int r = 0; r < kUniqueItems; ++r) {
+    if (!f[r]) continue;
+    qkeys[p] = k[r];
+    qrow[p] = p;
+    coords[p] = make_int4(key_field(L, k[r], 0), key_field(L, k[r], 1), key_field(L, k[r], 2), key_field(L, k[r], 3));
+    ++p;
+  }
+  // the last thread of the last tile ends at the total
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == kThreads - 1) *n_unique = p;
+}
+
 __global__ __launch_bounds__(kThreads) void k_unique_flags(const uint64_t* keys, int64_t n, uint32_t* flags) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
@@ -1802,6 +1874,16 @@ hipError_t unique_keys(const uint64_t* keys, int64_t n, const KeyLayout* L, uint
                        uint64_t* qkeys, uint32_t* qrow, int32_t* out_coords, ControlBlock* cb, hipStream_t s) {
   if (n <= 0) return launch_fill_u32(&cb->n_q, 0u, 1, s);
   ProfScope ps(KN_UNIQUE, s);
+  const int64_t ntiles = (n + kUniqueTile - 1) / kUniqueTile;
+  if (ntiles <= kUniqueTiles) {
+    // (the per-key flags' buffer holds the tile counts: n >= ntiles)
+    hipLaunchKernelGGL(k_unique_tile_count, dim3((unsigned)ntiles), dim3(kThreads), 0, s, keys, n, flags);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_unique_tile_write, dim3((unsigned)ntiles), dim3(kThreads), 0, s, keys, n, L, flags, qkeys,
+                       qrow, reinterpret_cast<int4*>(out_coords), &cb->n_q);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_unique_flags, dim3(grid_for(n)), dim3(kThreads), 0, s, keys, n, flags);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

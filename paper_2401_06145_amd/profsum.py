@@ -55,7 +55,7 @@ FOLD = [
     (r"k_tile_(scan|reduce)\b", "k_scan"),
     (r"k_minmax_(partial|final)\b|k_layout\b", "k_minmax"),
     (r"k_scatter(_rows)?\b", "k_scatter"),
-    (r"k_unique_(flags|write)\b", "k_unique"),
+    (r"k_unique_(flags|write|tile_count|tile_write)\b", "k_unique"),
     (r"k_fill_u32\b", "k_fill"),
 ]
 

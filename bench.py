@@ -269,6 +269,20 @@ class LayerBench:
         B.spconv_profile_enable(False)
         return B.spconv_profile_read(reset=True)
 
+    def layer_ms(self, R=20, **variant):
+        """Whole steps (Map build + forward) of a variant, no events: ms per step."""
+        import torch
+
+        fopt, ws = self.variant(**variant)
+        for _ in range(3):
+            self.step(fopt, ws)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(R):
+            self.step(fopt, ws)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / R
+
     def phases(self, R=10, **variant):
         prof = self.timed_pass(self.B.PHASES_ALL, R, **variant)
         return {k: v[0] / R for k, v in prof.items() if not k.startswith("k_") and v[1] > 0}
@@ -420,21 +434,24 @@ def main():
         out["counters"] = counters
 
     if not args.no_extras:
-        # the same layer with the other GMaS variants (phase events, untimed breakdown pass)
-        def gmas_of(ph):
+        # the same layer with the other GMaS variants: phase events (a breakdown pass), and
+        # whole steps without events beside the default's, timed back to back (phase sums
+        # of two variants can rank them differently from their whole steps)
+        def gmas_of(ph, **variant):
             return {**{p: round(ph.get(p, 0.0), 5) for p in GMAS_PHASES},
-                    "total": round(sum(ph.get(p, 0.0) for p in GMAS_PHASES), 5)}
+                    "total": round(sum(ph.get(p, 0.0) for p in GMAS_PHASES), 5),
+                    "layer_ms": round(lb.layer_ms(**variant), 5), "default_layer_ms": round(lb.layer_ms(), 5)}
 
         B = lb.B
         other_p = 1 if lb.partial_dtype == 2 else 2
         out["gmas_ms_other_partials"] = {"gemm_partials": "f32" if other_p == 1 else L.dtype,
-                                         **gmas_of(lb.phases(partial_dtype=other_p))}
+                                         **gmas_of(lb.phases(partial_dtype=other_p), partial_dtype=other_p)}
         other_g = B.GATHER_BUFFER if lb.fused else B.GATHER_FUSED
         out["gmas_ms_other_gather"] = {"gather": "buffer" if lb.fused else "fused",
-                                       **gmas_of(lb.phases(gather=other_g))}
+                                       **gmas_of(lb.phases(gather=other_g), gather=other_g)}
         if lb.plan.centre:
             # the centre offset through the GEMM and its partial buffer, like the other offsets
-            out["gmas_ms_centre_through_gemm"] = gmas_of(lb.phases(centre=1))
+            out["gmas_ms_centre_through_gemm"] = gmas_of(lb.phases(centre=1), centre=1)
     lb_cpu = (lb.coords_np, lb.x_np, lb.w_np, L)
     lb.close()
     del lb

@@ -1096,6 +1096,10 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
 // order, and o, the pair's GEMM buffer row, is also stored in both metadata
 // tables (T_q in place of the source position, T_s at the source position).
 // ----------------------------------------------------------------------------
+// a value that every lane of the wave holds alike (say, read from LDS), in a
+// scalar register, so that loops and branches on it stay scalar
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 // Sorted position of ROUNDS independent keys at once in the LDS block, by binary
 // lifting: the block holds 2^LOG2B + 1 keys, padded past its nB real keys with
 // the largest key (never smaller than a query), so no step needs a bounds check.
@@ -1104,10 +1108,6 @@ __global__ __launch_bounds__(kThreads) void k_backward(SearchArgs a, int64_t nb,
 // ROUNDS reads of a step are issued together.  pos = number of keys < key (at
 // most 2^LOG2B - 1; then the final probe tells a hit from a key past the block),
 // hit = whether the key is present.
-// a value that every lane of the wave holds alike (say, read from LDS), in a
-// scalar register, so that loops and branches on it stay scalar
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
-
 template <int ROUNDS, int LOG2B>
 __device__ __forceinline__ void lds_search(const uint64_t* lkey, const uint64_t (&key)[ROUNDS], int (&pos)[ROUNDS],
                                            bool (&hit)[ROUNDS]) {

@@ -392,6 +392,16 @@ def main():
     roof = roofline_for(dominant, models, mean_launch_ms, L, lb.wl.name)
     roof.update({"mean_launch_ms": round(mean_launch_ms, 6), "launches_per_step": launches_per_step,
                  "timed_launches": timed_launches, "event_steps": f"1 in {EVENT_EVERY} timed steps"})
+    # the kernel with the next most time per step (at C = 256 the GEMM and the centre
+    # scatter take about the same), priced the same way from the breakdown pass
+    ranked = sorted((k for k in kern if k in models or k == "k_gemm"), key=lambda k: -kern[k][0])
+    roof_next = None
+    if len(ranked) > 1:
+        second = ranked[1] if ranked[0] == dominant else ranked[0]
+        ms2, cnt2 = kern[second]
+        roof_next = roofline_for(second, models, ms2 / cnt2, L, lb.wl.name)
+        roof_next.update({"mean_launch_ms": round(ms2 / cnt2, 6), "launches_per_step": cnt2,
+                          "event_steps": "breakdown pass, events around this kernel only"})
 
     map_ms = sum(ph_ms.get(p, 0.0) for p in MAP_PHASES)
     gmas_ms = sum(ph_ms.get(p, 0.0) for p in GMAS_PHASES)
@@ -428,6 +438,7 @@ def main():
         "gemm_launches": lb.plan.n_gemm_launches,
         "gather": args.gather,
         "roofline": roof,
+        "roofline_next": roof_next,
     }
     counters = measured_counters(lb.wl.name)
     if counters:

@@ -116,10 +116,11 @@ typedef struct {
                         SPCONV_EUNSUPPORTED where it does not apply.  The sums differ from the
                         unfused path only in rounding (the centre's product is not rounded to the
                         partial type) */
-  int count_group;   /* spconv_build_map, sorted search: offsets per workgroup of the forward
-                        search's count pass, which stages a source block once for all of them
-                        (1 to 64, at most K^3); 0 = default, sized so that the pass has about 4k
-                        workgroups.  Changes only the launch shape: the same map */
+  int count_group;   /* spconv_build_map, sorted search (Section 5.1.2): offsets per workgroup
+                        of the forward search's count pass, which stages a source block once for
+                        all of them; 1 to 64 (more than K^3 acts as K^3, SPCONV_EINVAL outside
+                        [0, 64]); 0 = default, sized so that the pass has about 4k workgroups.
+                        Changes only the launch shape: the same map */
   int reserved[2];
 } spconv_options;
 

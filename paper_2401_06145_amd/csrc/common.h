@@ -244,7 +244,8 @@ hipError_t launch_gather(const void* x, int64_t n_in, int c_in, int elem, const 
                          hipStream_t s);
 // Scatter: y[perm[p]] = sum_k buf_out[omt[k][p]] (float32 sum, k ascending), tile T
 // channels per thread.  Optional epilogue: y = relu?(sum + residual) (residual NULL: none).
-// stream: the output rows go out with non-temporal stores (store_stream).
+// stream: the row-group kernel's output rows go out with non-temporal stores
+// (store_stream); the one-thread-per-tile kernel always stores plainly.
 hipError_t launch_scatter(const void* buf_out, int part_dtype, int64_t n_out, int c_out,
                           const int32_t* omt, int64_t mt_stride, const uint32_t* perm, int K3, void* y,
                           int dtype, int tile, const void* residual, int relu, bool stream, hipStream_t s);

@@ -57,6 +57,7 @@ FOLD = [
     (r"k_scatter(_rows)?\b", "k_scatter"),
     (r"k_unique_(flags|write|tile_count|tile_write)\b", "k_unique"),
     (r"k_fill_u32\b", "k_fill"),
+    (r"k_transpose_w(64)?\b", "k_transpose_w"),
 ]
 
 

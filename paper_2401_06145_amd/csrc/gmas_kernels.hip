@@ -80,7 +80,7 @@ __device__ __forceinline__ __hip_bfloat16 from_f32<__hip_bfloat16>(float v) { re
 // stores are plain: a store instruction leaves each line partly written (the
 // lanes' tiles are TILE channels apart) and the next ones complete it, which
 // L2 merges; as non-temporal stores the wide tiles ran at half speed (C = 256,
-// 300k outputs: T = 32 from 169 to 283 us).
+// 300k outputs: T = 32 from 162 to 283 us).
 template <int TILE, typename TP, typename TO>
 __global__ __launch_bounds__(kThreads) void k_scatter(const TP* __restrict__ buf, int64_t n_out, int c_out,
                                                       const int32_t* __restrict__ omt, int64_t stride,
